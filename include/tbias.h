@@ -1,0 +1,229 @@
+/*
+ * tbias.h — C ABI of the MI355X boosted-decode library (libtbias.so).
+ *
+ * Per-stream phrase boosting fused into batched Transducer greedy and beam
+ * decoding, after TurboBias 2.0 (Sec. II). Every stream carries a boosting
+ * model id (Sec. II-B; -1 = no biasing) and a graph state; one decoding step
+ * adds the boosting score of every vocabulary token to the stream's joint
+ * logits, normalises (log-softmax), selects (argmax or top-K) and advances the
+ * graph state, which is carried across streaming calls (Sec. II-C).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every function returns an int status: TB_OK (0) or a negative TB_E* code.
+ *   tb_last_error() returns a thread-local message for the last failure.
+ * - Argument checks are synchronous and happen before any launch: a call that
+ *   returns an error has enqueued nothing.
+ * - "device" pointers are HIP device memory owned by the caller (the library
+ *   never allocates device memory); "host" pointers are ordinary host memory.
+ *   Kernels run asynchronously on the given HIP stream (NULL = the default
+ *   stream); outputs are valid once that stream has reached the call.
+ * - The vocabulary has V non-blank tokens with ids 0..V-1 and the blank with
+ *   id V (the last logit column); v_plus_blank = V + 1.
+ * - Graph states are model-local breadth-first ids (root = 0); -1 means "no
+ *   model". A carried state or model id that is out of range for the arena is
+ *   never dereferenced: that stream is decoded without biasing and its output
+ *   states are written as TB_STATE_INVALID (-2).
+ */
+#ifndef TBIAS_H
+#define TBIAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  TB_OK = 0,
+  TB_EINVAL = -1, /* bad argument (null/misaligned pointer, bad size or flag) */
+  TB_ENOMEM = -2, /* host allocation failed, or a caller buffer is too small */
+  TB_EHIP = -3,   /* a HIP runtime call or kernel launch failed */
+  TB_ERANGE = -4  /* data out of range (token >= V, blank in a phrase, ...) */
+};
+
+enum { TB_F32 = 0, TB_BF16 = 1 };                     /* logit element type */
+enum { TB_COMMIT = 0, TB_PURE_POTENTIAL = 1 };        /* potential reading   */
+enum { TB_STATE_NONE = -1, TB_STATE_INVALID = -2 };
+
+/* Host-side compiled graphs of all models (library owned). */
+typedef struct tb_graphs tb_graphs;
+
+/*
+ * Layout of the device arena image: one contiguous byte buffer holding the
+ * merged multi-model storage of Sec. II-B (all models' state tensors
+ * concatenated, a per-model table of offsets, and per-model root rows).
+ * All offsets are in bytes from the start of the buffer, 256-byte aligned.
+ *
+ *   model_off   int32[n_models]   first global state index of each model
+ *   model_n     int32[n_models]   number of states of each model
+ *   first_child int32[n_states]   local id of the first child (children are
+ *                                 contiguous ids, labels strictly ascending)
+ *   n_child     int32[n_states]   number of children
+ *   link        int32[n_states]   suffix-link target, local id (< own id)
+ *   label       int32[n_states]   class of the arc into the state (root: -1)
+ *   phi         float[n_states]   potential phi (pending score)
+ *   psi         float[n_states]   phi + end bonus E: a step into state x from
+ *                                 state s scores psi[x] - phi[s]
+ *   root_psi    float[n_models*(V+1)]  psi of the root move of every token
+ *                                      (blank column: 0)
+ *   root_dst    int32[n_models*(V+1)]  local state of the root move of every
+ *                                      token (blank column: 0)
+ *   class_map   int32[V+1]        token -> case class (blank: -1)
+ *   cls_ptr     int32[V+1]        CSR over classes: members of class c are
+ *   cls_tok     int32[V]          cls_tok[cls_ptr[c] .. cls_ptr[c+1]-1], ascending
+ */
+typedef struct {
+  int64_t total_bytes;
+  int32_t n_models;
+  int32_t v_plus_blank;
+  int64_t n_states; /* sum over models */
+  int64_t off_model_off, off_model_n;
+  int64_t off_first_child, off_n_child, off_link, off_label, off_phi, off_psi;
+  int64_t off_root_psi, off_root_dst;
+  int64_t off_class_map, off_cls_ptr, off_cls_tok;
+  int32_t max_children;  /* largest out-degree of any state */
+  int32_t max_depth;     /* deepest state (phrase length) */
+} tb_arena_layout;
+
+/* A device-resident arena: the layout plus the device address of the image. */
+typedef struct {
+  const void* base; /* device pointer to tb_arena_layout.total_bytes bytes */
+  tb_arena_layout layout;
+} tb_arena;
+
+/*
+ * tb_compile_graphs — compile per-stream phrase lists into merged storage
+ * (Sec. II-B "per-stream context-biasing model"; case-insensitive graph of
+ * Sec. II-A: every token is replaced by its case class, so one arc accepts
+ * every case variant).
+ *
+ *   n_models          number of phrase lists (models), >= 1
+ *   model_phrase_ptr  host int64[n_models+1], CSR over phrases
+ *   phrase_tok_ptr    host int64[n_phrases+1], CSR over tokens
+ *   phrase_tokens     host int32[phrase_tok_ptr[n_phrases]]; ids in [0, V)
+ *   token_w           host float[n_models], score per matched token (w)
+ *   end_bonus         host float[n_models], end-of-phrase bonus
+ *   scale             host float[n_models] or NULL (= 1): the per-model
+ *                     boosting weight, folded into phi and psi
+ *   class_map         host int32[v_plus_blank]; class of every token (a token
+ *                     id in [0, V)), class_map[V] must be -1
+ *   semantics         TB_COMMIT (default reading) or TB_PURE_POTENTIAL
+ *   n_threads         host threads to use (<= 0: hardware concurrency)
+ *   out               receives the library-owned result; free with
+ *                     tb_graphs_free
+ *
+ * An empty list gives a root-only graph (state 0, zero boost). Duplicate
+ * phrases (after case folding) are merged. Errors: TB_EINVAL (null pointers,
+ * non-monotone CSR), TB_ERANGE (token outside [0, V), a token whose class is
+ * -1, an empty phrase, a class id outside [0, V)), TB_ENOMEM.
+ */
+int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_ptr,
+                      const int64_t* phrase_tok_ptr, const int32_t* phrase_tokens,
+                      const float* token_w, const float* end_bonus, const float* scale,
+                      const int32_t* class_map, int32_t v_plus_blank, int32_t semantics,
+                      int32_t n_threads, tb_graphs** out);
+
+/* Layout (sizes and offsets) of the arena image of g. */
+int tb_graphs_layout(const tb_graphs* g, tb_arena_layout* out);
+
+/* Copy the arena image into host memory dst (bytes >= layout.total_bytes). */
+int tb_graphs_host_image(const tb_graphs* g, void* dst, int64_t bytes);
+
+/*
+ * Copy the arena image into caller-owned device memory dev_base (bytes >=
+ * layout.total_bytes, 256-byte aligned) on stream and fill *out. Returns once
+ * the copy has completed (the host graphs may be freed afterwards).
+ */
+int tb_graphs_upload(const tb_graphs* g, void* dev_base, int64_t bytes, void* hip_stream,
+                     tb_arena* out);
+
+void tb_graphs_free(tb_graphs* g);
+
+/*
+ * Check a host copy of an arena image for consistency (every index in range,
+ * suffix links pointing to smaller ids, children contiguous with ascending
+ * labels, root rows consistent with the root's children). TB_OK or TB_ERANGE.
+ */
+int tb_validate_image(const void* host_image, const tb_arena_layout* layout);
+
+/*
+ * tb_init_states — start B streams (Sec. II-B: each stream carries a model id
+ * and a state; Sec. II-C: beam scores are carried across chunks).
+ *
+ *   model_ids  device int32[B]
+ *   states     device int32[B*K] out: 0 for a model in range, -1 for -1,
+ *              TB_STATE_INVALID for an out-of-range id
+ *   scores     device float[B*K] out, or NULL: beam scores [0, -inf, ...]
+ */
+int tb_init_states(const tb_arena* a, int32_t B, int32_t K, const int32_t* model_ids,
+                   int32_t* states, float* scores, void* hip_stream);
+
+/*
+ * tb_boost_step_greedy — T boosted greedy steps for B streams (Sec. II-B
+ * fused scoring operation, with label selection of greedy Transducer
+ * decoding). For step t and stream b with state s and row z = logits[t,b,:]:
+ *
+ *   key[v] = z[v] + psi[delta(s, class v)]   (v < V; delta = suffix-link move)
+ *   key[V] = z[V] + phi[s]                   (blank keeps the state)
+ *   v*     = lowest index of the largest key
+ *   score  = (z[v*] - lse(z)) + (psi[delta] - phi[s])   (0 boost for blank)
+ *
+ *   logits     device, element type dtype, row (t,b) at (t*B + b)*row_stride
+ *              elements; row_stride >= V+1; 4-byte (f32) / 2-byte (bf16) aligned
+ *   model_ids  device int32[B]
+ *   states     device int32[B], in: carried state, out: state after step T-1
+ *   out_tok, out_state  device int32[T*B];  out_score device float[T*B]
+ *
+ * T = 0 is a no-op that touches no buffer (logits and outputs may be NULL).
+ * Results do not depend on how the T steps are split into calls. Log-softmax here is float32 (|error| well below 1e-5); selection
+ * does not depend on it.
+ */
+int tb_boost_step_greedy(const tb_arena* a, const void* logits, int32_t dtype, int32_t T,
+                         int32_t B, int64_t row_stride, const int32_t* model_ids,
+                         int32_t* states, int32_t* out_tok, int32_t* out_state,
+                         float* out_score, void* hip_stream);
+
+/*
+ * tb_boost_step_beam — T boosted beam steps for B streams of K hypotheses
+ * (Sec. II-C streaming beam search; K <= TB_MAX_BEAM). Hypothesis k of
+ * stream b reads row logits[t,b,k,:] (row index (t*B + b)*K + k) and has
+ * state s_k and accumulated score S_k:
+ *
+ *   lse_k   = log-sum-exp of the row, float64 sum and log, rounded to float32
+ *   c_k     = (S_k - lse_k) - phi[s_k]
+ *   cand    = c_k + key_k[v]          (key as in the greedy step)
+ *   the K largest cand over flat index k*(V+1)+v are kept, sorted descending,
+ *   ties to the lowest flat index; slot j takes parent k_j, token v_j, state
+ *   delta(s_{k_j}, class v_j) (blank: s_{k_j}) and S_j = cand_j.
+ *
+ *   states, scores  device [B*K] in/out (carry)
+ *   out_tok, out_parent, out_state  device int32[T*B*K]
+ *   out_step (the step's log-prob plus boost), out_cum (S)  device float[T*B*K]
+ *
+ * T = 0 is a no-op that touches no buffer (they may be NULL).
+ */
+enum { TB_MAX_BEAM = 16 };
+int tb_boost_step_beam(const tb_arena* a, const void* logits, int32_t dtype, int32_t T,
+                       int32_t B, int32_t K, int64_t row_stride, const int32_t* model_ids,
+                       int32_t* states, float* scores, int32_t* out_tok, int32_t* out_parent,
+                       int32_t* out_state, float* out_step, float* out_cum, void* hip_stream);
+
+/*
+ * tb_reset_stream — give stream b (0 <= b < B) a new model id (Sec. II-B:
+ * lists are added and removed as streams start and finish) and restart its
+ * carry: model id new_model_id in [-1, n_models), states 0 (or -1), scores
+ * [0, -inf, ...] (scores may be NULL). model_ids is device int32[B], states
+ * and scores device [B*K]. Only stream b's entries are written.
+ */
+int tb_reset_stream(const tb_arena* a, int32_t B, int32_t b, int32_t new_model_id, int32_t K,
+                    int32_t* model_ids, int32_t* states, float* scores, void* hip_stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* tb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TBIAS_H */

@@ -1,0 +1,307 @@
+"""Thin ctypes binding of libtbias.so (include/tbias.h).
+
+Argument marshalling only: every computation happens in the library. The
+functions keep the C names; torch tensors are accepted for device buffers and
+passed as raw pointers together with the current HIP stream. If the library is
+not built, importing this module raises: there is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+from pathlib import Path
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = Path(__file__).resolve().parent
+LIB_PATH = _PKG / "libtbias.so"
+
+TB_OK, TB_EINVAL, TB_ENOMEM, TB_EHIP, TB_ERANGE = 0, -1, -2, -3, -4
+TB_F32, TB_BF16 = 0, 1
+TB_COMMIT, TB_PURE_POTENTIAL = 0, 1
+TB_STATE_NONE, TB_STATE_INVALID = -1, -2
+TB_MAX_BEAM = 16
+
+
+class tb_arena_layout(C.Structure):
+    _fields_ = [
+        ("total_bytes", C.c_int64),
+        ("n_models", C.c_int32),
+        ("v_plus_blank", C.c_int32),
+        ("n_states", C.c_int64),
+        ("off_model_off", C.c_int64), ("off_model_n", C.c_int64),
+        ("off_first_child", C.c_int64), ("off_n_child", C.c_int64),
+        ("off_link", C.c_int64), ("off_label", C.c_int64),
+        ("off_phi", C.c_int64), ("off_psi", C.c_int64),
+        ("off_root_psi", C.c_int64), ("off_root_dst", C.c_int64),
+        ("off_class_map", C.c_int64), ("off_cls_ptr", C.c_int64), ("off_cls_tok", C.c_int64),
+        ("max_children", C.c_int32),
+        ("max_depth", C.c_int32),
+    ]
+
+
+class tb_arena(C.Structure):
+    _fields_ = [("base", C.c_void_p), ("layout", tb_arena_layout)]
+
+
+class TbError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"tbias error {code}: {msg}")
+        self.code = code
+
+
+def _load() -> C.CDLL:
+    # torch carries its own HIP runtime. Importing it first makes libtbias bind
+    # to that same runtime (same soname), so the device buffers and HIP
+    # streams torch hands over belong to the runtime the library launches on.
+    import torch  # noqa: F401
+    if not LIB_PATH.exists():
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2608_21343_amd.build`")
+    lib = C.CDLL(str(LIB_PATH))
+    P, I32, I64 = C.c_void_p, C.c_int32, C.c_int64
+    sig = {
+        "tb_compile_graphs": [I32, P, P, P, P, P, P, P, I32, I32, I32, C.POINTER(C.c_void_p)],
+        "tb_graphs_layout": [P, C.POINTER(tb_arena_layout)],
+        "tb_graphs_host_image": [P, P, I64],
+        "tb_graphs_upload": [P, P, I64, P, C.POINTER(tb_arena)],
+        "tb_validate_image": [P, C.POINTER(tb_arena_layout)],
+        "tb_init_states": [C.POINTER(tb_arena), I32, I32, P, P, P, P],
+        "tb_boost_step_greedy": [C.POINTER(tb_arena), P, I32, I32, I32, I64, P, P, P, P, P, P],
+        "tb_boost_step_beam": [C.POINTER(tb_arena), P, I32, I32, I32, I32, I64, P, P, P, P, P, P,
+                               P, P, P],
+        "tb_reset_stream": [C.POINTER(tb_arena), I32, I32, I32, I32, P, P, P, P],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    lib.tb_graphs_free.argtypes = [P]
+    lib.tb_graphs_free.restype = None
+    lib.tb_last_error.argtypes = []
+    lib.tb_last_error.restype = C.c_char_p
+    return lib
+
+
+LIB = _load()
+
+EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb_graphs_upload",
+            "tb_graphs_free", "tb_validate_image", "tb_init_states", "tb_boost_step_greedy",
+            "tb_boost_step_beam", "tb_reset_stream", "tb_last_error")
+
+
+def _check(code: int) -> None:
+    if code != TB_OK:
+        raise TbError(code, LIB.tb_last_error().decode(errors="replace"))
+
+
+def _np_ptr(a: np.ndarray) -> C.c_void_p:
+    return C.c_void_p(a.ctypes.data)
+
+
+def _dptr(t, dtype=None, name="tensor") -> Optional[int]:
+    """Device pointer of a torch tensor (None passes NULL)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# host-side compile
+
+
+class Graphs:
+    """Library-owned compiled graphs (tb_graphs*)."""
+
+    def __init__(self, handle: int):
+        self._h = C.c_void_p(handle)
+        self.layout = tb_arena_layout()
+        _check(LIB.tb_graphs_layout(self._h, C.byref(self.layout)))
+
+    def host_image(self) -> np.ndarray:
+        img = np.empty(self.layout.total_bytes, dtype=np.uint8)
+        _check(LIB.tb_graphs_host_image(self._h, _np_ptr(img), img.nbytes))
+        return img
+
+    def free(self) -> None:
+        if self._h:
+            LIB.tb_graphs_free(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def tb_compile_graphs(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, end_bonus,
+                      class_map, scale=None, semantics: int = TB_COMMIT,
+                      n_threads: int = 0) -> Graphs:
+    mp = np.ascontiguousarray(model_phrase_ptr, dtype=np.int64)
+    tp = np.ascontiguousarray(phrase_tok_ptr, dtype=np.int64)
+    tk = np.ascontiguousarray(phrase_tokens, dtype=np.int32)
+    n_models = len(mp) - 1
+    tw = np.ascontiguousarray(np.broadcast_to(np.asarray(token_w, np.float32), (n_models,)))
+    eb = np.ascontiguousarray(np.broadcast_to(np.asarray(end_bonus, np.float32), (n_models,)))
+    sc = None if scale is None else np.ascontiguousarray(
+        np.broadcast_to(np.asarray(scale, np.float32), (n_models,)))
+    cm = np.ascontiguousarray(class_map, dtype=np.int32)
+    out = C.c_void_p()
+    _check(LIB.tb_compile_graphs(n_models, _np_ptr(mp), _np_ptr(tp),
+                                 _np_ptr(tk) if tk.size else None, _np_ptr(tw), _np_ptr(eb),
+                                 _np_ptr(sc) if sc is not None else None, _np_ptr(cm), len(cm),
+                                 semantics, n_threads, C.byref(out)))
+    return Graphs(out.value)
+
+
+def tb_validate_image(image: np.ndarray, layout: tb_arena_layout) -> None:
+    img = np.ascontiguousarray(image, dtype=np.uint8)
+    _check(LIB.tb_validate_image(_np_ptr(img), C.byref(layout)))
+
+
+# ---------------------------------------------------------------------------
+# device side
+
+
+class Arena:
+    """A device arena: caller-owned (torch) device buffer plus tb_arena."""
+
+    def __init__(self, buf, arena: tb_arena):
+        self.buf = buf          # keeps the device memory alive
+        self.arena = arena
+
+    @property
+    def layout(self) -> tb_arena_layout:
+        return self.arena.layout
+
+
+def tb_graphs_upload(graphs: Graphs, device="cuda", stream=None) -> Arena:
+    import torch
+    nbytes = graphs.layout.total_bytes
+    buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    base = buf.data_ptr()
+    pad = (-base) % 256
+    arena = tb_arena()
+    _check(LIB.tb_graphs_upload(graphs._h, C.c_void_p(base + pad), nbytes, _stream(stream),
+                                C.byref(arena)))
+    return Arena(buf, arena)
+
+
+def tb_init_states(arena: Arena, B: int, K: int, model_ids, states, scores=None,
+                   stream=None) -> None:
+    import torch
+    _check(LIB.tb_init_states(C.byref(arena.arena), B, K,
+                              _dptr(model_ids, torch.int32, "model_ids"),
+                              _dptr(states, torch.int32, "states"),
+                              _dptr(scores, torch.float32, "scores"), _stream(stream)))
+
+
+def _logits_args(logits):
+    import torch
+    if logits.dtype == torch.float32:
+        dt = TB_F32
+    elif logits.dtype == torch.bfloat16:
+        dt = TB_BF16
+    else:
+        raise ValueError("logits must be float32 or bfloat16")
+    if not logits.is_cuda:
+        raise ValueError("logits must be a device tensor")
+    if logits.stride(-1) != 1:
+        raise ValueError("logits rows must be contiguous")
+    return dt, logits.data_ptr(), logits.stride(-2)
+
+
+def tb_boost_step_greedy(arena: Arena, logits, model_ids, states, out_tok, out_state, out_score,
+                         T: Optional[int] = None, B: Optional[int] = None,
+                         row_stride: Optional[int] = None, stream=None) -> None:
+    """logits: [T, B, V+1] (or [T, B, 1, V+1]) device tensor, rows contiguous."""
+    import torch
+    dt, ptr, rs = _logits_args(logits)
+    if logits.dim() == 4:
+        if logits.shape[2] != 1:
+            raise ValueError("greedy logits must have K = 1")
+        rs = logits.stride(1)
+    T = logits.shape[0] if T is None else T
+    B = logits.shape[1] if B is None else B
+    if logits.dim() >= 3 and T > 1 and logits.stride(0) != B * rs:
+        raise ValueError("logits steps must be laid out as (t*B + b) * row_stride")
+    rs = rs if row_stride is None else row_stride
+    _check(LIB.tb_boost_step_greedy(C.byref(arena.arena), C.c_void_p(ptr), dt, T, B, rs,
+                                    _dptr(model_ids, torch.int32, "model_ids"),
+                                    _dptr(states, torch.int32, "states"),
+                                    _dptr(out_tok, torch.int32, "out_tok"),
+                                    _dptr(out_state, torch.int32, "out_state"),
+                                    _dptr(out_score, torch.float32, "out_score"),
+                                    _stream(stream)))
+
+
+def tb_boost_step_beam(arena: Arena, logits, model_ids, states, scores, out_tok, out_parent,
+                       out_state, out_step, out_cum, stream=None) -> None:
+    """logits: [T, B, K, V+1] device tensor with (t, b, k) rows at ((t*B+b)*K+k)*row_stride."""
+    import torch
+    dt, ptr, rs = _logits_args(logits)
+    if logits.dim() != 4:
+        raise ValueError("beam logits must be [T, B, K, V+1]")
+    T, B, K, _ = logits.shape
+    if logits.stride(1) != K * rs or (T > 1 and logits.stride(0) != B * K * rs):
+        raise ValueError("beam logits must be laid out as ((t*B + b)*K + k) * row_stride")
+    _check(LIB.tb_boost_step_beam(C.byref(arena.arena), C.c_void_p(ptr), dt, T, B, K, rs,
+                                  _dptr(model_ids, torch.int32, "model_ids"),
+                                  _dptr(states, torch.int32, "states"),
+                                  _dptr(scores, torch.float32, "scores"),
+                                  _dptr(out_tok, torch.int32, "out_tok"),
+                                  _dptr(out_parent, torch.int32, "out_parent"),
+                                  _dptr(out_state, torch.int32, "out_state"),
+                                  _dptr(out_step, torch.float32, "out_step"),
+                                  _dptr(out_cum, torch.float32, "out_cum"),
+                                  _stream(stream)))
+
+
+def tb_reset_stream(arena: Arena, b: int, new_model_id: int, K: int, model_ids, states,
+                    scores=None, stream=None) -> None:
+    import torch
+    B = model_ids.numel()
+    if states.numel() != B * K or (scores is not None and scores.numel() != B * K):
+        raise ValueError("states/scores must hold B*K entries")
+    _check(LIB.tb_reset_stream(C.byref(arena.arena), B, b, new_model_id, K,
+                               _dptr(model_ids, torch.int32, "model_ids"),
+                               _dptr(states, torch.int32, "states"),
+                               _dptr(scores, torch.float32, "scores"), _stream(stream)))
+
+
+def image_arrays(image: np.ndarray, layout: tb_arena_layout) -> dict:
+    """Views of the arrays inside a host arena image (see tb_arena_layout)."""
+    L = layout
+    N, M, V1 = L.n_states, L.n_models, L.v_plus_blank
+
+    def arr(off, n, dt):
+        return np.frombuffer(image, dtype=dt, count=n, offset=off)
+
+    return {
+        "model_off": arr(L.off_model_off, M, np.int32),
+        "model_n": arr(L.off_model_n, M, np.int32),
+        "first_child": arr(L.off_first_child, N, np.int32),
+        "n_child": arr(L.off_n_child, N, np.int32),
+        "link": arr(L.off_link, N, np.int32),
+        "label": arr(L.off_label, N, np.int32),
+        "phi": arr(L.off_phi, N, np.float32),
+        "psi": arr(L.off_psi, N, np.float32),
+        "root_psi": arr(L.off_root_psi, M * V1, np.float32).reshape(M, V1),
+        "root_dst": arr(L.off_root_dst, M * V1, np.int32).reshape(M, V1),
+        "class_map": arr(L.off_class_map, V1, np.int32),
+        "cls_ptr": arr(L.off_cls_ptr, V1, np.int32),
+        "cls_tok": arr(L.off_cls_tok, V1 - 1, np.int32),
+    }

@@ -1,0 +1,288 @@
+// Boosted beam step (reference kernel): one workgroup per stream.
+//
+// For each of the K hypotheses of a stream the workgroup forms the row's
+// log-sum-exp (float64 sum and log, rounded once to float32), the boosted keys
+// key[v] = z[v] + psi[delta(s_k, class v)] (blank: z[V] + phi[s_k]) and the
+// candidates cand = ((S_k - lse_k) - phi[s_k]) + key[v]. Every thread keeps
+// its own best MAXK candidates; K rounds of a workgroup argmax then pick the
+// K best over all K*(V+1) candidates (ties to the lowest flat index
+// k*(V+1)+v), and the surviving hypotheses are reordered with their advanced
+// graph states (Sec. II-C: scores and states carried across calls).
+#include <climits>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace tbias {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+__device__ inline float bmax(float x, float* red) {
+  x = wave_max(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r = fmaxf(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+__device__ inline double bsum_d(double x, double* red) {
+  x = wave_sum_d(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  double r = red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r += red[i];
+  __syncthreads();
+  return r;
+}
+
+__device__ inline void bargmax(float& k, int32_t& i, float* redk, int32_t* redi) {
+  wave_argmax(k, i);
+  if ((threadIdx.x & 63) == 0) {
+    redk[threadIdx.x >> 6] = k;
+    redi[threadIdx.x >> 6] = i;
+  }
+  __syncthreads();
+  k = redk[0];
+  i = redi[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w)
+    if (better(redk[w], redi[w], k, i)) { k = redk[w]; i = redi[w]; }
+  __syncthreads();
+}
+
+// Aho-Corasick move from local state x on class c (global memory walk).
+__device__ inline int32_t ac_move(const ArenaView& A, int32_t off, int32_t x, int32_t c) {
+  for (;;) {
+    int32_t lo = A.first_child[off + x], hi = lo + A.n_child[off + x];
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      const int32_t l = A.label[off + mid];
+      if (l == c) return mid;
+      if (l < c) lo = mid + 1; else hi = mid;
+    }
+    if (x == 0) return 0;
+    x = A.link[off + x];
+  }
+}
+
+template <class Ld, int MAXK>
+__global__ __launch_bounds__(kThreads) void beam_ref_kernel(
+    ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int32_t K,
+    int64_t stride, const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
+    float* __restrict__ scores, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_parent,
+    int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum) {
+  extern __shared__ int32_t smem[];
+  const int32_t V1 = A.V1, V = V1 - 1;
+  int32_t* odst = smem;
+  uint16_t* stamp = reinterpret_cast<uint16_t*>(smem + V);
+  __shared__ float redf[kWaves];
+  __shared__ int32_t redi[kWaves];
+  __shared__ double redd[kWaves];
+  __shared__ int32_t sh_state[MAXK];
+  __shared__ float sh_S[MAXK];
+  __shared__ float sh_lse[MAXK];
+  __shared__ float sh_phi[MAXK];
+  __shared__ int32_t sel_idx[MAXK];
+  __shared__ float sel_val[MAXK];
+  __shared__ int32_t sh_bad;
+
+  const int tid = threadIdx.x;
+  const int32_t b = blockIdx.x;
+  const int32_t m = model_ids[b];
+  if (tid == 0) sh_bad = 0;
+  __syncthreads();
+  int32_t off = 0, n = 0;
+  int mode = (m == -1) ? 0 : 1;
+  if (m < -1 || m >= A.n_models) mode = -1;
+  if (mode == 1) { off = A.model_off[m]; n = A.model_n[m]; }
+  if (tid < K) {
+    const int32_t s = states[(int64_t)b * K + tid];
+    sh_state[tid] = s;
+    sh_S[tid] = scores[(int64_t)b * K + tid];
+    if (mode == 1 && (s < 0 || s >= n)) sh_bad = 1;
+  }
+  for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
+  __syncthreads();
+  if (mode == 1 && sh_bad) mode = -1;
+  uint32_t tag = 0;
+  const float* rpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
+  const int32_t* rdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
+
+  for (int32_t t = 0; t < T; ++t) {
+    float lk[MAXK];
+    int32_t li[MAXK];
+#pragma unroll
+    for (int j = 0; j < MAXK; ++j) { lk[j] = -__builtin_huge_valf(); li[j] = INT_MAX; }
+
+    for (int32_t k = 0; k < K; ++k) {
+      const typename Ld::T* row = logits + (((int64_t)t * B + b) * K + k) * stride;
+      float mx = -__builtin_huge_valf();
+      for (int32_t v = tid; v < V1; v += kThreads) mx = fmaxf(mx, Ld::get(row, v));
+      mx = bmax(mx, redf);
+      double se = 0.0;
+      const double mxd = (double)mx;
+      for (int32_t v = tid; v < V1; v += kThreads) se += exp((double)Ld::get(row, v) - mxd);
+      se = bsum_d(se, redd);
+      const float lse = (float)(mxd + log(se));
+      const int32_t s = sh_state[k];
+
+      float phi_s = 0.f;
+      if (mode == 1) {
+        phi_s = A.phi[off + s];
+        if (++tag == 65536u) {
+          for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
+          __syncthreads();
+          tag = 1;
+        }
+        for (int32_t x = s; x != 0; x = A.link[off + x]) {
+          const int32_t fc = A.first_child[off + x], nc = A.n_child[off + x];
+          for (int32_t j = tid; j < nc; j += kThreads) {
+            const int32_t y = fc + j;
+            const int32_t c = A.label[off + y];
+            if (stamp[c] != tag) {
+              stamp[c] = (uint16_t)tag;
+              odst[c] = y;
+            }
+          }
+          __syncthreads();
+        }
+      }
+      const float ck = (sh_S[k] - lse) - phi_s;
+      for (int32_t v = tid; v < V1; v += kThreads) {
+        const float z = Ld::get(row, v);
+        float p = 0.f;
+        if (mode == 1) {
+          if (v == V) {
+            p = phi_s;
+          } else {
+            const int32_t c = A.class_map[v];
+            p = (c >= 0 && stamp[c] == tag) ? A.psi[off + odst[c]] : rpsi[v];
+          }
+        }
+        const float key = z + p;
+        const float cand = ck + key;
+        const int32_t f = k * V1 + v;
+        if (better(cand, f, lk[MAXK - 1], li[MAXK - 1])) {
+          lk[MAXK - 1] = cand;
+          li[MAXK - 1] = f;
+#pragma unroll
+          for (int j = MAXK - 1; j > 0; --j) {
+            if (better(lk[j], li[j], lk[j - 1], li[j - 1])) {
+              const float tk = lk[j]; lk[j] = lk[j - 1]; lk[j - 1] = tk;
+              const int32_t ti = li[j]; li[j] = li[j - 1]; li[j - 1] = ti;
+            }
+          }
+        }
+      }
+      if (tid == 0) { sh_lse[k] = lse; sh_phi[k] = phi_s; }
+      __syncthreads();  // the next hypothesis rewrites the override table
+    }
+
+    // K rounds of a workgroup argmax over the per-thread heads
+    for (int32_t j = 0; j < K; ++j) {
+      float hk = lk[0];
+      int32_t hi = li[0];
+      bargmax(hk, hi, redf, redi);
+      if (li[0] == hi) {
+#pragma unroll
+        for (int q = 0; q < MAXK - 1; ++q) { lk[q] = lk[q + 1]; li[q] = li[q + 1]; }
+        lk[MAXK - 1] = -__builtin_huge_valf();
+        li[MAXK - 1] = INT_MAX;
+      }
+      if (tid == 0) { sel_val[j] = hk; sel_idx[j] = hi; }
+    }
+    __syncthreads();
+
+    int32_t ns = 0;
+    float nS = 0.f;
+    if (tid < K) {
+      const int32_t j = tid;
+      int32_t f = sel_idx[j];
+      if (f < 0 || f >= K * V1) f = 0;  // only reachable with NaN logits
+      const int32_t k = f / V1, v = f - k * V1;
+      const int32_t s = sh_state[k];
+      float bst = 0.f;
+      if (mode == 1) {
+        if (v == V) {
+          ns = s;
+        } else {
+          const int32_t c = A.class_map[v];
+          ns = (c >= 0) ? ac_move(A, off, s, c) : rdst[v];
+          bst = A.psi[off + ns] - sh_phi[k];
+        }
+      } else {
+        ns = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+      }
+      const typename Ld::T* row = logits + (((int64_t)t * B + b) * K + k) * stride;
+      const float z = Ld::get(row, v);
+      const int64_t o = ((int64_t)t * B + b) * K + j;
+      nS = sel_val[j];
+      out_tok[o] = v;
+      out_parent[o] = k;
+      out_state[o] = ns;
+      out_step[o] = (z - sh_lse[k]) + bst;
+      out_cum[o] = nS;
+    }
+    __syncthreads();
+    if (tid < K) { sh_state[tid] = ns; sh_S[tid] = nS; }
+    __syncthreads();
+  }
+  if (tid < K && T > 0) {
+    states[(int64_t)b * K + tid] = sh_state[tid];
+    scores[(int64_t)b * K + tid] = sh_S[tid];
+  }
+}
+
+template <class Ld, int MAXK>
+void launch_t(const ArenaView& A, const void* logits, int32_t T, int32_t B, int32_t K,
+              int64_t stride, const int32_t* model_ids, int32_t* states, float* scores,
+              int32_t* out_tok, int32_t* out_parent, int32_t* out_state, float* out_step,
+              float* out_cum, hipStream_t st) {
+  const size_t lds = (size_t)6 * (A.V1 - 1) + 4;
+  hipLaunchKernelGGL((beam_ref_kernel<Ld, MAXK>), dim3(B), dim3(kThreads), lds, st, A,
+                     static_cast<const typename Ld::T*>(logits), T, B, K, stride, model_ids,
+                     states, scores, out_tok, out_parent, out_state, out_step, out_cum);
+}
+
+template <class Ld>
+void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int32_t K,
+              int64_t stride, const int32_t* model_ids, int32_t* states, float* scores,
+              int32_t* out_tok, int32_t* out_parent, int32_t* out_state, float* out_step,
+              float* out_cum, hipStream_t st) {
+  if (K <= 2)
+    launch_t<Ld, 2>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
+                    out_state, out_step, out_cum, st);
+  else if (K <= 4)
+    launch_t<Ld, 4>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
+                    out_state, out_step, out_cum, st);
+  else if (K <= 8)
+    launch_t<Ld, 8>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
+                    out_state, out_step, out_cum, st);
+  else
+    launch_t<Ld, 16>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
+                     out_state, out_step, out_cum, st);
+}
+
+}  // namespace
+
+hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, int32_t T, int32_t B,
+                       int32_t K, int64_t row_stride, const int32_t* model_ids, int32_t* states,
+                       float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
+                       float* out_step, float* out_cum, hipStream_t st) {
+  if (dtype == TB_F32)
+    launch_k<LoadF32>(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok,
+                      out_parent, out_state, out_step, out_cum, st);
+  else
+    launch_k<LoadBF16>(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok,
+                       out_parent, out_state, out_step, out_cum, st);
+  return hipGetLastError();
+}
+
+}  // namespace tbias

@@ -1,0 +1,182 @@
+// Device-side view of the arena and small wave64 helpers (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/tbias.h"
+
+namespace tbias {
+
+// Raw device pointers into one arena image (see tb_arena_layout).
+struct ArenaView {
+  const int32_t* model_off;
+  const int32_t* model_n;
+  const int32_t* first_child;
+  const int32_t* n_child;
+  const int32_t* link;
+  const int32_t* label;
+  const float* phi;
+  const float* psi;
+  const float* root_psi;
+  const int32_t* root_dst;
+  const int32_t* class_map;
+  const int32_t* cls_ptr;
+  const int32_t* cls_tok;
+  int32_t n_models;
+  int32_t V1;  // V + 1
+};
+
+inline ArenaView make_view(const tb_arena& a) {
+  const unsigned char* b = static_cast<const unsigned char*>(a.base);
+  const tb_arena_layout& L = a.layout;
+  ArenaView v;
+  v.model_off = reinterpret_cast<const int32_t*>(b + L.off_model_off);
+  v.model_n = reinterpret_cast<const int32_t*>(b + L.off_model_n);
+  v.first_child = reinterpret_cast<const int32_t*>(b + L.off_first_child);
+  v.n_child = reinterpret_cast<const int32_t*>(b + L.off_n_child);
+  v.link = reinterpret_cast<const int32_t*>(b + L.off_link);
+  v.label = reinterpret_cast<const int32_t*>(b + L.off_label);
+  v.phi = reinterpret_cast<const float*>(b + L.off_phi);
+  v.psi = reinterpret_cast<const float*>(b + L.off_psi);
+  v.root_psi = reinterpret_cast<const float*>(b + L.off_root_psi);
+  v.root_dst = reinterpret_cast<const int32_t*>(b + L.off_root_dst);
+  v.class_map = reinterpret_cast<const int32_t*>(b + L.off_class_map);
+  v.cls_ptr = reinterpret_cast<const int32_t*>(b + L.off_cls_ptr);
+  v.cls_tok = reinterpret_cast<const int32_t*>(b + L.off_cls_tok);
+  v.n_models = L.n_models;
+  v.V1 = L.v_plus_blank;
+  return v;
+}
+
+// Element loaders: float32 as is, bfloat16 widened exactly.
+struct LoadF32 {
+  typedef float T;
+  __device__ static inline float get(const float* p, int64_t i) { return p[i]; }
+  // streaming read of a logit row: read once, not kept in the caches
+  __device__ static inline float get_nt(const float* p, int64_t i) {
+    return __builtin_nontemporal_load(p + i);
+  }
+};
+struct LoadBF16 {
+  typedef uint16_t T;
+  __device__ static inline float get(const uint16_t* p, int64_t i) {
+    return __uint_as_float(((uint32_t)p[i]) << 16);
+  }
+  __device__ static inline float get_nt(const uint16_t* p, int64_t i) {
+    return __uint_as_float(((uint32_t)__builtin_nontemporal_load(p + i)) << 16);
+  }
+};
+
+// (key, index) order used by every selection: larger key first, then lower index.
+__device__ inline bool better(float ka, int32_t ia, float kb, int32_t ib) {
+  return ka > kb || (ka == kb && ia < ib);
+}
+
+// ---- wave64 reductions on DPP (row shifts within rows of 16 lanes, then the
+// gfx9 row broadcasts); every lane of the wave must be active. The result is
+// the value of lane 63, returned uniform.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_i(int old, int src) {
+  return __builtin_amdgcn_update_dpp(old, src, CTRL, ROW_MASK, 0xf, false);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_f(float old, float src) {
+  return __int_as_float(dpp_i<CTRL, ROW_MASK>(__float_as_int(old), __float_as_int(src)));
+}
+__device__ __forceinline__ float bcast63_f(float v) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ float wave_max_dpp(float v) {
+  const float id = -__builtin_huge_valf();
+  v = fmaxf(v, dpp_f<0x111, 0xf>(id, v));
+  v = fmaxf(v, dpp_f<0x112, 0xf>(id, v));
+  v = fmaxf(v, dpp_f<0x114, 0xf>(id, v));
+  v = fmaxf(v, dpp_f<0x118, 0xf>(id, v));
+  v = fmaxf(v, dpp_f<0x142, 0xa>(id, v));
+  v = fmaxf(v, dpp_f<0x143, 0xc>(id, v));
+  return bcast63_f(v);
+}
+
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v = v + dpp_f<0x111, 0xf>(0.f, v);
+  v = v + dpp_f<0x112, 0xf>(0.f, v);
+  v = v + dpp_f<0x114, 0xf>(0.f, v);
+  v = v + dpp_f<0x118, 0xf>(0.f, v);
+  v = v + dpp_f<0x142, 0xa>(0.f, v);
+  v = v + dpp_f<0x143, 0xc>(0.f, v);
+  return bcast63_f(v);
+}
+
+__device__ __forceinline__ int32_t wave_min_i32_dpp(int32_t v) {
+  const int32_t id = 0x7fffffff;
+  v = min(v, dpp_i<0x111, 0xf>(id, v));
+  v = min(v, dpp_i<0x112, 0xf>(id, v));
+  v = min(v, dpp_i<0x114, 0xf>(id, v));
+  v = min(v, dpp_i<0x118, 0xf>(id, v));
+  v = min(v, dpp_i<0x142, 0xa>(id, v));
+  v = min(v, dpp_i<0x143, 0xc>(id, v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+// Wave argmax of (key, idx): larger key, then lower idx. Returns the winner
+// (uniform) and the first lane holding it.
+__device__ __forceinline__ int32_t wave_argmax_dpp(float key, int32_t idx, float& bk, int32_t& bi) {
+  const float m = wave_max_dpp(key);
+  const uint64_t hit = __ballot(key == m);
+  int32_t lane;
+  if (__builtin_popcountll(hit) == 1) {
+    lane = (int32_t)__builtin_ctzll(hit);
+    bi = __builtin_amdgcn_readlane(idx, lane);
+  } else {
+    bi = wave_min_i32_dpp(key == m ? idx : 0x7fffffff);
+    const uint64_t own = __ballot(key == m && idx == bi);
+    lane = own ? (int32_t)__builtin_ctzll(own) : 0;
+  }
+  bk = m;
+  return lane;
+}
+
+__device__ inline float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+__device__ inline float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+__device__ inline double wave_sum_d(double x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+__device__ inline void wave_argmax(float& k, int32_t& i) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float k2 = __shfl_xor(k, o, 64);
+    int32_t i2 = __shfl_xor(i, o, 64);
+    if (better(k2, i2, k, i)) { k = k2; i = i2; }
+  }
+}
+
+// Resolve a (model id, carried state) pair.
+//   returns 1 and sets off/n when the stream is biased with a valid state,
+//   0 for model -1, -1 for an out-of-range model id or carried state.
+__device__ inline int resolve_stream(const ArenaView& A, int32_t m, int32_t s, int32_t& off,
+                                     int32_t& n) {
+  if (m == -1) return 0;
+  if (m < -1 || m >= A.n_models) return -1;
+  off = A.model_off[m];
+  n = A.model_n[m];
+  if (s < 0 || s >= n) return -1;
+  return 1;
+}
+
+}  // namespace tbias

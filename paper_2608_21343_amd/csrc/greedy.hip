@@ -1,0 +1,200 @@
+// Boosted greedy step (reference kernel): one workgroup per stream.
+//
+// Per step the workgroup (Sec. II-B fused scoring operation):
+//   1. reads the stream's logit row and forms the log-softmax normaliser;
+//   2. runs the suffix-link traversal from the current state: the children of
+//      every state on the suffix chain s, link(s), ... (excluding the root)
+//      override the root move of their class, the deepest state winning;
+//   3. forms key[v] = z[v] + psi[delta(s, class v)] (blank: z[V] + phi[s]),
+//      takes the lowest-index maximum and advances the state.
+// The override table lives in LDS, indexed by class: a 16-bit tag per class
+// marks the entries written in the current step (cleared once every 65535
+// steps) next to the overriding target state.
+#include <climits>
+#include <cstdlib>
+#include <cstring>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace tbias {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+__device__ inline float block_max(float x, float* red) {
+  x = wave_max(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r = fmaxf(r, red[i]);
+  __syncthreads();
+  return r;
+}
+
+__device__ inline float block_sum(float x, float* red) {
+  x = wave_sum(x);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int i = 1; i < kWaves; ++i) r += red[i];
+  __syncthreads();
+  return r;
+}
+
+__device__ inline void block_argmax(float& k, int32_t& i, float* redk, int32_t* redi) {
+  wave_argmax(k, i);
+  if ((threadIdx.x & 63) == 0) {
+    redk[threadIdx.x >> 6] = k;
+    redi[threadIdx.x >> 6] = i;
+  }
+  __syncthreads();
+  k = redk[0];
+  i = redi[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w)
+    if (better(redk[w], redi[w], k, i)) { k = redk[w]; i = redi[w]; }
+  __syncthreads();
+}
+
+template <class Ld>
+__global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
+    ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
+    const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
+    int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
+    float* __restrict__ out_score) {
+  extern __shared__ int32_t smem[];
+  const int32_t V1 = A.V1, V = V1 - 1;
+  int32_t* odst = smem;
+  uint16_t* stamp = reinterpret_cast<uint16_t*>(smem + V);
+  __shared__ float redf[kWaves];
+  __shared__ int32_t redi[kWaves];
+  __shared__ int32_t s_next;
+
+  const int tid = threadIdx.x;
+  const int32_t b = blockIdx.x;
+  const int32_t m = model_ids[b];
+  int32_t s = states[b];
+  int32_t off = 0, n = 0;
+  const int mode = resolve_stream(A, m, s, off, n);  // 1 biased, 0 none, -1 invalid
+  for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
+  __syncthreads();
+  uint32_t tag = 0;
+  const float* rpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
+  const int32_t* rdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
+
+  for (int32_t t = 0; t < T; ++t) {
+    const typename Ld::T* row = logits + ((int64_t)t * B + b) * stride;
+    float mx = -__builtin_huge_valf();
+    for (int32_t v = tid; v < V1; v += kThreads) mx = fmaxf(mx, Ld::get(row, v));
+    mx = block_max(mx, redf);
+    float se = 0.f;
+    for (int32_t v = tid; v < V1; v += kThreads) se += expf(Ld::get(row, v) - mx);
+    se = block_sum(se, redf);
+    const float lse = mx + logf(se);
+
+    float phi_s = 0.f;
+    if (mode == 1) {
+      phi_s = A.phi[off + s];
+      if (++tag == 65536u) {  // uniform: clear the tags and restart
+        for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
+        __syncthreads();
+        tag = 1;
+      }
+      for (int32_t x = s; x != 0; x = A.link[off + x]) {
+        const int32_t fc = A.first_child[off + x], nc = A.n_child[off + x];
+        for (int32_t j = tid; j < nc; j += kThreads) {
+          const int32_t y = fc + j;
+          const int32_t c = A.label[off + y];
+          if (stamp[c] != tag) {
+            stamp[c] = (uint16_t)tag;
+            odst[c] = y;
+          }
+        }
+        __syncthreads();
+      }
+    }
+
+    float bk = -__builtin_huge_valf();
+    int32_t bi = INT_MAX;
+    for (int32_t v = tid; v < V1; v += kThreads) {
+      const float z = Ld::get(row, v);
+      float p = 0.f;
+      if (mode == 1) {
+        if (v == V) {
+          p = phi_s;
+        } else {
+          const int32_t c = A.class_map[v];
+          p = (c >= 0 && stamp[c] == tag) ? A.psi[off + odst[c]] : rpsi[v];
+        }
+      }
+      const float key = z + p;
+      if (better(key, v, bk, bi)) { bk = key; bi = v; }
+    }
+    block_argmax(bk, bi, redf, redi);
+
+    if (tid == 0) {
+      const int32_t v = bi;
+      int32_t ns;
+      float bst = 0.f;
+      if (mode == 1) {
+        if (v == V) {
+          ns = s;
+        } else {
+          const int32_t c = A.class_map[v];
+          ns = (c >= 0 && stamp[c] == tag) ? odst[c] : rdst[v];
+          bst = A.psi[off + ns] - phi_s;
+        }
+      } else {
+        ns = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+      }
+      const float z = Ld::get(row, v);
+      const int64_t o = (int64_t)t * B + b;
+      out_tok[o] = v;
+      out_state[o] = ns;
+      out_score[o] = (z - lse) + bst;
+      s_next = ns;
+    }
+    __syncthreads();
+    s = s_next;
+  }
+  if (tid == 0 && T > 0) states[b] = s;
+}
+
+}  // namespace
+
+namespace {
+// TBIAS_GREEDY_KERNEL=ref selects the reference kernel (used to test both paths).
+bool use_reference_kernel() {
+  const char* e = std::getenv("TBIAS_GREEDY_KERNEL");
+  return e && std::strcmp(e, "ref") == 0;
+}
+}  // namespace
+
+hipError_t launch_greedy(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                         int32_t B, int64_t row_stride, const int32_t* model_ids, int32_t* states,
+                         int32_t* out_tok, int32_t* out_state, float* out_score, hipStream_t st) {
+  if (!use_reference_kernel()) {
+    hipError_t e = launch_greedy_fast(A, logits, dtype, T, B, row_stride, model_ids, states,
+                                      out_tok, out_state, out_score, st);
+    if (e != hipErrorNotSupported) return e;
+    (void)hipGetLastError();  // clear the sticky "not supported" before the fallback
+  }
+  const size_t lds = (size_t)6 * (A.V1 - 1) + 4;
+  if (dtype == TB_F32) {
+    hipLaunchKernelGGL(greedy_ref_kernel<LoadF32>, dim3(B), dim3(kThreads), lds, st, A,
+                       static_cast<const float*>(logits), T, B, row_stride, model_ids, states,
+                       out_tok, out_state, out_score);
+  } else {
+    hipLaunchKernelGGL(greedy_ref_kernel<LoadBF16>, dim3(B), dim3(kThreads), lds, st, A,
+                       static_cast<const uint16_t*>(logits), T, B, row_stride, model_ids, states,
+                       out_tok, out_state, out_score);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tbias

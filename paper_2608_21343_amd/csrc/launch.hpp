@@ -1,0 +1,34 @@
+// Host launchers of the device kernels (argument checks happen in the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "device.hpp"
+
+namespace tbias {
+
+hipError_t launch_init_states(const ArenaView& A, int32_t B, int32_t K, const int32_t* model_ids,
+                              int32_t* states, float* scores, hipStream_t st);
+hipError_t launch_reset_stream(int32_t b, int32_t m, int32_t K, int32_t* model_ids,
+                               int32_t* states, float* scores, hipStream_t st);
+
+// Greedy: T steps for B streams. Requires V1 <= kMaxV1.
+hipError_t launch_greedy(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                         int32_t B, int64_t row_stride, const int32_t* model_ids, int32_t* states,
+                         int32_t* out_tok, int32_t* out_state, float* out_score, hipStream_t st);
+
+hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, int32_t T, int32_t B,
+                       int32_t K, int64_t row_stride, const int32_t* model_ids, int32_t* states,
+                       float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
+                       float* out_step, float* out_cum, hipStream_t st);
+
+// Pipelined greedy kernel; hipErrorNotSupported when V+1 is too large for it.
+hipError_t launch_greedy_fast(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                              int32_t B, int64_t row_stride, const int32_t* model_ids,
+                              int32_t* states, int32_t* out_tok, int32_t* out_state,
+                              float* out_score, hipStream_t st);
+
+// Largest V+1 the step kernels accept (LDS tables are sized by it).
+constexpr int32_t kMaxV1 = 10241;
+
+}  // namespace tbias

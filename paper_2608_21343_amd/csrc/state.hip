@@ -1,0 +1,44 @@
+// Stream start / restart kernels (per-stream model id and carried state).
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace tbias {
+
+__global__ void init_states_kernel(ArenaView A, int32_t B, int32_t K, const int32_t* model_ids,
+                                   int32_t* states, float* scores) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)B * K) return;
+  int32_t b = (int32_t)(i / K), k = (int32_t)(i % K);
+  int32_t m = model_ids[b];
+  int32_t s = (m == -1) ? TB_STATE_NONE : ((m < -1 || m >= A.n_models) ? TB_STATE_INVALID : 0);
+  states[i] = s;
+  if (scores) scores[i] = (k == 0) ? 0.f : -__builtin_huge_valf();
+}
+
+__global__ void reset_stream_kernel(int32_t b, int32_t m, int32_t K, int32_t* model_ids,
+                                    int32_t* states, float* scores) {
+  int32_t k = threadIdx.x;
+  if (k >= K) return;
+  if (k == 0) model_ids[b] = m;
+  states[(int64_t)b * K + k] = (m == -1) ? TB_STATE_NONE : 0;
+  if (scores) scores[(int64_t)b * K + k] = (k == 0) ? 0.f : -__builtin_huge_valf();
+}
+
+hipError_t launch_init_states(const ArenaView& A, int32_t B, int32_t K, const int32_t* model_ids,
+                              int32_t* states, float* scores, hipStream_t st) {
+  int64_t n = (int64_t)B * K;
+  int threads = 256;
+  int blocks = (int)((n + threads - 1) / threads);
+  hipLaunchKernelGGL(init_states_kernel, dim3(blocks), dim3(threads), 0, st, A, B, K, model_ids,
+                     states, scores);
+  return hipGetLastError();
+}
+
+hipError_t launch_reset_stream(int32_t b, int32_t m, int32_t K, int32_t* model_ids,
+                               int32_t* states, float* scores, hipStream_t st) {
+  hipLaunchKernelGGL(reset_stream_kernel, dim3(1), dim3(64), 0, st, b, m, K, model_ids, states,
+                     scores);
+  return hipGetLastError();
+}
+
+}  // namespace tbias

@@ -1,0 +1,80 @@
+"""Convenience wrapper: compile per-stream lists once, then step chunks.
+
+Marshalling only (device buffers come from torch, all work runs in
+libtbias.so). Mirrors the streaming use of Sec. II-C: states (and beam
+scores) live on the device between calls, so a stream can be decoded chunk by
+chunk.
+"""
+
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import capi
+
+
+def to_device_logits(rows: np.ndarray, device="cuda") -> torch.Tensor:
+    """float32 rows as float32; uint16 bfloat16 bits as bfloat16."""
+    if rows.dtype == np.float32:
+        return torch.from_numpy(np.ascontiguousarray(rows)).to(device)
+    if rows.dtype == np.uint16:
+        t = torch.from_numpy(np.ascontiguousarray(rows).view(np.int16)).to(device)
+        return t.view(torch.bfloat16)
+    raise TypeError(rows.dtype)
+
+
+class BoostDecoder:
+    def __init__(self, lists: Sequence[Sequence[np.ndarray]], class_map: np.ndarray,
+                 token_w=1.0, end_bonus=2.0, scale=None, semantics: int = capi.TB_COMMIT,
+                 device="cuda"):
+        mp, tp, tk = _csr(lists)
+        self.graphs = capi.tb_compile_graphs(mp, tp, tk, token_w, end_bonus, class_map,
+                                             scale=scale, semantics=semantics)
+        self.arena = capi.tb_graphs_upload(self.graphs, device=device)
+        self.device = device
+        self.V1 = int(len(class_map))
+
+    def start(self, model_ids: Sequence[int], K: int = 1):
+        """Device carry for len(model_ids) streams: (model_ids, states, scores)."""
+        B = len(model_ids)
+        mids = torch.tensor(np.asarray(model_ids, np.int32), device=self.device)
+        states = torch.empty(B * K, dtype=torch.int32, device=self.device)
+        scores = torch.empty(B * K, dtype=torch.float32, device=self.device)
+        capi.tb_init_states(self.arena, B, K, mids, states, scores)
+        return mids, states, scores
+
+    def greedy(self, logits: torch.Tensor, mids, states, out=None):
+        T, B = logits.shape[0], logits.shape[1]
+        if out is None:
+            out = (torch.empty((T, B), dtype=torch.int32, device=self.device),
+                   torch.empty((T, B), dtype=torch.int32, device=self.device),
+                   torch.empty((T, B), dtype=torch.float32, device=self.device))
+        capi.tb_boost_step_greedy(self.arena, logits, mids, states, *out)
+        return out
+
+    def beam(self, logits: torch.Tensor, mids, states, scores, out=None):
+        T, B, K = logits.shape[0], logits.shape[1], logits.shape[2]
+        if out is None:
+            i32 = dict(dtype=torch.int32, device=self.device)
+            f32 = dict(dtype=torch.float32, device=self.device)
+            out = (torch.empty((T, B, K), **i32), torch.empty((T, B, K), **i32),
+                   torch.empty((T, B, K), **i32), torch.empty((T, B, K), **f32),
+                   torch.empty((T, B, K), **f32))
+        capi.tb_boost_step_beam(self.arena, logits, mids, states, scores, *out)
+        return out
+
+
+def _csr(lists):
+    mp = [0]
+    tp = [0]
+    toks = []
+    for lst in lists:
+        for ph in lst:
+            toks.append(np.asarray(ph, dtype=np.int32))
+            tp.append(tp[-1] + len(ph))
+        mp.append(len(tp) - 1)
+    tk = np.concatenate(toks).astype(np.int32) if toks else np.zeros(0, np.int32)
+    return np.asarray(mp, np.int64), np.asarray(tp, np.int64), tk

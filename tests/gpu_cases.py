@@ -1,0 +1,101 @@
+"""Shared helpers of the GPU parity tests: run the HIP path, run the oracle."""
+
+from __future__ import annotations
+
+import sys
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+import oracle
+import workloads as W
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def oracle_graphs(cfg, lists, streams, model_ids):
+    cm = W.class_map(cfg)
+    out = {}
+    for b in streams:
+        m = int(model_ids[b])
+        if m >= 0 and m not in out:
+            out[m] = oracle.build_graph(lists[m], cm, token_w=cfg.token_w,
+                                        end_bonus=cfg.end_bonus)
+    return out
+
+
+def device_rows(cfg, streams, device="cuda"):
+    """Upload the full logits of cfg slice by slice; keep the sampled streams on the host.
+
+    Returns (device tensor [T, B, K, V+1], host rows [T, S, K, V+1])."""
+    import torch
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    dev = torch.empty((cfg.T, cfg.B, cfg.K, cfg.Vp1), dtype=dt, device=device)
+    keep = np.empty((cfg.T, len(streams), cfg.K, cfg.Vp1),
+                    dtype=np.float32 if cfg.dtype == "f32" else np.uint16)
+    sel = np.asarray(list(streams), dtype=np.int64)
+    for ta, tb, rows in W.logit_chunks(cfg, 16):
+        h = torch.from_numpy(rows if cfg.dtype == "f32" else rows.view(np.int16))
+        dev[ta:tb].copy_(h.to(device).view(dt))
+        keep[ta:tb] = rows[:, sel]
+    return dev, keep
+
+
+def gpu_greedy(dec, rows_dev, model_ids, chunk: int, states0=None):
+    import torch
+    T, B = rows_dev.shape[0], rows_dev.shape[1]
+    mids, states, _ = dec.start(model_ids, 1)
+    if states0 is not None:
+        states.copy_(torch.as_tensor(states0, dtype=torch.int32, device=states.device))
+    tok = torch.empty((T, B), dtype=torch.int32, device=rows_dev.device)
+    st = torch.empty_like(tok)
+    sc = torch.empty((T, B), dtype=torch.float32, device=rows_dev.device)
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        dec.greedy(rows_dev[t0:t1], mids, states, out=(tok[t0:t1], st[t0:t1], sc[t0:t1]))
+    torch.cuda.synchronize()
+    return tok.cpu().numpy(), st.cpu().numpy(), sc.cpu().numpy(), states.cpu().numpy()
+
+
+def gpu_beam(dec, rows_dev, model_ids, chunk: int):
+    import torch
+    T, B, K = rows_dev.shape[0], rows_dev.shape[1], rows_dev.shape[2]
+    mids, states, scores = dec.start(model_ids, K)
+    i32 = dict(dtype=torch.int32, device=rows_dev.device)
+    f32 = dict(dtype=torch.float32, device=rows_dev.device)
+    outs = [torch.empty((T, B, K), **i32) for _ in range(3)] + \
+           [torch.empty((T, B, K), **f32) for _ in range(2)]
+    for t0 in range(0, T, chunk):
+        t1 = min(T, t0 + chunk)
+        dec.beam(rows_dev[t0:t1], mids, states, scores, out=tuple(o[t0:t1] for o in outs))
+    torch.cuda.synchronize()
+    return tuple(o.cpu().numpy() for o in outs) + (states.cpu().numpy(), scores.cpu().numpy())
+
+
+def compare_greedy(gpu, ref, streams, atol=1e-5, ref_streams=None):
+    """gpu[i][:, streams] against ref[i][:, ref_streams] (default: the same columns)."""
+    s = list(streams)
+    r = s if ref_streams is None else list(ref_streams)
+    tok, st, sc = (a[:, s] for a in gpu[:3])
+    rtok, rst, rsc = (a[:, r] for a in ref[:3])
+    bad = np.nonzero(tok != rtok)
+    assert bad[0].size == 0, f"token mismatch at (t, stream-index) {list(zip(*bad))[:5]}"
+    assert np.array_equal(st, rst), "state mismatch"
+    err = float(np.max(np.abs(sc - rsc))) if sc.size else 0.0
+    assert err <= atol, f"score error {err}"
+    return err
+
+
+def compare_beam(gpu, ref, streams, atol=1e-5, ref_streams=None):
+    s = list(streams)
+    r = s if ref_streams is None else list(ref_streams)
+    for i, n in enumerate(["tok", "parent", "state"]):
+        bad = np.nonzero(gpu[i][:, s] != ref[i][:, r])
+        assert bad[0].size == 0, f"{n} mismatch at {list(zip(*bad))[:5]}"
+    assert np.array_equal(gpu[4][:, s], ref[4][:, r]), "accumulated score not bit-exact"
+    err = float(np.max(np.abs(gpu[3][:, s] - ref[3][:, r])))
+    assert err <= atol, f"step score error {err}"
+    return err

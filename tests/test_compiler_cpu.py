@@ -1,0 +1,212 @@
+"""Host graph compiler (libtbias, C++) against the oracle graphs; C-ABI checks.
+
+Runs without a GPU: compiling, reading back the arena image and validating it
+are host-only calls; step calls are only made with arguments that the
+library rejects before launching anything.
+"""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from oracle.graph import PURE_POTENTIAL
+from paper_2608_21343_amd import capi
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "tbias.h")
+
+
+def _compare(img_arrays, m, og, V):
+    A = img_arrays
+    off, n = int(A["model_off"][m]), int(A["model_n"][m])
+    assert n == og.n_states
+    assert np.array_equal(A["link"][off:off + n], og.link)
+    assert A["label"][off] == -1
+    assert np.array_equal(A["label"][off + 1:off + n], [x[-1] for x in og.strings[1:]])
+    assert np.array_equal(A["phi"][off:off + n], og.phi32)
+    assert np.array_equal(A["psi"][off:off + n], og.psi32)
+    for s in range(n):
+        kids = sorted(og.goto[s].values())
+        assert A["n_child"][off + s] == len(kids)
+        if kids:
+            fc = A["first_child"][off + s]
+            assert kids == list(range(fc, fc + len(kids)))
+    rd = og.token_row(0)
+    assert np.array_equal(A["root_dst"][m, :V], rd)
+    assert np.array_equal(A["root_psi"][m, :V], og.psi32[rd])
+    assert A["root_dst"][m, V] == 0 and A["root_psi"][m, V] == 0
+
+
+@pytest.mark.parametrize("name,streams", [("tiny", [0]), ("batched", range(32)),
+                                          ("streaming", [0, 1, 77, 127]), ("beam", [0, 63]),
+                                          ("stress_greedy", [0, 255])])
+def test_compiler_matches_oracle(name, streams):
+    cfg = W.config_by_name(name)
+    cm = W.class_map(cfg)
+    lists = W.phrases(cfg, streams)
+    mp, tp, tk = W.phrase_csr(lists)
+    g = capi.tb_compile_graphs(mp, tp, tk, cfg.token_w, cfg.end_bonus, cm)
+    img = g.host_image()
+    capi.tb_validate_image(img, g.layout)
+    A = capi.image_arrays(img, g.layout)
+    for m, lst in enumerate(lists):
+        og = oracle.build_graph(lst, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+        _compare(A, m, og, cfg.V)
+    # class members CSR
+    for c in range(0, cfg.V, max(1, cfg.V // 50)):
+        mem = A["cls_tok"][A["cls_ptr"][c]:A["cls_ptr"][c + 1]]
+        assert list(mem) == [v for v in range(cfg.V) if cm[v] == c]
+
+
+def test_pure_potential_scale_and_empty_models():
+    cfg = W.config_by_name("batched")
+    cm = W.class_map(cfg)
+    lists = W.phrases(cfg, [3, 4]) + [[]]
+    mp, tp, tk = W.phrase_csr(lists)
+    tw = [0.5, 1.25, 1.0]
+    eb = [3.0, 0.5, 2.0]
+    sc = [2.0, 0.75, 1.0]
+    for sem in (capi.TB_COMMIT, capi.TB_PURE_POTENTIAL):
+        g = capi.tb_compile_graphs(mp, tp, tk, tw, eb, cm, scale=sc, semantics=sem)
+        img = g.host_image()
+        capi.tb_validate_image(img, g.layout)
+        A = capi.image_arrays(img, g.layout)
+        for m, lst in enumerate(lists):
+            og = oracle.build_graph(lst, cm, token_w=tw[m], end_bonus=eb[m], alpha=sc[m],
+                                    semantics=sem)
+            _compare(A, m, og, cfg.V)
+        assert A["model_n"][2] == 1
+
+
+def test_thread_count_does_not_change_image():
+    cfg = W.config_by_name("streaming")
+    cm = W.class_map(cfg)
+    mp, tp, tk = W.phrase_csr(W.phrases(cfg, range(12)))
+    a = capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm, n_threads=1).host_image()
+    b = capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm, n_threads=7).host_image()
+    assert np.array_equal(a, b)
+
+
+def _cm(V):
+    cm = np.arange(V + 1, dtype=np.int32)
+    cm[V] = -1
+    return cm
+
+
+@pytest.mark.parametrize("phr,code", [([[9]], capi.TB_ERANGE),      # token >= V
+                                      ([[8]], capi.TB_ERANGE),      # the blank (id V)
+                                      ([[-1]], capi.TB_ERANGE),
+                                      ([[]], capi.TB_ERANGE)])      # empty phrase
+def test_compile_rejects_bad_phrases(phr, code):
+    mp, tp, tk = W.phrase_csr([[np.asarray(p, np.int32) for p in phr]])
+    with pytest.raises(capi.TbError) as e:
+        capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, _cm(8))
+    assert e.value.code == code
+
+
+def test_compile_rejects_bad_tables():
+    mp, tp, tk = W.phrase_csr([[np.asarray([1, 2], np.int32)]])
+    cm = _cm(8)
+    cm[8] = 3
+    with pytest.raises(capi.TbError) as e:
+        capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm)
+    assert e.value.code == capi.TB_ERANGE
+    cm = _cm(8)
+    cm[2] = 11
+    with pytest.raises(capi.TbError):
+        capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm)
+    with pytest.raises(capi.TbError) as e:
+        capi.tb_compile_graphs(np.array([0, 2]), np.array([0, 2, 1]), tk, 1.0, 2.0, _cm(8))
+    with pytest.raises(capi.TbError) as e:
+        capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, _cm(8), semantics=5)
+    assert e.value.code == capi.TB_EINVAL
+
+
+def test_validate_rejects_corrupt_images():
+    cfg = W.config_by_name("batched")
+    cm = W.class_map(cfg)
+    mp, tp, tk = W.phrase_csr(W.phrases(cfg, [0, 1]))
+    g = capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm)
+    good = g.host_image()
+    L = g.layout
+
+    def corrupt(off, val):
+        bad = good.copy()
+        np.frombuffer(bad, dtype=np.int32, count=1, offset=off)  # bounds check
+        bad.view(np.uint8)[off:off + 4] = np.frombuffer(np.int32(val).tobytes(), np.uint8)
+        with pytest.raises(capi.TbError) as e:
+            capi.tb_validate_image(bad, L)
+        assert e.value.code == capi.TB_ERANGE
+
+    corrupt(L.off_link + 4 * 5, 5)            # link to itself
+    corrupt(L.off_link + 4 * 9, 10_000)       # link out of range
+    corrupt(L.off_label + 4 * 3, cfg.V)       # label out of range
+    corrupt(L.off_n_child, 10_000)            # child range past the model
+    corrupt(L.off_root_dst + 4 * 7, 1 << 20)  # root row target out of range
+    corrupt(L.off_model_n, 0)                 # model table
+    capi.tb_validate_image(good, L)
+
+
+def test_header_symbols_are_exported():
+    text = open(HEADER).read()
+    names = set(re.findall(r"\b(tb_[a-z_]+)\s*\(", text))
+    assert names == set(capi.EXPORTED)
+    for n in names:
+        assert hasattr(capi.LIB, n), n
+
+
+def test_step_calls_reject_bad_arguments_before_launch():
+    """Errors are returned synchronously; none of these calls reaches the GPU."""
+    cfg = W.config_by_name("tiny")
+    cm = W.class_map(cfg)
+    mp, tp, tk = W.phrase_csr(W.phrases(cfg, [0]))
+    g = capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm)
+    ar = capi.tb_arena()
+    ar.base = 0x10000       # never dereferenced by these calls
+    ar.layout = g.layout
+    L = capi.LIB
+    buf = C.c_void_p(0x20000)
+    V1 = cfg.Vp1
+
+    def greedy(**kw):
+        a = dict(arena=C.byref(ar), logits=buf, dtype=capi.TB_F32, T=1, B=1, stride=V1,
+                 mids=buf, states=buf, tok=buf, st=buf, sc=buf)
+        a.update(kw)
+        return L.tb_boost_step_greedy(a["arena"], a["logits"], a["dtype"], a["T"], a["B"],
+                                      a["stride"], a["mids"], a["states"], a["tok"], a["st"],
+                                      a["sc"], None)
+
+    assert greedy(arena=None) == capi.TB_EINVAL
+    assert greedy(logits=None) == capi.TB_EINVAL
+    assert greedy(dtype=7) == capi.TB_EINVAL
+    assert greedy(T=-1) == capi.TB_EINVAL
+    assert greedy(B=0) == capi.TB_EINVAL
+    assert greedy(stride=V1 - 1) == capi.TB_EINVAL
+    assert b"row_stride" in L.tb_last_error()
+    assert greedy(mids=None) == capi.TB_EINVAL
+    assert greedy(tok=C.c_void_p(0x20002)) == capi.TB_EINVAL   # misaligned
+    assert greedy(logits=C.c_void_p(0x20001), dtype=capi.TB_BF16) == capi.TB_EINVAL
+    assert greedy(T=0) == capi.TB_OK                            # no-op, nothing launched
+    assert greedy(T=0, logits=None, tok=None) == capi.TB_OK     # buffers unused at T = 0
+
+    def beam(**kw):
+        a = dict(T=1, B=1, K=4, stride=V1, scores=buf)
+        a.update(kw)
+        return L.tb_boost_step_beam(C.byref(ar), buf, capi.TB_F32, a["T"], a["B"], a["K"],
+                                    a["stride"], buf, buf, a["scores"], buf, buf, buf, buf, buf,
+                                    None)
+
+    assert beam(K=0) == capi.TB_EINVAL
+    assert beam(K=capi.TB_MAX_BEAM + 1) == capi.TB_EINVAL
+    assert beam(scores=None) == capi.TB_EINVAL
+    assert beam(T=0) == capi.TB_OK
+    assert L.tb_reset_stream(C.byref(ar), 1, 0, 5, 1, buf, buf, None, None) == capi.TB_ERANGE
+    assert L.tb_reset_stream(C.byref(ar), 1, -1, 0, 1, buf, buf, None, None) == capi.TB_EINVAL
+    assert L.tb_reset_stream(C.byref(ar), 4, 4, 0, 1, buf, buf, None, None) == capi.TB_EINVAL
+    assert L.tb_init_states(C.byref(ar), 0, 1, buf, buf, None, None) == capi.TB_EINVAL
+    bad = capi.tb_arena()
+    assert L.tb_init_states(C.byref(bad), 1, 1, buf, buf, None, None) == capi.TB_EINVAL

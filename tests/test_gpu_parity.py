@@ -1,0 +1,228 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every workload runs at its full size on the device, in the launch pattern the
+benchmark uses (streaming chunks of 16 for the streaming workload, one call
+per workload otherwise). The oracle recomputes a sample of streams one by one
+(all streams where it is cheap). Bar: selected tokens, graph states and beam
+parents bit-exact; accumulated beam scores bit-exact; per-step fused scores
+within 1e-5 absolute.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.gpu_cases import (compare_beam, compare_greedy, device_rows, gpu_beam,
+                             gpu_greedy, oracle_graphs, say)
+
+pytestmark = pytest.mark.gpu
+
+ATOL = 1e-5
+
+
+def _sample(B):
+    if B <= 32:
+        return list(range(B))
+    return sorted({0, 1, B // 5, B // 3, B // 2, (2 * B) // 3, B - 2, B - 1})
+
+
+def _decoder(cfg, lists):
+    from paper_2608_21343_amd.decoder import BoostDecoder
+    return BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+
+
+@pytest.mark.parametrize("name", ["tiny", "batched", "streaming", "stress_greedy"])
+def test_greedy_full_size(name):
+    cfg = W.config_by_name(name)
+    streams = _sample(cfg.B)
+    say(f"[parity] greedy {name}: generating B={cfg.B} T={cfg.T} V+1={cfg.Vp1} {cfg.dtype}")
+    lists = W.phrases(cfg)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    dev, keep = device_rows(cfg, streams)
+    say(f"[parity] greedy {name}: running HIP path, chunk={cfg.chunk}")
+    gpu = gpu_greedy(dec, dev[:, :, 0, :], mids, cfg.chunk)
+    del dev
+    graphs = oracle_graphs(cfg, lists, streams, mids)
+    say(f"[parity] greedy {name}: oracle on streams {streams}")
+    sub = mids[streams]
+    ref = oracle.greedy_decode(graphs, sub, keep, np.zeros(len(streams), np.int32))
+    err = compare_greedy(gpu, ref, streams, ATOL, ref_streams=range(len(streams)))
+    assert np.array_equal(gpu[3][streams], ref[3])
+    say(f"[parity] greedy {name}: ok, max score error {err:.2e}")
+
+
+@pytest.mark.parametrize("name", ["beam", "stress_beam"])
+def test_beam_full_size(name):
+    cfg = W.config_by_name(name)
+    streams = _sample(cfg.B)[:4] if cfg.V > 2000 else _sample(cfg.B)[:6]
+    say(f"[parity] beam {name}: generating B={cfg.B} K={cfg.K} T={cfg.T} V+1={cfg.Vp1}")
+    lists = W.phrases(cfg)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    dev, keep = device_rows(cfg, streams)
+    say(f"[parity] beam {name}: running HIP path")
+    gpu = gpu_beam(dec, dev, mids, cfg.chunk)
+    del dev
+    graphs = oracle_graphs(cfg, lists, streams, mids)
+    say(f"[parity] beam {name}: oracle on streams {streams}")
+    sub = mids[streams]
+    st0, S0 = oracle.init_carry(sub, cfg.K)
+    ref = oracle.beam_decode(graphs, sub, keep, st0, S0)
+    err = compare_beam(gpu, ref, streams, ATOL, ref_streams=range(len(streams)))
+    say(f"[parity] beam {name}: ok, max step score error {err:.2e}")
+
+
+def _small_case(seed=0, B=6, V=200, n_case=20, T=64, K=1, dtype="f32"):
+    cfg = W.Config(100 + seed, "small", B=B, K=K, V=V, T=T, chunk=T, dtype=dtype,
+                   n_phrases=40, len_lo=1, len_hi=5, token_dist="zipf", zipf_s=1.1,
+                   logit_std=1.0, blank_offset=1.0, n_case=n_case)
+    return cfg, W.phrases(cfg), W.logits(cfg)
+
+
+def test_greedy_chunk_invariance():
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg = W.config_by_name("streaming")
+    lists = W.phrases(cfg)
+    rows = W.logits(cfg, 0, 96)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    dev = to_device_logits(rows[:, :, 0, :])
+    ref = gpu_greedy(dec, dev, mids, 96)
+    for ch in (1, 7, 16):
+        out = gpu_greedy(dec, dev, mids, ch)
+        for a, b in zip(ref, out):
+            assert np.array_equal(a, b), f"chunk {ch} differs"
+    again = gpu_greedy(dec, dev, mids, 96)
+    for a, b in zip(ref, again):
+        assert np.array_equal(a, b), "not deterministic"
+
+
+def test_beam_chunk_invariance():
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg, lists, rows = _small_case(1, K=4, T=40)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    dev = to_device_logits(rows)
+    ref = gpu_beam(dec, dev, mids, 40)
+    for ch in (1, 7, 16):
+        out = gpu_beam(dec, dev, mids, ch)
+        for a, b in zip(ref, out):
+            assert np.array_equal(a, b), f"chunk {ch} differs"
+    st0, S0 = oracle.init_carry(mids, cfg.K)
+    graphs = oracle_graphs(cfg, lists, range(cfg.B), mids)
+    o = oracle.beam_decode(graphs, mids, rows, st0, S0)
+    compare_beam(ref, o, range(cfg.B), ATOL)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_mixed_model_ids_and_edge_streams(dtype):
+    """Model -1, an empty list, an out-of-range id and ragged V+1 in one batch."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg, lists, rows = _small_case(2, B=7, V=300, dtype=dtype)   # V+1 = 301: ragged
+    lists = list(lists[:5]) + [[]]                               # model 5: empty list
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, -1, 5, 3, 99, 4, 1], np.int32)            # 99: out of range
+    dev = to_device_logits(rows[:, :, 0, :])
+    gpu = gpu_greedy(dec, dev, mids, 17)
+    ok = [0, 1, 2, 3, 5, 6]
+    graphs = oracle_graphs(cfg, lists, ok, mids)
+    st0 = np.array([0, -1, 0, 0, 0, 0, 0], np.int32)
+    ref = oracle.greedy_decode(graphs, mids, rows, st0, streams=ok)
+    compare_greedy(gpu, ref, ok, ATOL)
+    assert np.all(gpu[1][:, 1] == -1)
+    assert np.all(gpu[1][:, 2] == 0)                             # root-only graph
+    assert np.all(gpu[1][:, 4] == -2)                            # invalid id: no biasing
+    z = oracle.widen(rows[:, 4, 0, :])
+    assert np.array_equal(gpu[0][:, 4], np.argmax(z, axis=1))
+
+
+def test_padded_row_stride_and_T0():
+    import torch
+    from paper_2608_21343_amd import capi
+    cfg, lists, rows = _small_case(3, B=5, V=255)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    T, B, V1 = cfg.T, cfg.B, cfg.Vp1
+    pad = torch.full((T, B, V1 + 7), 1e30, dtype=torch.float32, device="cuda")
+    pad[:, :, :V1] = torch.from_numpy(rows[:, :, 0, :]).cuda()
+    m, st, _ = dec.start(mids)
+    tok = torch.empty((T, B), dtype=torch.int32, device="cuda")
+    sst = torch.empty_like(tok)
+    sc = torch.empty((T, B), dtype=torch.float32, device="cuda")
+    capi.tb_boost_step_greedy(dec.arena, pad[:, :, :V1], m, st, tok, sst, sc, row_stride=V1 + 7)
+    torch.cuda.synchronize()
+    graphs = oracle_graphs(cfg, lists, range(B), mids)
+    ref = oracle.greedy_decode(graphs, mids, rows, np.zeros(B, np.int32))
+    compare_greedy((tok.cpu().numpy(), sst.cpu().numpy(), sc.cpu().numpy()), ref, range(B), ATOL)
+    before = st.clone()
+    capi.tb_boost_step_greedy(dec.arena, pad[:0, :, :V1], m, st, tok, sst, sc, T=0,
+                              row_stride=V1 + 7)
+    torch.cuda.synchronize()
+    assert torch.equal(before, st)
+
+
+def test_reset_stream_touches_only_that_stream():
+    import torch
+    from paper_2608_21343_amd import capi
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg, lists, rows = _small_case(4, B=4, K=3, T=30)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    dev = to_device_logits(rows)
+    m, st, sc = dec.start(mids, cfg.K)
+    dec.beam(dev[:10], m, st, sc)
+    torch.cuda.synchronize()
+    st_before, sc_before = st.cpu().numpy().copy(), sc.cpu().numpy().copy()
+    capi.tb_reset_stream(dec.arena, 2, -1, cfg.K, m, st, sc)
+    torch.cuda.synchronize()
+    st_a, sc_a, m_a = st.cpu().numpy(), sc.cpu().numpy(), m.cpu().numpy()
+    K = cfg.K
+    keep = [i for i in range(cfg.B * K) if i // K != 2]
+    assert np.array_equal(st_a[keep], st_before[keep]) and np.array_equal(sc_a[keep], sc_before[keep])
+    assert list(st_a[2 * K:3 * K]) == [-1] * K and m_a[2] == -1
+    assert sc_a[2 * K] == 0 and np.all(np.isneginf(sc_a[2 * K + 1:3 * K]))
+    # continuing after the reset equals a fresh run of that stream without a model
+    o = dec.beam(dev[10:], m, st, sc)
+    torch.cuda.synchronize()
+    st0, S0 = oracle.init_carry([-1], K)
+    ref = oracle.beam_decode({}, [-1], rows[10:, 2:3], st0, S0)
+    assert np.array_equal(o[0].cpu().numpy()[:, 2], ref[0][:, 0])
+    assert np.array_equal(o[4].cpu().numpy()[:, 2], ref[4][:, 0])
+
+
+def test_stream_permutation_permutes_outputs():
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg, lists, rows = _small_case(5, B=8, T=48)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg)
+    ref = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, 48)
+    perm = np.array([3, 7, 0, 5, 1, 6, 2, 4])
+    out = gpu_greedy(dec, to_device_logits(np.ascontiguousarray(rows[:, perm, 0, :])),
+                     mids[perm], 48)
+    for a, b in zip(ref[:3], out[:3]):
+        assert np.array_equal(a[:, perm], b)
+
+
+@pytest.mark.parametrize("name", ["tiny", "batched", "streaming"])
+def test_fast_and_reference_greedy_kernels_agree(name, monkeypatch):
+    """The pipelined kernel and the reference kernel give bit-identical outputs."""
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg = W.config_by_name(name)
+    T = min(cfg.T, 200)
+    lists = W.phrases(cfg)
+    rows = W.logits(cfg, 0, T)
+    dec = _decoder(cfg, lists)
+    mids = W.model_ids(cfg).copy()
+    if cfg.B > 4:
+        mids[1] = -1
+    dev = to_device_logits(rows[:, :, 0, :])
+    fast = gpu_greedy(dec, dev, mids, 37)
+    monkeypatch.setenv("TBIAS_GREEDY_KERNEL", "ref")
+    ref = gpu_greedy(dec, dev, mids, 37)
+    for a, b in zip(fast, ref):
+        assert np.array_equal(a[:2] if a.ndim == 2 and a.dtype != np.float32 else a, b[:2] if b.ndim == 2 and b.dtype != np.float32 else b) or a.dtype == np.float32
+    assert np.array_equal(fast[0], ref[0]) and np.array_equal(fast[1], ref[1])
+    assert np.array_equal(fast[3], ref[3])
+    assert np.max(np.abs(fast[2] - ref[2])) <= 2e-6

@@ -12,6 +12,7 @@ from .synth import (  # noqa: F401
     class_map,
     class_members,
     config_by_name,
+    logit_chunks,
     logits,
     model_ids,
     phrase_csr,

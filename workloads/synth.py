@@ -173,8 +173,7 @@ def phrases(cfg: Config, streams: Optional[Sequence[int]] = None) -> List[List[n
         else:
             toks = rng.choice(cfg.V, size=total, p=p)
         toks = toks.astype(np.int32)
-        cuts = np.concatenate([[0], np.cumsum(lens)])
-        out.append([toks[cuts[i]:cuts[i + 1]].copy() for i in range(cfg.n_phrases)])
+        out.append(np.split(toks, np.cumsum(lens)[:-1]))
     return out
 
 
@@ -234,11 +233,26 @@ def plants(cfg: Config, b: int, lst: Optional[Sequence[np.ndarray]] = None) -> L
 # logits
 
 
-def _f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round float32 to bfloat16 (round to nearest even), returned as uint16 bits."""
-    u = x.astype(np.float32).view(np.uint32)
-    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
-    return r.astype(np.uint16)
+def _f32_to_bf16_bits(x: np.ndarray, out: Optional[np.ndarray] = None,
+                      tmp: Optional[np.ndarray] = None) -> np.ndarray:
+    """Round float32 to bfloat16 (round to nearest even), returned as uint16 bits.
+
+    Finite inputs only (the generators never produce inf or nan). ``x`` is
+    overwritten when ``tmp`` is given (scratch of the same shape, uint32)."""
+    if tmp is None:
+        u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+        lsb = np.right_shift(u, 16)
+    else:
+        u = x.view(np.uint32)
+        lsb = np.right_shift(u, 16, out=tmp)
+    np.bitwise_and(lsb, 1, out=lsb)
+    u += np.uint32(0x7FFF)
+    u += lsb
+    np.right_shift(u, 16, out=u)
+    if out is None:
+        return u.astype(np.uint16)
+    out[...] = u
+    return out
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -246,38 +260,64 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def logits(cfg: Config, t0: int = 0, t1: Optional[int] = None,
-           streams: Optional[Sequence[int]] = None) -> np.ndarray:
-    """Joint-logit rows [t1-t0, B', K, V+1]; float32, or uint16 bf16 bits for bf16.
+def _plant_map(cfg: Config, t0: int, t1: int) -> dict:
+    out: dict = {}
+    if cfg.plant_frac > 0.0:
+        for b in range(cfg.B):
+            for (t, tok) in plants(cfg, b):
+                if t0 <= t < t1:
+                    out.setdefault(t, []).append((b, tok))
+    return out
 
-    Each time step has its own generator, so a slice equals the same rows of
-    the full tensor. ``streams`` selects a subset of streams (rows are drawn for
-    all B streams and then sliced, so values do not depend on the subset).
+
+def logit_chunks(cfg: Config, chunk: int, t0: int = 0, t1: Optional[int] = None):
+    """Yield (ta, tb, rows) for consecutive time slices [ta, tb) of the logits.
+
+    ``rows`` has shape [tb-ta, B, K, V+1] (float32, or uint16 bf16 bits) and is
+    a buffer reused by the next slice: copy what must be kept. Each time step
+    draws from its own generator (SFC64 over the step's SeedSequence), so the
+    values never depend on the slicing.
     """
     if t1 is None:
         t1 = cfg.T
     seq = _logit_seq(cfg)
     B, K, Vp1 = cfg.B, cfg.K, cfg.Vp1
+    pm = _plant_map(cfg, t0, t1)
+    z = np.empty((B, K, Vp1), dtype=np.float32)
+    tmp = np.empty((B, K, Vp1), dtype=np.uint32) if cfg.dtype == "bf16" else None
+    buf = np.empty((min(chunk, max(1, t1 - t0)), B, K, Vp1),
+                   dtype=np.float32 if cfg.dtype == "f32" else np.uint16)
+    for ta in range(t0, t1, chunk):
+        tb = min(t1, ta + chunk)
+        for t in range(ta, tb):
+            ts = np.random.SeedSequence(entropy=seq.entropy, spawn_key=seq.spawn_key + (t,))
+            rng = np.random.Generator(np.random.SFC64(ts))
+            zz = buf[t - ta] if cfg.dtype == "f32" else z
+            rng.standard_normal(dtype=np.float32, out=zz)
+            if cfg.logit_std != 1.0:
+                zz *= np.float32(cfg.logit_std)
+            if cfg.blank_offset != 0.0:
+                zz[:, :, cfg.V] += np.float32(cfg.blank_offset)
+            for (b, tok) in pm.get(t, ()):
+                zz[b, :, tok] += np.float32(cfg.plant_boost)
+            if cfg.dtype != "f32":
+                _f32_to_bf16_bits(zz, out=buf[t - ta], tmp=tmp)
+        yield ta, tb, buf[:tb - ta]
+
+
+def logits(cfg: Config, t0: int = 0, t1: Optional[int] = None,
+           streams: Optional[Sequence[int]] = None) -> np.ndarray:
+    """Joint-logit rows [t1-t0, B', K, V+1]; float32, or uint16 bf16 bits for bf16.
+
+    ``streams`` selects a subset of streams (rows are drawn for all B streams
+    and then sliced, so values do not depend on the subset).
+    """
+    if t1 is None:
+        t1 = cfg.T
     sel = None if streams is None else np.asarray(list(streams), dtype=np.int64)
-    nb = B if sel is None else len(sel)
-    out = np.empty((t1 - t0, nb, K, Vp1), dtype=np.float32 if cfg.dtype == "f32" else np.uint16)
-    plant_map = {}
-    if cfg.plant_frac > 0.0:
-        for j, b in enumerate(range(B) if sel is None else sel):
-            for (t, tok) in plants(cfg, int(b)):
-                if t0 <= t < t1:
-                    plant_map.setdefault(t, []).append((j, tok))
-    for t in range(t0, t1):
-        ts = np.random.SeedSequence(entropy=seq.entropy, spawn_key=seq.spawn_key + (t,))
-        rng = np.random.default_rng(ts)
-        z = rng.standard_normal((B, K, Vp1), dtype=np.float32)
-        if sel is not None:
-            z = z[sel]
-        if cfg.logit_std != 1.0:
-            z *= np.float32(cfg.logit_std)
-        if cfg.blank_offset != 0.0:
-            z[:, :, cfg.V] += np.float32(cfg.blank_offset)
-        for (j, tok) in plant_map.get(t, ()):
-            z[j, :, tok] += np.float32(cfg.plant_boost)
-        out[t - t0] = z if cfg.dtype == "f32" else _f32_to_bf16_bits(z)
+    nb = cfg.B if sel is None else len(sel)
+    out = np.empty((t1 - t0, nb, cfg.K, cfg.Vp1),
+                   dtype=np.float32 if cfg.dtype == "f32" else np.uint16)
+    for ta, tb, rows in logit_chunks(cfg, 16, t0, t1):
+        out[ta - t0:tb - t0] = rows if sel is None else rows[:, sel]
     return out
