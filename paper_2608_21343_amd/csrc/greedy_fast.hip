@@ -2,24 +2,23 @@
 //
 // The greedy decode of one stream is a chain: the state after step t depends
 // on the token chosen at step t, which depends on the state. Everything that
-// does not depend on the state is taken off that chain:
+// does not depend on the state is taken off that chain, and the state-
+// dependent part is precomputed for the states the stream is likely in:
 //
-//  * 4 loader waves stream the logit rows into a ring of LDS slots (row t
-//    belongs to loader t % 4, three rows in flight per loader, non-temporal
-//    loads); loaders issue no other memory traffic, so nothing waits behind
-//    their loads.
-//  * 11 compute waves take the rows from LDS and compute per row the
-//    log-softmax normaliser and the best root move
-//    r1 = argmax_v z[v] + psi[root move of v] (ties to the lowest v, blank
-//    excluded).
-//  * They also evaluate the complete step from two predicted states and store
-//    both answers: x1 = the root-move target of r1 of the previous row, and
-//    x2 = the answer of the previous row's x1 evaluation (at the first row of
-//    a call x1 is the carried state itself). A stream that follows the best
-//    root move, or did so one step earlier, is in one of these states.
-//  * One consumer wave (raised issue priority) walks the chain: when the
-//    stream's state is x1 or x2 the step is a compare and a select;
-//    otherwise it evaluates the step itself with the same routine.
+//  * 5 loader waves stream the logit rows (row t belongs to loader t % 5,
+//    three rows in flight per loader) and compute per row the log-softmax
+//    normaliser and the best root move r1 = argmax_v z[v] + psi[root move of
+//    v] (ties to the lowest v, blank excluded) into a ring of row summaries in
+//    LDS. The rows themselves stay in global memory (and L2), where the
+//    evaluations below read the few logits they need.
+//  * 10 compute waves evaluate the complete step from up to three predicted
+//    states: x1 = the root-move target of r1 of the previous row (the carried
+//    state itself at the first row of a call), x2 = the answer from x1 of the
+//    previous row, x3 = the answer from x2 of the previous row. The outputs of
+//    the x1 answer are written speculatively.
+//  * One consumer wave (raised issue priority) walks the chain: in state x1
+//    the step is a compare (its outputs are already written); in x2 or x3 it
+//    writes that answer; otherwise it evaluates the step itself.
 //
 // Evaluating a step from state x (the suffix-link traversal of the boosting
 // graph): the children of x, link(x), ... (excluding the root) override the
@@ -27,12 +26,13 @@
 // 8-bit tags marks the classes already claimed. The candidates are every
 // override class (its best case variant in the row), the best root move whose
 // class is not overridden, and the blank (z[V] + phi[x]); the largest key
-// wins, ties to the lowest token id.
+// wins, ties to the lowest token id. The records of the first states
+// (breadth-first ids, so the shallow ones) are cached in LDS for long calls.
 //
 // LDS is a static struct sized by the template (all addressing constant
-// offset). Producers and consumer hand rows over through per-slot flags
-// holding the row index. Every wait is bounded; on exhaustion the stream's
-// outputs are marked with state -3.
+// offset). Waves hand rows over through per-slot flags holding the row index,
+// written after the data they guard and read before it. Every wait is
+// bounded; on exhaustion the stream's outputs are marked with state -3.
 #include <climits>
 
 #include "device.hpp"
@@ -42,8 +42,9 @@ namespace tbias {
 
 namespace {
 
-constexpr int kWaves = 16;                // wave 0 consumer, 1..4 loaders, 5..15 computers
-constexpr int kLoaders = 4;
+constexpr int kWaves = 16;                // wave 0 consumer, 1..5 loaders, 6..15 computers
+constexpr int kConsumerAhead = 4;         // summaries the consumer keeps in flight
+constexpr int kLoaders = 5;
 constexpr int kLoadDepth = 3;             // rows in flight per loader (vmcnt budget)
 constexpr int kComputers = kWaves - 1 - kLoaders;
 constexpr int kThreads = 64 * kWaves;
@@ -52,28 +53,28 @@ constexpr int32_t kStateTimeout = -3;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 // states cached in LDS (ids < HOT): smaller for the largest rows to fit 160 KB
-constexpr int hot_states(int per) { return per <= 17 ? 2048 : 1024; }
+constexpr int hot_states(int per) { return per <= 17 ? 4096 : 2048; }
 constexpr int32_t kHotMinT = 64;          // shorter calls read the graph from global memory
 
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
-// One row's summary. c0.x is the "fully ready" flag (row index); it is read
-// first, so the chunks read after it are complete.
+// One row's summary. `ready` (row index) is written after everything else
+// and read before it.
 struct alignas(16) RowSum {
-  v4i c0;  // ready, lse, zb, x1
-  v4i c1;  // tok1, ns1, b1, zv1
-  v4i c2;  // x2, tok2, ns2, b2
-  v4i c3;  // zv2, r1_y, r1_tok, r1_dst
-  v4i c4;  // r1_cls, -, -, -
+  v4i c0;  // ready, x1, ns1, x2
+  v4i c1;  // ns2, tok2, b2, zv2
+  v4i c2;  // x3, ns3, tok3, b3
+  v4i c3;  // zv3, lse, zb, r1_tok
+  v4i c4;  // r1_y, r1_dst, r1_cls, -
 };
 
 template <class TT, int PER, int NSLOT>
 struct alignas(16) Lds {
-  TT z[NSLOT][64 * PER];          // logit rows (ring)
   RowSum sum[NSLOT];
-  int32_t loaded[NSLOT];          // row whose logits are in the slot
-  int32_t a_flag[NSLOT];          // row whose r1 is published
+  int32_t ready[NSLOT];           // row whose summary is complete
+  int32_t a_flag[NSLOT];          // row whose normaliser and r1 are published
   int32_t p1_flag[NSLOT];         // row whose x1 answer is published
+  int32_t p2_flag[NSLOT];         // row whose x2 answer is published
   int32_t freed;                  // rows < freed may be overwritten
   int32_t abort_flag;
   float rpsi[64 * PER];           // psi of the root move; -inf for blank and padding
@@ -150,14 +151,14 @@ __device__ __forceinline__ float rlf(float v, int32_t lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// The boosted step from state x on the row in `slot`, given that row's best
-// root move. All lanes take part; the result is uniform.
+// The boosted step from state x on logit row zrow (global memory), given that
+// row's best root move. All lanes take part; the result is uniform.
 template <class Ld, class L>
-__device__ Answer eval_state(const ArenaView& A, int32_t off, L& S, int32_t slot, int32_t x,
+__device__ Answer eval_state(const ArenaView& A, int32_t off, L& S,
+                             const typename Ld::T* __restrict__ zrow, int32_t x,
                              float zb, float r1_y, int32_t r1_tok, int32_t r1_dst, int32_t r1_cls,
                              int wave, uint32_t& tag, int32_t V, int32_t nhot) {
   const int lane = __lane_id();
-  const auto* zrow = S.z[slot];
   uint8_t* stamps = S.stamps[wave];
   if (++tag == 256u) {  // 8-bit tags: clear this wave's table on wrap
     uint32_t* w = reinterpret_cast<uint32_t*>(stamps);
@@ -290,9 +291,10 @@ __global__ __launch_bounds__(kThreads) void greedy_fast_kernel(
   }
   for (int32_t i = threadIdx.x; i < NSLOT; i += kThreads) {
     S.sum[i].c0.x = -1;
-    S.loaded[i] = -1;
+    S.ready[i] = -1;
     S.a_flag[i] = -1;
     S.p1_flag[i] = -1;
+    S.p2_flag[i] = -1;
   }
   if (threadIdx.x == 0) {
     S.freed = 0;
@@ -307,68 +309,82 @@ __global__ __launch_bounds__(kThreads) void greedy_fast_kernel(
   if (wave == 0) {
     // ------------------------------------------------------------ consumer
     __builtin_amdgcn_s_setprio(3);
-    int32_t s = s0;
+    // unbiased streams never leave their constant state
+    int32_t s = (mode == 1) ? s0 : ((mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID);
     bool ok = true;
-    int32_t o_tok = 0, o_st = 0;
-    float o_sc = 0.f;
-    v4i c0 = vload4(&S.sum[0].c0);
-    v4i c1 = S.sum[0].c1, c2 = S.sum[0].c2;
-    for (int32_t t = 0; t < T; ++t) {
-      const int32_t slot = t % NSLOT;
-      uint32_t spins = 0;
-      while (__builtin_amdgcn_readfirstlane(c0.x) != t) {
-        if (vload(&S.abort_flag) || ++spins > 64u * kSpinLimit) { ok = false; break; }
-        c0 = vload4(&S.sum[slot].c0);
-        c1 = S.sum[slot].c1;
-        c2 = S.sum[slot].c2;
-      }
-      if (!ok) break;
-      // the summary is uniform: move it to scalar registers
-      const float lse = __int_as_float(__builtin_amdgcn_readfirstlane(c0.y));
-      const float zb = __int_as_float(__builtin_amdgcn_readfirstlane(c0.z));
-      const int32_t x1 = __builtin_amdgcn_readfirstlane(c0.w);
-      const int32_t x2 = __builtin_amdgcn_readfirstlane(c2.x);
-      const v4i h1 = c1, h2 = c2;
-      // prefetch the next row's summary (checked at the top of the next step)
-      const int32_t nslot = (t + 1) % NSLOT;
-      c0 = vload4(&S.sum[nslot].c0);
-      c1 = S.sum[nslot].c1;
-      c2 = S.sum[nslot].c2;
-      Answer a;
-      if (s == x1) {
-        a.tok = __builtin_amdgcn_readfirstlane(h1.x);
-        a.ns = __builtin_amdgcn_readfirstlane(h1.y);
-        a.b = __int_as_float(__builtin_amdgcn_readfirstlane(h1.z));
-        a.zv = __int_as_float(__builtin_amdgcn_readfirstlane(h1.w));
-      } else if (s == x2) {
-        a.tok = __builtin_amdgcn_readfirstlane(h2.y);
-        a.ns = __builtin_amdgcn_readfirstlane(h2.z);
-        a.b = __int_as_float(__builtin_amdgcn_readfirstlane(h2.w));
-        a.zv = __int_as_float(__builtin_amdgcn_readfirstlane(S.sum[slot].c3.x));
-      } else {
-        const v4i c3 = S.sum[slot].c3;
-        const int32_t r1_cls = __builtin_amdgcn_readfirstlane(S.sum[slot].c4.x);
-        a = eval_state<Ld>(A, off, S, slot, s, zb, __int_as_float(__builtin_amdgcn_readfirstlane(c3.y)),
-                           __builtin_amdgcn_readfirstlane(c3.z), __builtin_amdgcn_readfirstlane(c3.w),
-                           r1_cls, 0, tag, V, nhot);
-      }
-      // lane (t % 64) keeps step t; one store per 64 steps
-      const int32_t ln = t & 63;
-      const float sc = (a.zv - lse) + a.b;
-      const bool mine = lane == ln;
-      o_tok = mine ? a.tok : o_tok;
-      o_st = mine ? a.ns : o_st;
-      o_sc = mine ? sc : o_sc;
-      if (ln == 63 || t == T - 1) {
-        if (lane <= ln) {
-          const int64_t oi = (int64_t)(t - ln + lane) * B + b;
-          out_tok[oi] = o_tok;
-          out_state[oi] = o_st;
-          out_score[oi] = o_sc;
+    // summaries of the next kConsumerAhead rows: the ready flag is read
+    // before the data, so a flag equal to the row index vouches for the data
+    int32_t pf[kConsumerAhead];
+    v4i pd[kConsumerAhead];
+#pragma unroll
+    for (int k = 0; k < kConsumerAhead; ++k) {
+      pf[k] = vload(&S.ready[k % NSLOT]);
+      cbar();
+      pd[k] = S.sum[k % NSLOT].c0;
+      cbar();
+    }
+    for (int32_t t0 = 0; t0 < T && ok; t0 += kConsumerAhead) {
+#pragma unroll
+      for (int k = 0; k < kConsumerAhead; ++k) {
+        const int32_t t = t0 + k;
+        if (t < T && ok) {
+          const int32_t slot = t % NSLOT;
+          uint32_t spins = 0;
+          while (__builtin_amdgcn_readfirstlane(pf[k]) != t) {
+            if (vload(&S.abort_flag) || ++spins > 64u * kSpinLimit) { ok = false; break; }
+            pf[k] = vload(&S.ready[slot]);
+            cbar();
+            pd[k] = S.sum[slot].c0;
+            cbar();
+          }
+          if (ok) {
+            const int32_t x1 = __builtin_amdgcn_readfirstlane(pd[k].y);
+            const int32_t ns1 = __builtin_amdgcn_readfirstlane(pd[k].z);
+            const int32_t x2 = __builtin_amdgcn_readfirstlane(pd[k].w);
+            // refill this prefetch slot with row t + kConsumerAhead
+            const int32_t nslot = (t + kConsumerAhead) % NSLOT;
+            pf[k] = vload(&S.ready[nslot]);
+            cbar();
+            pd[k] = S.sum[nslot].c0;
+            cbar();
+            if (s == x1 || mode != 1) {
+              s = ns1;  // the x1 answer's outputs are already written
+            } else {
+              const RowSum& rs = S.sum[slot];
+              const TT* zrow = logits + ((int64_t)t * B + b) * stride;
+              const v4i c1 = rs.c1, c2 = rs.c2, c3 = rs.c3, c4 = rs.c4;
+              const float lse = __int_as_float(__builtin_amdgcn_readfirstlane(c3.y));
+              Answer a;
+              if (s == x2) {
+                a.ns = __builtin_amdgcn_readfirstlane(c1.x);
+                a.tok = __builtin_amdgcn_readfirstlane(c1.y);
+                a.b = __int_as_float(__builtin_amdgcn_readfirstlane(c1.z));
+                a.zv = __int_as_float(__builtin_amdgcn_readfirstlane(c1.w));
+              } else if (s == __builtin_amdgcn_readfirstlane(c2.x)) {
+                a.ns = __builtin_amdgcn_readfirstlane(c2.y);
+                a.tok = __builtin_amdgcn_readfirstlane(c2.z);
+                a.b = __int_as_float(__builtin_amdgcn_readfirstlane(c2.w));
+                a.zv = __int_as_float(__builtin_amdgcn_readfirstlane(c3.x));
+              } else {
+                a = eval_state<Ld>(A, off, S, zrow, s,
+                                   __int_as_float(__builtin_amdgcn_readfirstlane(c3.z)),
+                                   __int_as_float(__builtin_amdgcn_readfirstlane(c4.x)),
+                                   __builtin_amdgcn_readfirstlane(c3.w),
+                                   __builtin_amdgcn_readfirstlane(c4.y),
+                                   __builtin_amdgcn_readfirstlane(c4.z), 0, tag, V, nhot);
+              }
+              if (lane == 0) {
+                const int64_t oi = (int64_t)t * B + b;
+                out_tok[oi] = a.tok;
+                out_state[oi] = a.ns;
+                out_score[oi] = (a.zv - lse) + a.b;
+              }
+              s = __builtin_amdgcn_readfirstlane(a.ns);
+            }
+            if (lane == 0) vstore(&S.freed, t);  // rows < t may be overwritten
+          }
         }
       }
-      s = __builtin_amdgcn_readfirstlane(a.ns);
-      if (lane == 0) vstore(&S.freed, t);  // rows < t may be overwritten
     }
     if (ok) {
       if (lane == 0 && T > 0) states[b] = s;
@@ -385,15 +401,18 @@ __global__ __launch_bounds__(kThreads) void greedy_fast_kernel(
     // rows t = li, li + kLoaders, ...; kLoadDepth rows in flight in registers
     const int li = wave - 1;
     float buf[kLoadDepth][PER];
+    float rp[PER];  // root-move psi of this lane's tokens (-inf past V - 1)
+#pragma unroll
+    for (int j = 0; j < PER; ++j) rp[j] = S.rpsi[64 * j + lane];
     auto issue = [&](float* dst, int32_t tr) {
       const TT* row = logits + ((int64_t)tr * B + b) * stride;
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const int32_t v = 64 * j + lane;
         if (64 * (j + 1) <= V1) {  // uniform: the whole wave is inside the row
-          dst[j] = Ld::get_nt(row, v);
+          dst[j] = Ld::get(row, v);
         } else {
-          dst[j] = (v < V1) ? Ld::get_nt(row, v) : kNegInf;
+          dst[j] = (v < V1) ? Ld::get(row, v) : kNegInf;
         }
       }
     };
@@ -410,18 +429,45 @@ __global__ __launch_bounds__(kThreads) void greedy_fast_kernel(
           const int32_t slot = t % NSLOT;
           // the slot held row t - NSLOT: wait until the consumer is past row t - NSLOT + 1
           if (!wait_flag(&S.freed, t - NSLOT + 1, true, &S.abort_flag)) return;
+          const float* cur = buf[k];
+          // ---- normaliser and best root move (padding past V+1 is -inf)
+          float ymax = kNegInf;
+          float zb = 0.f;
 #pragma unroll
           for (int j = 0; j < PER; ++j) {
-            const int32_t v = 64 * j + lane;
-            if (sizeof(TT) == 4) {
-              reinterpret_cast<float*>(S.z[slot])[v] = buf[k][j];
-            } else {
-              reinterpret_cast<uint16_t*>(S.z[slot])[v] =
-                  (uint16_t)(__float_as_uint(buf[k][j]) >> 16);
-            }
+            const float yj = cur[j] + rp[j];
+            ymax = ymax > yj ? ymax : yj;
+            if (j == (V >> 6)) zb = rlf(cur[j], V & 63);
+          }
+          ymax = wave_max_dpp(ymax);
+          const float mref = ymax > zb ? ymax : zb;
+          const float mL = mref * kLog2e;
+          float se = 0.f;
+#pragma unroll
+          for (int j = 0; j < PER; ++j)
+            se += __builtin_amdgcn_exp2f(__builtin_fmaf(cur[j], kLog2e, -mL));
+          se = wave_sum_dpp(se);
+          const float lse = mref + __logf(se);
+          int32_t hit = INT_MAX;
+#pragma unroll
+          for (int j = PER - 1; j >= 0; --j) {
+            const float yj = cur[j] + rp[j];
+            hit = (yj == ymax) ? 64 * j + lane : hit;
+          }
+          int32_t r1_tok = wave_min_i32_dpp(hit);
+          if (r1_tok >= V) r1_tok = 0;  // only with -inf / nan logits: keep indices in range
+          const int32_t r1_dst = S.rdst[r1_tok];
+          const int32_t c16 = S.cls[r1_tok];
+          const int32_t r1_cls = (c16 == 0xffff) ? -1 : c16;
+          RowSum& rs = S.sum[slot];
+          if (lane == 0) {
+            rs.c3.y = __float_as_int(lse);
+            rs.c3.z = __float_as_int(zb);
+            rs.c3.w = r1_tok;
+            rs.c4 = v4i{__float_as_int(ymax), r1_dst, r1_cls, 0};
           }
           lds_fence();
-          if (lane == 0) vstore(&S.loaded[slot], t);
+          if (lane == 0) vstore(&S.a_flag[slot], t);
           const int32_t tn = t + kLoadDepth * kLoaders;
           if (tn < T) issue(buf[k], tn);
         }
@@ -433,100 +479,97 @@ __global__ __launch_bounds__(kThreads) void greedy_fast_kernel(
   // -------------------------------------------------------------- computers
   for (int32_t t = wave - 1 - kLoaders; t < T; t += kComputers) {
     const int32_t slot = t % NSLOT;
-    if (!wait_flag(&S.loaded[slot], t, false, &S.abort_flag)) return;
-
-    // ---- normaliser and best root move of row t
-    constexpr bool kKeepY = PER <= 17;  // larger rows recompute y to stay within 128 VGPRs
-    // the loaders pad every slot past V+1 with -inf, and rpsi is -inf past
-    // V - 1, so the whole 64*PER range is read without guards
-    float cur[PER];
-    float y[kKeepY ? PER : 1];
-    float ymax = kNegInf;
-    const float zb = Ld::get(S.z[slot], V);
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int32_t v = 64 * j + lane;
-      cur[j] = Ld::get(S.z[slot], v);
-      const float yj = cur[j] + S.rpsi[v];
-      if (kKeepY) y[kKeepY ? j : 0] = yj;
-      ymax = ymax > yj ? ymax : yj;
-    }
-    ymax = wave_max_dpp(ymax);
-    const float mref = ymax > zb ? ymax : zb;
-    const float mL = mref * kLog2e;
-    float se = 0.f;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) se += __builtin_amdgcn_exp2f(__builtin_fmaf(cur[j], kLog2e, -mL));
-    se = wave_sum_dpp(se);
-    const float lse = mref + __logf(se);
-    // lowest token whose root key equals ymax: per-lane first hit, then a wave min
-    int32_t hit = INT_MAX;
-#pragma unroll
-    for (int j = PER - 1; j >= 0; --j) {
-      const float yj = kKeepY ? y[kKeepY ? j : 0] : cur[j] + S.rpsi[64 * j + lane];
-      hit = (yj == ymax) ? 64 * j + lane : hit;
-    }
-    int32_t r1_tok = wave_min_i32_dpp(hit);
-    if (r1_tok >= V) r1_tok = 0;  // only with -inf / nan logits: keep indices in range
-    const int32_t r1_dst = S.rdst[r1_tok];
-    const int32_t c16 = S.cls[r1_tok];
-    const int32_t r1_cls = (c16 == 0xffff) ? -1 : c16;
+    if (!wait_flag(&S.a_flag[slot], t, false, &S.abort_flag)) return;
     RowSum& rs = S.sum[slot];
-    if (lane == 0) {
-      rs.c3.y = __float_as_int(ymax);
-      rs.c3.z = r1_tok;
-      rs.c3.w = r1_dst;
-      rs.c4.x = r1_cls;
-    }
-    lds_fence();
-    if (lane == 0) vstore(&S.a_flag[slot], t);
+    const TT* zrow = logits + ((int64_t)t * B + b) * stride;
+    const v4i c3 = rs.c3, c4 = rs.c4;
+    const float lse = __int_as_float(__builtin_amdgcn_readfirstlane(c3.y));
+    const float zb = __int_as_float(__builtin_amdgcn_readfirstlane(c3.z));
+    const int32_t r1_tok = __builtin_amdgcn_readfirstlane(c3.w);
+    const float ymax = __int_as_float(__builtin_amdgcn_readfirstlane(c4.x));
+    const int32_t r1_dst = __builtin_amdgcn_readfirstlane(c4.y);
+    const int32_t r1_cls = __builtin_amdgcn_readfirstlane(c4.z);
 
-    v4i c0 = v4i{t, __float_as_int(lse), __float_as_int(zb), -4};
+    int32_t x1, x2 = -4, x3 = -4;
+    Answer a1;
     if (mode != 1) {
       // no biasing: the answer does not depend on the (constant) state
       const bool blank = !better(ymax, r1_tok, zb, V);
-      const int32_t st = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
-      if (lane == 0)
-        rs.c1 = v4i{blank ? V : r1_tok, st, 0, __float_as_int(blank ? zb : ymax)};
-      c0.w = st;
+      x1 = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+      a1.tok = blank ? V : r1_tok;
+      a1.ns = x1;
+      a1.b = 0.f;
+      a1.zv = blank ? zb : ymax;
     } else {
       // ---- answer from x1 (the carried state at t = 0)
-      int32_t x1;
       if (t == 0) {
         x1 = s0;
       } else {
         const int32_t ps = (t - 1) % NSLOT;
         if (!wait_flag(&S.a_flag[ps], t - 1, false, &S.abort_flag)) return;
-        x1 = S.sum[ps].c3.w;
+        x1 = __builtin_amdgcn_readfirstlane(S.sum[ps].c4.y);
       }
-      x1 = __builtin_amdgcn_readfirstlane(x1);
-      const Answer a1 =
-          eval_state<Ld>(A, off, S, slot, x1, zb, ymax, r1_tok, r1_dst, r1_cls, wave, tag, V, nhot);
-      if (lane == 0) rs.c1 = v4i{a1.tok, a1.ns, __float_as_int(a1.b), __float_as_int(a1.zv)};
-      lds_fence();
-      if (lane == 0) vstore(&S.p1_flag[slot], t);
+      a1 = eval_state<Ld>(A, off, S, zrow, x1, zb, ymax, r1_tok, r1_dst, r1_cls, wave, tag, V,
+                          nhot);
+    }
+    if (lane == 0) {
+      // speculative outputs: right whenever the stream is in x1 at step t
+      const int64_t oi = (int64_t)t * B + b;
+      out_tok[oi] = a1.tok;
+      out_state[oi] = a1.ns;
+      out_score[oi] = (a1.zv - lse) + a1.b;
+      rs.c0.y = x1;
+      rs.c0.z = a1.ns;
+    }
+    lds_fence();
+    if (lane == 0) vstore(&S.p1_flag[slot], t);
+    if (mode == 1) {
       // ---- answer from the previous row's x1 answer
-      int32_t x2 = -4;
       if (t > 0) {
         const int32_t ps = (t - 1) % NSLOT;
         if (!wait_flag(&S.p1_flag[ps], t - 1, false, &S.abort_flag)) return;
-        x2 = S.sum[ps].c1.y;
+        x2 = __builtin_amdgcn_readfirstlane(S.sum[ps].c0.z);
       }
-      x2 = __builtin_amdgcn_readfirstlane(x2);
-      Answer a2 = a1;
+      int32_t ns2 = -4;
       if (x2 >= 0 && x2 != x1) {
-        a2 = eval_state<Ld>(A, off, S, slot, x2, zb, ymax, r1_tok, r1_dst, r1_cls, wave, tag, V, nhot);
+        const Answer a2 =
+            eval_state<Ld>(A, off, S, zrow, x2, zb, ymax, r1_tok, r1_dst, r1_cls, wave, tag, V,
+                           nhot);
+        ns2 = a2.ns;
+        if (lane == 0) rs.c1 = v4i{a2.ns, a2.tok, __float_as_int(a2.b), __float_as_int(a2.zv)};
       } else {
         x2 = -4;
       }
-      if (lane == 0) {
-        rs.c2 = v4i{x2, a2.tok, a2.ns, __float_as_int(a2.b)};
-        rs.c3.x = __float_as_int(a2.zv);
+      if (lane == 0) rs.c0.w = x2;
+      if (lane == 0) rs.c4.w = ns2;
+      lds_fence();
+      if (lane == 0) vstore(&S.p2_flag[slot], t);
+      // ---- answer from the previous row's x2 answer
+      if (t > 0) {
+        const int32_t ps = (t - 1) % NSLOT;
+        if (!wait_flag(&S.p2_flag[ps], t - 1, false, &S.abort_flag)) return;
+        x3 = __builtin_amdgcn_readfirstlane(S.sum[ps].c4.w);
       }
-      c0.w = x1;
+      if (x3 >= 0 && x3 != x1 && x3 != x2) {
+        const Answer a3 =
+            eval_state<Ld>(A, off, S, zrow, x3, zb, ymax, r1_tok, r1_dst, r1_cls, wave, tag, V,
+                           nhot);
+        if (lane == 0) {
+          rs.c2 = v4i{x3, a3.ns, a3.tok, __float_as_int(a3.b)};
+          rs.c3.x = __float_as_int(a3.zv);
+        }
+      } else if (lane == 0) {
+        rs.c2.x = -4;
+      }
+    } else if (lane == 0) {
+      rs.c0.w = -4;
+      rs.c2.x = -4;
     }
+    // the speculative outputs land before the row is published, so that a
+    // correction by the consumer is ordered after them
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     lds_fence();
-    if (lane == 0) rs.c0 = c0;  // publishes row t
+    if (lane == 0) vstore(&S.ready[slot], t);  // publishes row t
     cbar();
   }
 }
@@ -556,13 +599,13 @@ hipError_t launch_greedy_fast(const ArenaView& A, const void* logits, int32_t dt
   return launch_fast<LD, P, NS>(A, logits, T, B, row_stride, model_ids, states, out_tok,       \
                                 out_state, out_score, st)
   if (dtype == TB_F32) {
-    if (V1 <= 64 * 5) TB_FAST(LoadF32, 5, 16);
-    if (V1 <= 64 * 17) TB_FAST(LoadF32, 17, 16);
-    TB_FAST(LoadF32, 32, 8);
+    if (V1 <= 64 * 5) TB_FAST(LoadF32, 5, 64);
+    if (V1 <= 64 * 17) TB_FAST(LoadF32, 17, 64);
+    TB_FAST(LoadF32, 32, 64);
   } else {
-    if (V1 <= 64 * 5) TB_FAST(LoadBF16, 5, 16);
-    if (V1 <= 64 * 17) TB_FAST(LoadBF16, 17, 16);
-    TB_FAST(LoadBF16, 32, 16);
+    if (V1 <= 64 * 5) TB_FAST(LoadBF16, 5, 64);
+    if (V1 <= 64 * 17) TB_FAST(LoadBF16, 17, 64);
+    TB_FAST(LoadBF16, 32, 64);
   }
 #undef TB_FAST
 }
