@@ -168,19 +168,26 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
 }  // namespace
 
 namespace {
-// TBIAS_GREEDY_KERNEL=ref selects the reference kernel (used to test both paths).
-bool use_reference_kernel() {
+// TBIAS_GREEDY_KERNEL selects a kernel for testing: "ref" (one workgroup per
+// stream, any V), "pipe" (pipelined), anything else the segmented kernel.
+int greedy_kernel_choice() {
   const char* e = std::getenv("TBIAS_GREEDY_KERNEL");
-  return e && std::strcmp(e, "ref") == 0;
+  if (e && std::strcmp(e, "ref") == 0) return 0;
+  if (e && std::strcmp(e, "pipe") == 0) return 1;
+  return 2;
 }
 }  // namespace
 
 hipError_t launch_greedy(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
                          int32_t B, int64_t row_stride, const int32_t* model_ids, int32_t* states,
                          int32_t* out_tok, int32_t* out_state, float* out_score, hipStream_t st) {
-  if (!use_reference_kernel()) {
-    hipError_t e = launch_greedy_fast(A, logits, dtype, T, B, row_stride, model_ids, states,
-                                      out_tok, out_state, out_score, st);
+  const int choice = greedy_kernel_choice();
+  if (choice != 0) {
+    hipError_t e = (choice == 1)
+                       ? launch_greedy_fast(A, logits, dtype, T, B, row_stride, model_ids, states,
+                                            out_tok, out_state, out_score, st)
+                       : launch_greedy_seg(A, logits, dtype, T, B, row_stride, model_ids, states,
+                                           out_tok, out_state, out_score, st);
     if (e != hipErrorNotSupported) return e;
     (void)hipGetLastError();  // clear the sticky "not supported" before the fallback
   }

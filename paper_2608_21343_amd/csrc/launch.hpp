@@ -28,6 +28,13 @@ hipError_t launch_greedy_fast(const ArenaView& A, const void* logits, int32_t dt
                               int32_t* states, int32_t* out_tok, int32_t* out_state,
                               float* out_score, hipStream_t st);
 
+// Segmented greedy kernel (plus its boundary fix-up); hipErrorNotSupported
+// when V+1 is too large for it.
+hipError_t launch_greedy_seg(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                             int32_t B, int64_t row_stride, const int32_t* model_ids,
+                             int32_t* states, int32_t* out_tok, int32_t* out_state,
+                             float* out_score, hipStream_t st);
+
 // Largest V+1 the step kernels accept (LDS tables are sized by it).
 constexpr int32_t kMaxV1 = 10241;
 

@@ -205,12 +205,16 @@ def test_stream_permutation_permutes_outputs():
         assert np.array_equal(a[:, perm], b)
 
 
-@pytest.mark.parametrize("name", ["tiny", "batched", "streaming"])
-def test_fast_and_reference_greedy_kernels_agree(name, monkeypatch):
-    """The pipelined kernel and the reference kernel give bit-identical outputs."""
+@pytest.mark.parametrize("kernel", ["seg", "pipe"])
+@pytest.mark.parametrize("name,T,chunk", [("tiny", 50, 50), ("batched", 500, 500),
+                                          ("streaming", 1024, 1024), ("streaming", 200, 37)])
+def test_greedy_kernels_agree_with_reference_kernel(kernel, name, T, chunk, monkeypatch):
+    """The segmented and pipelined kernels give the reference kernel's outputs:
+    tokens, states and carries identical, scores within rounding of the
+    normaliser. Whole-length calls make the segmented kernel split streams
+    over several workgroups and run its boundary fix-up."""
     from paper_2608_21343_amd.decoder import to_device_logits
     cfg = W.config_by_name(name)
-    T = min(cfg.T, 200)
     lists = W.phrases(cfg)
     rows = W.logits(cfg, 0, T)
     dec = _decoder(cfg, lists)
@@ -218,11 +222,72 @@ def test_fast_and_reference_greedy_kernels_agree(name, monkeypatch):
     if cfg.B > 4:
         mids[1] = -1
     dev = to_device_logits(rows[:, :, 0, :])
-    fast = gpu_greedy(dec, dev, mids, 37)
+    del rows
+    say(f"[agree] {kernel} vs ref: {name} T={T} chunk={chunk}")
+    monkeypatch.setenv("TBIAS_GREEDY_KERNEL", kernel)
+    out = gpu_greedy(dec, dev, mids, chunk)
     monkeypatch.setenv("TBIAS_GREEDY_KERNEL", "ref")
-    ref = gpu_greedy(dec, dev, mids, 37)
-    for a, b in zip(fast, ref):
-        assert np.array_equal(a[:2] if a.ndim == 2 and a.dtype != np.float32 else a, b[:2] if b.ndim == 2 and b.dtype != np.float32 else b) or a.dtype == np.float32
-    assert np.array_equal(fast[0], ref[0]) and np.array_equal(fast[1], ref[1])
-    assert np.array_equal(fast[3], ref[3])
-    assert np.max(np.abs(fast[2] - ref[2])) <= 2e-6
+    ref = gpu_greedy(dec, dev, mids, chunk)
+    bad = np.nonzero(out[0] != ref[0])
+    assert bad[0].size == 0, f"token mismatch at (t, b) {list(zip(*bad))[:5]}"
+    assert np.array_equal(out[1], ref[1]) and np.array_equal(out[3], ref[3])
+    assert np.max(np.abs(out[2] - ref[2])) <= 2e-6
+
+
+def _phrase_following_rows(rng, T, B, V, plen, blank_every=9, margin=3.0):
+    """Logits whose boosted greedy path walks through the phrase 1..plen over
+    and over (a blank every blank_every rows), each stream out of phase."""
+    rows = rng.normal(0.0, 0.1, size=(T, B, V + 1)).astype(np.float32)
+    for b in range(B):
+        k = 5 * b
+        for t in range(T):
+            if (t + b) % blank_every == 0:
+                rows[t, b, V] += margin
+            else:
+                rows[t, b, 1 + (k % plen)] += margin
+                k += 1
+    return rows
+
+
+@pytest.mark.parametrize("chunk", [600, 16, 100])
+def test_segment_starts_deep_inside_long_phrases(chunk):
+    """Trajectories that stay deep inside a 40-token phrase: a segment start
+    guessed from the root is wrong almost everywhere, so repairs run across
+    many segments and workgroup boundaries."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V, B, T = 64, 5, 600
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    phrase = list(range(1, 41))
+    lists = [[phrase], [phrase, list(range(5, 30))], [list(range(1, 11))], [phrase]]
+    rows = _phrase_following_rows(np.random.default_rng(7), T, B, V, 40)
+    mids = np.array([0, 1, 2, 3, -1], np.int32)
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    say(f"[repair] long phrases, chunk={chunk}")
+    gpu = gpu_greedy(dec, to_device_logits(rows), mids, chunk)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    ref = oracle.greedy_decode(graphs, mids, rows[:, :, None, :], np.array([0, 0, 0, 0, -1], np.int32))
+    compare_greedy(gpu, ref, range(B), ATOL)
+    assert np.array_equal(gpu[3], ref[3])
+    assert np.max(ref[1][:, 0]) >= 30          # the path really went deep
+
+
+def test_segments_longer_than_the_kept_trajectory():
+    """256 streams x 1100 steps in one call: one workgroup per stream with
+    segments of 69 rows, and a 120-token phrase keeping repairs going past
+    the first 64 rows of a segment."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V, B, T, plen = 128, 256, 1100, 120
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    lists = [[list(range(1, plen + 1))], [list(range(1, 31)), list(range(40, 90))]]
+    rows = _phrase_following_rows(np.random.default_rng(11), T, B, V, plen, blank_every=13)
+    mids = (np.arange(B) % 2).astype(np.int32)
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    say("[repair] 256 x 1100, segments of 69 rows")
+    gpu = gpu_greedy(dec, to_device_logits(rows), mids, T)
+    sample = [0, 1, 2, 3, 100, 201, 254, 255]
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    sub = np.ascontiguousarray(rows[:, sample, None, :])
+    ref = oracle.greedy_decode(graphs, mids[sample], sub, np.zeros(len(sample), np.int32))
+    compare_greedy(gpu, ref, sample, ATOL, ref_streams=range(len(sample)))
+    assert np.array_equal(gpu[3][sample], ref[3])
+    assert np.max(ref[1][:, 0]) >= 100
