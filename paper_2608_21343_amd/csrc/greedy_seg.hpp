@@ -45,6 +45,7 @@ namespace seg {
 constexpr int kWarm = 2;    // warm-up rows of a guessed segment start
 constexpr int kTraj = 64;   // trajectory states kept per segment
 constexpr int kMinSeg = 8;  // shortest segment worth a wave
+constexpr int kScalarKids = 8;  // arena children walked one at a time up to this many
 constexpr uint32_t kSpinLimit = 1u << 26;
 constexpr int32_t kStateTimeout = -3;
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -75,9 +76,21 @@ struct alignas(16) FixedLds {
   uint8_t stamps[W][64 * PER];
   Tables<PER> tab;
   int32_t traj[W][kTraj];  // state after each of the first kTraj steps
+  float rsum[W][4];        // short calls: per-row blank logit, best root key, normaliser, token
   int32_t fin_state[W];    // exact state after each segment
   int32_t fin_ready[W];
   int32_t abort_flag;
+};
+
+// Records of the first HOT states of a model (BFS order: the shallowest, the
+// most visited) held in LDS.
+template <int HOT>
+struct alignas(16) HotRecords {
+  int32_t fc[HOT];      // first child
+  uint32_t lknc[HOT];   // link | n_child << 16
+  float phi[HOT];
+  float psi[HOT];
+  uint16_t label[HOT];  // class on the arc into the state
 };
 
 constexpr int kHotRecordBytes = 4 + 4 + 4 + 4 + 2;
@@ -91,11 +104,7 @@ constexpr int hot_states() {
 template <int PER>
 struct alignas(16) SegLds : FixedLds<PER> {
   static constexpr int HOT = hot_states<PER>();
-  int32_t hs_fc[HOT];      // records of states < nhot
-  uint32_t hs_lknc[HOT];   // link | n_child << 16
-  float hs_phi[HOT];
-  float hs_psi[HOT];
-  uint16_t hs_label[HOT];
+  HotRecords<HOT> hot;
 };
 
 struct Answer {
@@ -116,34 +125,12 @@ __device__ __forceinline__ float rlf(float v, int32_t lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-// Graph records: from LDS for states < nhot, else from the arena.
-struct Graph {
-  const ArenaView* A;
-  int32_t off, nhot;
-  const int32_t* hs_fc;
-  const uint32_t* hs_lknc;
-  const float* hs_phi;
-  const float* hs_psi;
-  const uint16_t* hs_label;
-  __device__ __forceinline__ float phi(int32_t x) const {
-    return x < nhot ? hs_phi[x] : A->phi[off + x];
-  }
-  __device__ __forceinline__ float psi(int32_t x) const {
-    return x < nhot ? hs_psi[x] : A->psi[off + x];
-  }
-  __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk) const {
-    if (x < nhot) {
-      fc = hs_fc[x];
-      const uint32_t v = hs_lknc[x];
-      lnk = (int32_t)(v & 0xffffu);
-      nc = (int32_t)(v >> 16);
-    } else {
-      fc = A->first_child[off + x];
-      nc = A->n_child[off + x];
-      lnk = A->link[off + x];
-    }
-  }
-};
+// Read-only load through the scalar cache (uniform address). It waits on the
+// scalar counter, not behind the vector loads of the prefetched rows.
+template <class T>
+__device__ __forceinline__ T sload(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)(p);
+}
 
 // Lane geometry of the last chunk (see the row layout above).
 template <int PER>
@@ -162,6 +149,59 @@ struct RowShape {
   }
 };
 
+// Graph records: from LDS for states < nhot, else from the arena by scalar
+// loads (the arena is immutable while a step runs; state ids are uniform).
+struct Graph {
+  const ArenaView* A;
+  int32_t off, nhot;
+  const int32_t* hs_fc;
+  const uint32_t* hs_lknc;
+  const float* hs_phi;
+  const float* hs_psi;
+  const uint16_t* hs_label;
+  template <int HOT>
+  __device__ __forceinline__ Graph(const ArenaView& a, int32_t o, int32_t nh,
+                                   const HotRecords<HOT>& h)
+      : A(&a), off(o), nhot(nh), hs_fc(h.fc), hs_lknc(h.lknc), hs_phi(h.phi), hs_psi(h.psi),
+        hs_label(h.label) {}
+  __device__ __forceinline__ float phi(int32_t x) const {
+    return x < nhot ? hs_phi[x] : sload(A->phi + off + x);
+  }
+  __device__ __forceinline__ float psi(int32_t x) const {
+    return x < nhot ? hs_psi[x] : sload(A->psi + off + x);
+  }
+  __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk) const {
+    if (x < nhot) {
+      fc = hs_fc[x];
+      const uint32_t v = hs_lknc[x];
+      lnk = (int32_t)(v & 0xffffu);
+      nc = (int32_t)(v >> 16);
+    } else {
+      fc = sload(A->first_child + off + x);
+      nc = sload(A->n_child + off + x);
+      lnk = sload(A->link + off + x);
+    }
+  }
+};
+
+// Records of states [0, nhot) of the model at off into LDS; NT threads.
+template <int HOT, int NT>
+__device__ __forceinline__ void fill_hot(HotRecords<HOT>& h, const ArenaView& A, int32_t off,
+                                         int32_t nhot) {
+#pragma unroll
+  for (int k = 0; k < (HOT + NT - 1) / NT; ++k) {
+    const int32_t i = k * NT + (int32_t)threadIdx.x;
+    if (i < nhot) {
+      h.fc[i] = A.first_child[off + i];
+      h.lknc[i] = (uint32_t)A.link[off + i] | ((uint32_t)A.n_child[off + i] << 16);
+      h.phi[i] = A.phi[off + i];
+      h.psi[i] = A.psi[off + i];
+      const int32_t lab = A.label[off + i];
+      h.label[i] = (uint16_t)(lab < 0 ? 0 : lab);
+    }
+  }
+}
+
 template <class Ld, int PER>
 __device__ __forceinline__ void load_row(float* dst, const typename Ld::T* row,
                                          const RowShape<PER>& rs) {
@@ -176,8 +216,9 @@ __device__ __forceinline__ void load_row(float* dst, const typename Ld::T* row,
 template <int PER>
 __device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& tb,
                                              const float* zrow, uint8_t* stamps, uint32_t& tag,
-                                             int32_t x, float zb, float r1_y, int32_t r1_tok,
-                                             int32_t r1_dst, int32_t r1_cls, int32_t V) {
+                                             const RowShape<PER>& rs, int32_t x, float zb,
+                                             float r1_y, int32_t r1_tok, int32_t r1_dst,
+                                             int32_t r1_cls, int32_t V) {
   const int lane = __lane_id();
   if (++tag == 256u) {  // 8-bit tags: clear the table on wrap
     uint32_t* w = reinterpret_cast<uint32_t*>(stamps);
@@ -193,20 +234,58 @@ __device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& 
   for (int32_t c = x; c != 0;) {
     int32_t fc, nc, lnk;
     G.rec(c, fc, nc, lnk);
-    const bool hot_kids = fc + nc <= G.nhot;
-    for (int32_t j0 = 0; j0 < nc; j0 += 64) {
-      const int32_t j = j0 + lane;
-      if (j < nc) {
+    if (fc + nc <= G.nhot) {
+      // children in LDS: one child per lane
+      for (int32_t j0 = 0; j0 < nc; j0 += 64) {
+        const int32_t j = j0 + lane;
+        if (j < nc) {
+          const int32_t y = fc + j;
+          const int32_t lab = G.hs_label[y];
+          if (stamps[lab] != tg) {
+            stamps[lab] = tg;
+            const float py = G.hs_psi[y];
+            const int32_t m0 = tb.cls_ptr[lab], m1 = tb.cls_ptr[lab + 1];
+            for (int32_t q = m0; q < m1; ++q) {
+              const int32_t tok = tb.cls_tok[q];
+              const float k = zrow[tok] + py;
+              if (better(k, tok, lk, lt)) { lk = k; lt = tok; lns = y; lpsi = py; }
+            }
+          }
+        }
+      }
+    } else if (nc <= kScalarKids) {
+      // a few children in the arena: one child at a time by scalar loads, the
+      // members of its class across the lanes
+      for (int32_t j = 0; j < nc; ++j) {
         const int32_t y = fc + j;
-        const int32_t lab = hot_kids ? (int32_t)G.hs_label[y] : G.A->label[G.off + y];
-        if (stamps[lab] != tg) {
+        const int32_t lab = sload(G.A->label + G.off + y);
+        const float py = sload(G.A->psi + G.off + y);
+        if (stamps[lab] != tg) {  // uniform
           stamps[lab] = tg;
-          const float py = hot_kids ? G.hs_psi[y] : G.A->psi[G.off + y];
-          const int32_t m0 = tb.cls_ptr[lab], m1 = tb.cls_ptr[lab + 1];
-          for (int32_t q = m0; q < m1; ++q) {
+          const int32_t q = tb.cls_ptr[lab] + lane;
+          if (q < tb.cls_ptr[lab + 1]) {
             const int32_t tok = tb.cls_tok[q];
             const float k = zrow[tok] + py;
             if (better(k, tok, lk, lt)) { lk = k; lt = tok; lns = y; lpsi = py; }
+          }
+        }
+      }
+    } else {
+      // many children in the arena: one child per lane
+      for (int32_t j0 = 0; j0 < nc; j0 += 64) {
+        const int32_t j = j0 + lane;
+        if (j < nc) {
+          const int32_t y = fc + j;
+          const int32_t lab = G.A->label[G.off + y];
+          if (stamps[lab] != tg) {
+            stamps[lab] = tg;
+            const float py = G.A->psi[G.off + y];
+            const int32_t m0 = tb.cls_ptr[lab], m1 = tb.cls_ptr[lab + 1];
+            for (int32_t q = m0; q < m1; ++q) {
+              const int32_t tok = tb.cls_tok[q];
+              const float k = zrow[tok] + py;
+              if (better(k, tok, lk, lt)) { lk = k; lt = tok; lns = y; lpsi = py; }
+            }
           }
         }
       }
@@ -219,20 +298,24 @@ __device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& 
   const int32_t o_ns = rl(lns, wl);
   const float o_psi = rlf(lpsi, wl);
 
-  // best root move whose class is not overridden
+  // best root move whose class is not overridden (unrolled over the row's
+  // chunks so that the table reads of several chunks issue together)
   float rk = r1_y;
   int32_t rt = r1_tok, r_ns = r1_dst;
   if (r1_cls >= 0 && stamps[r1_cls] == tg) {
     float k2 = kNegInf;
-    int32_t t2 = INT_MAX, d2 = 0;
-    for (int32_t v = lane; v < V; v += 64) {
+    int32_t t2 = INT_MAX;
+#pragma unroll 6
+    for (int j = 0; j < PER; ++j) {
+      const int32_t v = (j < PER - 1) ? 64 * j + lane : rs.last_idx;
       const int32_t c = tb.cls[v];
-      if (c != 0xffff && stamps[c] == tg) continue;
-      const float k = zrow[v] + tb.rpsi[v];
-      if (better(k, v, k2, t2)) { k2 = k; t2 = v; d2 = tb.rdst[v]; }
+      const bool ok_lane = (j < PER - 1) || rs.last_ok;
+      const float k = zrow[v] + tb.rpsi[v];  // -inf for the blank
+      const bool over = c != 0xffff && stamps[c] == tg;
+      if (ok_lane && !over && k > k2) { k2 = k; t2 = v; }
     }
-    const int32_t l2 = wave_argmax_dpp(k2, t2, rk, rt);
-    r_ns = rl(d2, l2);
+    wave_argmax_dpp(k2, t2, rk, rt);
+    r_ns = (rt < V) ? tb.rdst[rt] : 0;
   }
   Answer a;
   a.tok = V;
@@ -259,14 +342,18 @@ __device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& 
   return a;
 }
 
-// One complete step on a row held in registers (raw[j] as loaded). rp holds
-// this lane's root-move psi (-inf for blank and masked lanes). Returns the
-// answer and the row's normaliser.
+// State-independent part of a step on a row held in registers (raw[j] as
+// loaded): copies the row to zrow (LDS), and returns the blank logit, the best
+// root move (key and token) and, if asked, the normaliser. rp holds this
+// lane's root-move psi (-inf for blank and masked lanes).
+struct RowSum {
+  float zb, ymax, lse;
+  int32_t r1_tok;
+};
+
 template <int PER>
-__device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& tb, float* zrow,
-                                            uint8_t* stamps, uint32_t& tag, const float* raw,
-                                            const float* rp, const RowShape<PER>& rs, int32_t s,
-                                            int mode, int32_t V, float& lse) {
+__device__ __forceinline__ RowSum row_summary(float* zrow, const float* raw, const float* rp,
+                                              const RowShape<PER>& rs, int32_t V, bool need_lse) {
   const int lane = __lane_id();
   float cur[PER];
 #pragma unroll
@@ -276,7 +363,8 @@ __device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& t
   }
   zrow[rs.last_idx] = raw[PER - 1];  // repeated lanes rewrite equal values
   cur[PER - 1] = rs.last_ok ? raw[PER - 1] : kNegInf;
-  const float zb = rlf(raw[PER - 1], PER > 1 ? 63 : V);
+  RowSum r;
+  r.zb = rlf(raw[PER - 1], PER > 1 ? 63 : V);
   asm volatile("" ::: "memory");
 
   // best root move per lane: strict > keeps the lowest chunk, hence the lowest index
@@ -284,7 +372,7 @@ __device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& t
   int32_t jb = 0;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
-    zmax = zmax > cur[j] ? zmax : cur[j];
+    zmax = __builtin_fmaxf(zmax, cur[j]);
     const float yj = cur[j] + rp[j];
     const bool gt = yj > yb;
     yb = gt ? yj : yb;
@@ -292,28 +380,49 @@ __device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& t
   }
   const int32_t idx = (jb == PER - 1) ? rs.last_idx : 64 * jb + lane;
   zmax = wave_max_dpp(zmax);
-  float ymax;
-  int32_t r1_tok;
-  wave_argmax_dpp(yb, idx, ymax, r1_tok);
-  if (r1_tok >= V) r1_tok = 0;  // only with -inf / nan logits: keep indices in range
-  const float mL = zmax * kLog2e;
-  float se = 0.f;
+  wave_argmax_dpp(yb, idx, r.ymax, r.r1_tok);
+  if (r.r1_tok >= V) r.r1_tok = 0;  // only with -inf / nan logits: keep indices in range
+  r.lse = 0.f;
+  if (need_lse) {  // warm-up rows only need the state
+    const float mL = zmax * kLog2e;
+    float se = 0.f;
 #pragma unroll
-  for (int j = 0; j < PER; ++j) se += __builtin_amdgcn_exp2f(__builtin_fmaf(cur[j], kLog2e, -mL));
-  se = wave_sum_dpp(se);
-  lse = zmax + __logf(se);
+    for (int j = 0; j < PER; ++j) se += __builtin_amdgcn_exp2f(__builtin_fmaf(cur[j], kLog2e, -mL));
+    se = wave_sum_dpp(se);
+    r.lse = zmax + __logf(se);
+  }
+  return r;
+}
+
+// The step from state s on a summarised row (zrow in LDS).
+template <int PER>
+__device__ __forceinline__ Answer step_from(const Graph& G, const Tables<PER>& tb,
+                                            const float* zrow, uint8_t* stamps, uint32_t& tag,
+                                            const RowShape<PER>& rs, const RowSum& r, int32_t s,
+                                            int mode, int32_t V) {
   Answer a;
   if (mode != 1) {
-    const bool blank = !better(ymax, r1_tok, zb, V);
-    a.tok = blank ? V : r1_tok;
+    const bool blank = !better(r.ymax, r.r1_tok, r.zb, V);
+    a.tok = blank ? V : r.r1_tok;
     a.ns = s;
     a.b = 0.f;
-    a.zv = blank ? zb : ymax;
+    a.zv = blank ? r.zb : r.ymax;
     return a;
   }
-  const int32_t c16 = tb.cls[r1_tok];
-  return eval_state<PER>(G, tb, zrow, stamps, tag, s, zb, ymax, r1_tok, tb.rdst[r1_tok],
-                         c16 == 0xffff ? -1 : c16, V);
+  const int32_t c16 = tb.cls[r.r1_tok];
+  return eval_state<PER>(G, tb, zrow, stamps, tag, rs, s, r.zb, r.ymax, r.r1_tok,
+                         tb.rdst[r.r1_tok], c16 == 0xffff ? -1 : c16, V);
+}
+
+// One complete step on a row held in registers.
+template <int PER>
+__device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& tb, float* zrow,
+                                            uint8_t* stamps, uint32_t& tag, const float* raw,
+                                            const float* rp, const RowShape<PER>& rs, int32_t s,
+                                            int mode, int32_t V, bool need_lse, float& lse) {
+  const RowSum r = row_summary<PER>(zrow, raw, rp, rs, V, need_lse);
+  lse = r.lse;
+  return step_from<PER>(G, tb, zrow, stamps, tag, rs, r, s, mode, V);
 }
 
 // Root row and class tables of model m (mode 1) into LDS; NT threads.
@@ -347,6 +456,50 @@ __device__ __forceinline__ void root_psi_regs(float* rp, const Tables<PER>& tb,
   rp[PER - 1] = rs.last_ok ? tb.rpsi[rs.last_idx] : kNegInf;
 }
 
+// Sequential recompute from state x over rows [t, t_end), stopping after the
+// first row whose new state equals old_state(t): from there on the stored
+// outputs already follow the exact trajectory. With b2 given, rows are
+// prefetched two ahead in three buffers (b0, b1 hold or are loading rows t and
+// t+1, clamped to t_end - 1); with b2 null, one ahead in two buffers (b0 holds
+// row t). emit(t, answer, lse) writes a row. Returns true when the
+// trajectories met; x is the exact state after the last recomputed row.
+template <class Ld, int PER, bool kTwoAhead, class OldFn, class EmitFn>
+__device__ __forceinline__ bool repair_run(const Graph& G, const Tables<PER>& tb, float* zrow,
+                                           uint8_t* stamps, uint32_t& tag, const float* rp,
+                                           const RowShape<PER>& rs,
+                                           const typename Ld::T* col, int64_t tstride,
+                                           int32_t t, int32_t t_end, int32_t& x, int mode,
+                                           int32_t V, float* b0, float* b1, float* b2,
+                                           OldFn old_state, EmitFn emit) {
+  constexpr int kAhead = kTwoAhead ? 2 : 1;
+  auto sub = [&](const float* cur, float* pf, int32_t tt) -> bool {
+    const int32_t tn = (tt + kAhead < t_end) ? tt + kAhead : t_end - 1;
+    load_row<Ld, PER>(pf, col + (int64_t)tn * tstride, rs);
+    float lse;
+    const Answer a = full_step<PER>(G, tb, zrow, stamps, tag, cur, rp, rs, x, mode, V, true, lse);
+    const int32_t old = old_state(tt);
+    emit(tt, a, lse);
+    x = __builtin_amdgcn_readfirstlane(a.ns);
+    return x == old;
+  };
+  if constexpr (kTwoAhead) {
+    for (; t < t_end; t += 3) {
+      if (sub(b0, b2, t)) return true;
+      if (t + 1 >= t_end) break;
+      if (sub(b1, b0, t + 1)) return true;
+      if (t + 2 >= t_end) break;
+      if (sub(b2, b1, t + 2)) return true;
+    }
+  } else {
+    for (; t < t_end; t += 2) {
+      if (sub(b0, b1, t)) return true;
+      if (t + 1 >= t_end) break;
+      if (sub(b1, b0, t + 1)) return true;
+    }
+  }
+  return false;
+}
+
 template <class Ld, int PER>
 __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
@@ -362,25 +515,27 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   const int lane = __lane_id();
   const int32_t b = blockIdx.x % B;
   const int32_t g = blockIdx.x / B;
+  const typename Ld::T* col = logits + (int64_t)b * stride;  // row t of stream b: col + t*tstride
+  const int64_t tstride = (int64_t)B * stride;
 
   const int32_t m = model_ids[b];
   const int32_t s0 = states[b];
   int32_t off = 0, n = 0;
   const int mode = resolve_stream(A, m, s0, off, n);
+
+  const RowShape<PER> rs(V1);
+  const int32_t segi = g * W + w;
+  const int32_t t0 = segi * L;
+  const int32_t t1 = (t0 + L < T) ? t0 + L : T;
+  const bool exact_start = (segi == 0) || mode != 1;
+  const int32_t tw = exact_start ? t0 : (t0 - kWarm > 0 ? t0 - kWarm : 0);
+  // the first row is in flight while the tables are filled
+  float ra[PER], rb[PER];
+  if (t0 < t1) load_row<Ld, PER>(ra, col + (int64_t)tw * tstride, rs);
+
   fill_tables<PER, NT>(S.tab, A, m, mode);
   const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
-#pragma unroll
-  for (int k = 0; k < (HOT + NT - 1) / NT; ++k) {
-    const int32_t i = k * NT + (int32_t)threadIdx.x;
-    if (i < nhot) {
-      S.hs_fc[i] = A.first_child[off + i];
-      S.hs_lknc[i] = (uint32_t)A.link[off + i] | ((uint32_t)A.n_child[off + i] << 16);
-      S.hs_phi[i] = A.phi[off + i];
-      S.hs_psi[i] = A.psi[off + i];
-      const int32_t lab = A.label[off + i];
-      S.hs_label[i] = (uint16_t)(lab < 0 ? 0 : lab);
-    }
-  }
+  fill_hot<HOT, NT>(S.hot, A, off, nhot);
   for (int32_t i = threadIdx.x; i < (int32_t)sizeof(S.stamps) / 4; i += NT)
     reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
   if (threadIdx.x < W) {
@@ -390,29 +545,15 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   if (threadIdx.x == 0) S.abort_flag = 0;
   __syncthreads();
 
-  Graph Gr;
-  Gr.A = &A;
-  Gr.off = off;
-  Gr.nhot = nhot;
-  Gr.hs_fc = S.hs_fc;
-  Gr.hs_lknc = S.hs_lknc;
-  Gr.hs_phi = S.hs_phi;
-  Gr.hs_psi = S.hs_psi;
-  Gr.hs_label = S.hs_label;
+  const Graph Gr(A, off, nhot, S.hot);
   float* zrow = S.zbuf[w];
   uint8_t* stamps = S.stamps[w];
   uint32_t tag = 0;
-  const RowShape<PER> rs(V1);
   float rp[PER];
   root_psi_regs<PER>(rp, S.tab, rs);
 
   const int32_t unbiased_state = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
-  const int32_t segi = g * W + w;
-  const int32_t t0 = segi * L;
-  const int32_t t1 = (t0 + L < T) ? t0 + L : T;
-  const bool exact_start = (segi == 0) || mode != 1;
   const int32_t start = (mode == 1) ? (segi == 0 ? s0 : 0) : unbiased_state;
-  const int32_t tw = exact_start ? t0 : (t0 - kWarm > 0 ? t0 - kWarm : 0);
 
   // ---- main pass over the segment (with warm-up rows)
   int32_t s = start;
@@ -421,15 +562,15 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
     // Two row buffers used in turn; the prefetch is unconditional (the last
     // row of the segment is read again at the end) so that the wait for the
     // current row can leave the next row's loads in flight.
-    float ra[PER], rb[PER];
     int32_t o_tok = 0, o_st = 0;
     float o_sc = 0.f;
     auto step = [&](const float* cur, float* nxt, int32_t t) {
       const int32_t tn = (t + 1 < t1) ? t + 1 : t;
-      load_row<Ld, PER>(nxt, logits + ((int64_t)tn * B + b) * stride, rs);
+      load_row<Ld, PER>(nxt, col + (int64_t)tn * tstride, rs);
       if (t == t0) assumed = s;
       float lse;
-      const Answer a = full_step<PER>(Gr, S.tab, zrow, stamps, tag, cur, rp, rs, s, mode, V, lse);
+      const Answer a =
+          full_step<PER>(Gr, S.tab, zrow, stamps, tag, cur, rp, rs, s, mode, V, t >= t0, lse);
       if (t >= t0) {
         const int32_t i = t - t0;
         const int32_t ln = i & 63;
@@ -449,7 +590,6 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
       }
       s = __builtin_amdgcn_readfirstlane(a.ns);
     };
-    load_row<Ld, PER>(ra, logits + ((int64_t)tw * B + b) * stride, rs);
     for (int32_t t = tw; t < t1; t += 2) {
       step(ra, rb, t);
       if (t + 1 < t1) step(rb, ra, t + 1);
@@ -457,6 +597,9 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   }
 
   // ---- hand the exact state along the segments of this workgroup
+  // The first row a repair would need is loaded while waiting.
+  const bool may_repair = w > 0 && t0 < t1 && mode == 1;
+  if (may_repair) load_row<Ld, PER>(ra, col + (int64_t)t0 * tstride, rs);
   int32_t fin = s;
   if (w > 0) {
     uint32_t spins = 0;
@@ -474,29 +617,25 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
     } else if (t0 >= t1) {
       fin = exact;  // empty segment: pass the state on
     } else if (exact != assumed) {
-      // recompute from the exact state until the trajectories meet
-      int32_t x = exact;
-      bool met = false;
-      for (int32_t t = t0; t < t1; ++t) {
-        float cur[PER];
-        load_row<Ld, PER>(cur, logits + ((int64_t)t * B + b) * stride, rs);
-        float lse;
-        const Answer a =
-            full_step<PER>(Gr, S.tab, zrow, stamps, tag, cur, rp, rs, x, mode, V, lse);
+      // Stored states: LDS for the first kTraj rows, else read back by the
+      // lane that wrote them in the main pass (row i of the segment: lane i & 63).
+      auto old_state = [&](int32_t t) -> int32_t {
         const int32_t i = t - t0;
-        const int32_t old = (i < kTraj) ? __builtin_amdgcn_readfirstlane(S.traj[w][i]) : INT_MIN;
-        if (lane == (i & 63)) {  // the lane that wrote this row in the main pass
+        if (i < kTraj) return __builtin_amdgcn_readfirstlane(S.traj[w][i]);
+        return rl(out_state[(int64_t)t * B + b], i & 63);
+      };
+      auto emit = [&](int32_t t, const Answer& a, float lse) {
+        if (lane == ((t - t0) & 63)) {
           const int64_t oi = (int64_t)t * B + b;
           out_tok[oi] = a.tok;
           out_state[oi] = a.ns;
           out_score[oi] = (a.zv - lse) + a.b;
         }
-        x = __builtin_amdgcn_readfirstlane(a.ns);
-        if (x == old) {
-          met = true;
-          break;
-        }
-      }
+      };
+      int32_t x = exact;
+      const bool met =
+          repair_run<Ld, PER, false>(Gr, S.tab, zrow, stamps, tag, rp, rs, col, tstride, t0, t1,
+                                     x, mode, V, ra, rb, nullptr, old_state, emit);
       fin = met ? s : x;
     }
   }
@@ -509,90 +648,192 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   }
 }
 
-// Repairs the workgroup boundaries of each stream after greedy_seg_kernel
-// (one wave per stream, boundaries in order): from the exact state before a
-// boundary, recompute until the stored trajectory is met. Writes the carry.
+// Repairs the workgroup boundaries of each stream after greedy_seg_kernel,
+// boundaries in order: from the exact state before a boundary, recompute
+// until the stored trajectory is met. Four waves fill the tables, wave 0
+// repairs. Writes the carry.
+constexpr int kFixThreads = 256;
+constexpr int kFixHot = 2048;
+
+template <int PER>
+struct alignas(16) FixLds {
+  Tables<PER> tab;
+  float zrow[64 * PER];
+  uint8_t stamps[64 * PER];
+  HotRecords<kFixHot> hot;
+};
+
 template <class Ld, int PER>
-__global__ __launch_bounds__(64) void greedy_fix_kernel(
+__global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
     int32_t G, int32_t L, int32_t W, const int32_t* __restrict__ model_ids,
     int32_t* __restrict__ states, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
     float* __restrict__ out_score) {
-  __shared__ Tables<PER> tb;
-  __shared__ float zrow[64 * PER];
-  __shared__ uint8_t stamps[64 * PER];
+  __shared__ FixLds<PER> S;
   const int32_t V1 = A.V1, V = V1 - 1;
   const int lane = __lane_id();
   const int32_t b = blockIdx.x;
   const int32_t m = model_ids[b];
+  const typename Ld::T* col = logits + (int64_t)b * stride;
+  const int64_t tstride = (int64_t)B * stride;
   // The carried state was consumed by the main kernel; streams that are not
   // biased, or whose carried state was invalid, have exact (unboosted)
   // segment starts and need no repair.
   const bool biased = m >= 0 && m < A.n_models;
   bool timed_out = false;
   if (biased) {
-    const int32_t off = A.model_off[m], n = A.model_n[m];
-    fill_tables<PER, 64>(tb, A, m, 1);
-    for (int32_t i = lane; i < 16 * PER; i += 64) reinterpret_cast<uint32_t*>(stamps)[i] = 0u;
-    __syncthreads();
-    Graph Gr;
-    Gr.A = &A;
-    Gr.off = off;
-    Gr.nhot = 0;
-    Gr.hs_fc = nullptr;
-    Gr.hs_lknc = nullptr;
-    Gr.hs_phi = nullptr;
-    Gr.hs_psi = nullptr;
-    Gr.hs_label = nullptr;
-    uint32_t tag = 0;
     const RowShape<PER> rs(V1);
+    float ra[PER], rb[PER], rc[PER];
+    const int32_t first = W * L;  // the first workgroup boundary (< T)
+    if (threadIdx.x < 64) {
+      load_row<Ld, PER>(ra, col + (int64_t)first * tstride, rs);
+      load_row<Ld, PER>(rb, col + (int64_t)(first + 1 < T ? first + 1 : first) * tstride, rs);
+    }
+    const int32_t off = A.model_off[m], n = A.model_n[m];
+    const int32_t nhot = n < kFixHot ? n : kFixHot;
+    fill_tables<PER, kFixThreads>(S.tab, A, m, 1);
+    fill_hot<kFixHot, kFixThreads>(S.hot, A, off, nhot);
+    for (int32_t i = threadIdx.x; i < 16 * PER; i += kFixThreads)
+      reinterpret_cast<uint32_t*>(S.stamps)[i] = 0u;
+    __syncthreads();
+    if (threadIdx.x >= 64) return;  // no barrier follows
+    const Graph Gr(A, off, nhot, S.hot);
+    uint32_t tag = 0;
     float rp[PER];
-    root_psi_regs<PER>(rp, tb, rs);
-    int32_t t = 0;
+    root_psi_regs<PER>(rp, S.tab, rs);
+    auto old_state = [&](int32_t t) -> int32_t {
+      return __builtin_amdgcn_readfirstlane(out_state[(int64_t)t * B + b]);
+    };
+    auto emit = [&](int32_t t, const Answer& a, float lse) {
+      if (lane == 0) {
+        const int64_t oi = (int64_t)t * B + b;
+        out_tok[oi] = a.tok;
+        out_state[oi] = a.ns;
+        out_score[oi] = (a.zv - lse) + a.b;
+      }
+    };
+    int32_t done = 0;  // rows before this are exact
     for (int32_t gg = 1; gg < G; ++gg) {
       const int32_t tb0 = gg * W * L;
       if (tb0 >= T) break;
-      if (t > tb0) continue;  // an earlier repair already ran past this boundary
-      t = tb0;
-      int32_t x = __builtin_amdgcn_readfirstlane(out_state[(int64_t)(t - 1) * B + b]);
+      if (done > tb0) continue;  // an earlier repair already ran past this boundary
+      if (gg > 1) {
+        load_row<Ld, PER>(ra, col + (int64_t)tb0 * tstride, rs);
+        load_row<Ld, PER>(rb, col + (int64_t)(tb0 + 1 < T ? tb0 + 1 : tb0) * tstride, rs);
+      }
+      int32_t x = __builtin_amdgcn_readfirstlane(out_state[(int64_t)(tb0 - 1) * B + b]);
       if (x < 0 || x >= n) {  // invalid carried state (-2) or a timed-out main kernel (-3)
         timed_out = x == kStateTimeout;
         break;
       }
-      for (; t < T; ++t) {
-        float cur[PER];
-        load_row<Ld, PER>(cur, logits + ((int64_t)t * B + b) * stride, rs);
-        float lse;
-        const Answer a = full_step<PER>(Gr, tb, zrow, stamps, tag, cur, rp, rs, x, 1, V, lse);
-        const int64_t oi = (int64_t)t * B + b;
-        const int32_t old = __builtin_amdgcn_readfirstlane(out_state[oi]);
-        if (lane == 0) {
-          out_tok[oi] = a.tok;
-          out_state[oi] = a.ns;
-          out_score[oi] = (a.zv - lse) + a.b;
-        }
-        x = __builtin_amdgcn_readfirstlane(a.ns);
-        if (x == old) {
-          ++t;
-          break;
-        }
-      }
+      // the rows up to the meeting point are recomputed; find where it was
+      int32_t t_stop = tb0;
+      auto emit_track = [&](int32_t t, const Answer& a, float lse) {
+        emit(t, a, lse);
+        t_stop = t + 1;
+      };
+      repair_run<Ld, PER, true>(Gr, S.tab, S.zrow, S.stamps, tag, rp, rs, col, tstride, tb0, T,
+                                x, 1, V, ra, rb, rc, old_state, emit_track);
+      done = t_stop;
     }
   }
-  if (lane == 0) states[b] = timed_out ? kStateTimeout : out_state[(int64_t)(T - 1) * B + b];
+  if (lane == 0 && threadIdx.x < 64)
+    states[b] = timed_out ? kStateTimeout : out_state[(int64_t)(T - 1) * B + b];
 }
 
-// Launch geometry: workgroups per stream G and segment length L.
+// Short calls (T <= W steps, a streaming chunk): no speculation. Wave w
+// summarises row w (normaliser, best root move, row copy in LDS) in parallel;
+// then wave 0 takes the T state-dependent steps in order from LDS.
+template <class Ld, int PER>
+__global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
+    ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
+    const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
+    int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
+    float* __restrict__ out_score) {
+  constexpr int NT = Shape<PER>::NT;
+  constexpr int HOT = SegLds<PER>::HOT;
+  __shared__ SegLds<PER> S;
+  const int32_t V1 = A.V1, V = V1 - 1;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = __lane_id();
+  const int32_t b = blockIdx.x;
+  const typename Ld::T* col = logits + (int64_t)b * stride;
+  const int64_t tstride = (int64_t)B * stride;
+
+  const int32_t m = model_ids[b];
+  const int32_t s0 = states[b];
+  int32_t off = 0, n = 0;
+  const int mode = resolve_stream(A, m, s0, off, n);
+  const RowShape<PER> rs(V1);
+  float raw[PER];
+  if (w < T) load_row<Ld, PER>(raw, col + (int64_t)w * tstride, rs);
+
+  fill_tables<PER, NT>(S.tab, A, m, mode);
+  const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
+  fill_hot<HOT, NT>(S.hot, A, off, nhot);
+  for (int32_t i = threadIdx.x; i < 16 * PER; i += NT)
+    reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
+  __syncthreads();
+
+  if (w < T) {
+    float rp[PER];
+    root_psi_regs<PER>(rp, S.tab, rs);
+    const RowSum r = row_summary<PER>(S.zbuf[w], raw, rp, rs, V, true);
+    if (lane == 0) {
+      S.rsum[w][0] = r.zb;
+      S.rsum[w][1] = r.ymax;
+      S.rsum[w][2] = r.lse;
+      S.rsum[w][3] = __int_as_float(r.r1_tok);
+    }
+  }
+  __syncthreads();
+  if (w != 0) return;
+
+  const Graph Gr(A, off, nhot, S.hot);
+  uint32_t tag = 0;
+  int32_t s = (mode == 1) ? s0 : ((mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID);
+  int32_t o_tok = 0, o_st = 0;
+  float o_sc = 0.f;
+  for (int32_t t = 0; t < T; ++t) {
+    RowSum r;
+    r.zb = S.rsum[t][0];
+    r.ymax = S.rsum[t][1];
+    r.lse = S.rsum[t][2];
+    r.r1_tok = __float_as_int(S.rsum[t][3]);
+    const Answer a = step_from<PER>(Gr, S.tab, S.zbuf[t], S.stamps[0], tag, rs, r, s, mode, V);
+    const bool mine = lane == t;
+    o_tok = mine ? a.tok : o_tok;
+    o_st = mine ? a.ns : o_st;
+    o_sc = mine ? (a.zv - r.lse) + a.b : o_sc;
+    s = __builtin_amdgcn_readfirstlane(a.ns);
+  }
+  if (lane < T) {
+    const int64_t oi = (int64_t)lane * B + b;
+    out_tok[oi] = o_tok;
+    out_state[oi] = o_st;
+    out_score[oi] = o_sc;
+  }
+  if (lane == 0) states[b] = s;
+}
+
+// Launch geometry: workgroups per stream G and segment length L. Short calls
+// (a streaming chunk) use one workgroup per stream and segments of a few
+// rows; long calls use enough workgroups to cover the 256 CUs, with segments
+// of at least kMinSeg rows.
 template <int PER>
 inline void seg_geometry(int32_t T, int32_t B, int32_t& G, int32_t& L) {
   constexpr int W = Shape<PER>::W;
-  // enough workgroups to cover the 256 CUs, but segments of at least kMinSeg rows
+  if (T <= W * kMinSeg) {
+    G = 1;
+    L = (T + W - 1) / W;
+    if (L < 2) L = 2;
+    return;
+  }
   G = (256 + B - 1) / B;
-  const int32_t gmax = (T + W * kMinSeg - 1) / (W * kMinSeg);
+  const int32_t gmax = T / (W * kMinSeg);
   if (G > gmax) G = gmax;
   if (G < 1) G = 1;
   L = (T + G * W - 1) / (G * W);
-  if (L < kMinSeg) L = kMinSeg;
   // every workgroup must own rows (an empty one would not hand on a state)
   while (G > 1 && (G - 1) * W * L >= T) --G;
 }
@@ -604,6 +845,12 @@ hipError_t launch_seg(const ArenaView& A, const void* logits, int32_t T, int32_t
   typedef typename Ld::T TT;
   static_assert(sizeof(SegLds<PER>) <= Shape<PER>::kBudget + 1024, "LDS budget");
   static_assert(SegLds<PER>::HOT >= 64, "room for hot states");
+  if (T <= Shape<PER>::W) {
+    hipLaunchKernelGGL((greedy_chunk_kernel<Ld, PER>), dim3(B), dim3(Shape<PER>::NT), 0, st, A,
+                       static_cast<const TT*>(logits), T, B, stride, model_ids, states, out_tok,
+                       out_state, out_score);
+    return hipGetLastError();
+  }
   int32_t G, L;
   seg_geometry<PER>(T, B, G, L);
   hipLaunchKernelGGL((greedy_seg_kernel<Ld, PER>), dim3(B * G), dim3(Shape<PER>::NT), 0, st, A,
@@ -611,7 +858,7 @@ hipError_t launch_seg(const ArenaView& A, const void* logits, int32_t T, int32_t
                      out_tok, out_state, out_score);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || G == 1) return e;
-  hipLaunchKernelGGL((greedy_fix_kernel<Ld, PER>), dim3(B), dim3(64), 0, st, A,
+  hipLaunchKernelGGL((greedy_fix_kernel<Ld, PER>), dim3(B), dim3(kFixThreads), 0, st, A,
                      static_cast<const TT*>(logits), T, B, stride, G, L, Shape<PER>::W,
                      model_ids, states, out_tok, out_state, out_score);
   return hipGetLastError();

@@ -207,12 +207,14 @@ def test_stream_permutation_permutes_outputs():
 
 @pytest.mark.parametrize("kernel", ["seg", "pipe"])
 @pytest.mark.parametrize("name,T,chunk", [("tiny", 50, 50), ("batched", 500, 500),
-                                          ("streaming", 1024, 1024), ("streaming", 200, 37)])
+                                          ("streaming", 1024, 1024), ("streaming", 200, 37),
+                                          ("streaming", 96, 16), ("batched", 40, 7)])
 def test_greedy_kernels_agree_with_reference_kernel(kernel, name, T, chunk, monkeypatch):
     """The segmented and pipelined kernels give the reference kernel's outputs:
     tokens, states and carries identical, scores within rounding of the
     normaliser. Whole-length calls make the segmented kernel split streams
-    over several workgroups and run its boundary fix-up."""
+    over several workgroups and run its boundary fix-up; calls of at most 16
+    steps take the short-call kernel."""
     from paper_2608_21343_amd.decoder import to_device_logits
     cfg = W.config_by_name(name)
     lists = W.phrases(cfg)
