@@ -1,25 +1,29 @@
 """Benchmark of the boosted greedy decode step on one MI355X.
 
-Workload: the streaming greedy decode — B=128 streams, V=1024 tokens + blank,
-T=1024 steps fed in streaming chunks of 16 steps (64 calls, graph states
-carried across calls), fp32 joint logits N(0,1) with a +1.5 blank offset, and
-per-stream phrase lists of 1000 phrases (lengths 1-10, Zipf 1.1). All inputs
-are synthetic and seeded (workloads.logit_chunks); they are resident in HBM
-before the timed region starts.
+Workload: streaming greedy decoding -- B=128 streams, V=1024 tokens + blank,
+T=1024 steps fed as 64 calls of 16 steps each with the graph states carried
+from call to call; fp32 joint logits N(0,1) with a +1.5 blank offset; every
+stream has its own list of 1000 phrases (lengths 1-10, Zipf 1.1) and a
+case-insensitive token map. All inputs are synthetic and seeded
+(workloads.logit_chunks) and are resident in HBM before the timed region.
 
-One bench step = one pass of the whole hot path over the workload (all 64
-chunk calls). Printed value: token-scores per second (T*B*K*(V+1) per step /
-step time). ``roofline`` reports the greedy kernel's achieved algorithmic
-bandwidth from HIP events around every launch in the timed region;
-``cpu_baseline`` times the CPU oracle on a bounded sample of streams.
+One bench step = one pass of the whole hot path over that workload: state
+initialisation plus the 64 chunk calls. ``value`` is token-scores per second
+(T*B*K*(V+1) per step / step time). ``roofline`` describes the greedy
+short-call kernel (one launch per 16-step chunk): algorithmic bytes per launch
+over its mean duration, timed with HIP events around every launch of the
+timed region. ``whole_call`` times the same workload decoded by one call over
+all 1024 steps (the segmented kernel plus its boundary fix-up), for context.
+``cpu_baseline`` times the CPU oracle on the whole workload over a process
+pool (decode only).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                       [--copy-probe]
 """
 
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -32,33 +36,11 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 WORKLOAD = "streaming"
-KERNEL_SOURCES = ["paper_2608_21343_amd/csrc/greedy.hip", "paper_2608_21343_amd/csrc/device.hpp"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_streaming_traffic.json")
-
-
-def kernel_hash() -> str:
-    h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
-
-
-def measured_traffic(bytes_per_launch_alg: float):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
-    try:
-        with open(TRAFFIC_FILE) as fh:
-            rec = json.load(fh)
-    except (OSError, ValueError):
-        return None
-    if rec.get("kernel_hash") != kernel_hash():
-        return None
-    return rec.get("hbm_bytes_per_launch")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_chunk_streaming_traffic.json")
 
 
 def _cpu_worker(args):
-    """Oracle greedy decode of a few streams; returns (rows, seconds of decode)."""
+    """Oracle greedy decode of some streams; returns (rows, seconds of decode)."""
     name, streams = args
     import oracle
     import workloads as W
@@ -74,11 +56,11 @@ def _cpu_worker(args):
     return rows.shape[0] * rows.shape[1], time.perf_counter() - t0
 
 
-def cpu_baseline(cfg, n_streams: int):
-    """Time the CPU oracle on n_streams streams of the workload (all T steps)."""
+def cpu_baseline(cfg):
+    """The CPU oracle on every stream of the workload, one process per core."""
     import multiprocessing as mp
-    cores = min(len(os.sched_getaffinity(0)), 16, n_streams)
-    streams = list(range(0, cfg.B, max(1, cfg.B // n_streams)))[:n_streams]
+    cores = min(len(os.sched_getaffinity(0)), 16, cfg.B)
+    streams = list(range(cfg.B))
     parts = [streams[i::cores] for i in range(cores)]
     ctx = mp.get_context("spawn")
     with ctx.Pool(cores) as pool:
@@ -90,8 +72,9 @@ def cpu_baseline(cfg, n_streams: int):
         "unit": "token-scores/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": f"{len(streams)} of {cfg.B} streams x all {cfg.T} steps "
-                  f"({rows} rows), one process per core, decode time only",
+        "sample": f"the whole workload: all {cfg.B} streams x {cfg.T} steps ({rows} rows), "
+                  f"streams split over {cores} processes; decode time only (graph "
+                  f"building and logit generation untimed); wall = slowest process",
         "seconds": secs,
     }
 
@@ -102,23 +85,32 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-streams", type=int, default=16)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first run one plain 256 MiB device copy (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              f"(the streams are independent; see DESIGN.md for how the path shards)",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the "
+              f"streams are independent and shard by stream, see DESIGN.md)", file=sys.stderr)
         return 2
 
     import torch
     import workloads as W
-    from paper_2608_21343_amd import capi
+    from paper_2608_21343_amd import capi, profiling
     from paper_2608_21343_amd.decoder import BoostDecoder
 
     if not torch.cuda.is_available():
         print("bench.py needs a HIP device", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        n = profiling.COPY_PROBE_BYTES // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     cfg = W.config_by_name(WORKLOAD)
     T, B, V1, chunk = cfg.T, cfg.B, cfg.Vp1, cfg.chunk
     lists = W.phrases(cfg)
@@ -159,42 +151,63 @@ def main() -> int:
     wall = time.perf_counter() - t0
     launch_ms = [a.elapsed_time(b) for step in ev for (a, b) in step]
     avg_launch_s = float(np.mean(launch_ms)) / 1e3
+    chunked = (tok.clone(), sst.clone(), sc.clone())
 
-    ms_per_step = wall / args.steps * 1e3
+    step_s = wall / args.steps
     token_scores = T * B * cfg.K * V1
-    value = token_scores / (wall / args.steps)
-    # algorithmic bytes per launch: logits read once, 12 B of outputs per row,
-    # model id + carried state (read and write) per stream
-    rows_per_launch = chunk * B
-    alg_bytes = rows_per_launch * (V1 * 4 + 12) + B * 12
+    # algorithmic bytes per launch: the chunk's logit rows read once, 12 B of
+    # outputs per row, and per stream the model id, the carried state read
+    # and the carried state written
+    alg_bytes = chunk * B * (V1 * 4 + 12) + B * 12
     achieved = alg_bytes / avg_launch_s / 1e9
-    traffic = measured_traffic(alg_bytes)
+
+    # context: the same workload as one call over all T steps
+    whole_ms = []
+    for rep in range(4):
+        capi.tb_init_states(dec.arena, B, 1, mids, states)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        capi.tb_boost_step_greedy(dec.arena, logits, mids, states, tok, sst, sc)
+        b.record(stream)
+        torch.cuda.synchronize()
+        if rep > 0:
+            whole_ms.append(a.elapsed_time(b))
+    whole_s = float(np.median(whole_ms)) / 1e3
+    whole_bytes = T * B * (V1 * 4 + 12) + B * 12
+    same = all(torch.equal(x, y) for x, y in zip(chunked[:2], (tok, sst)))
+
     result = {
         "metric": "boosted decode token-scores/s (B x K x (V+1) per step) with achieved HBM GB/s",
-        "value": value,
+        "value": token_scores / step_s,
         "unit": "token-scores/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": step_s * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "streaming greedy boosted decode", "B": B, "K": 1, "V": cfg.V,
-                   "T": T, "chunk": chunk, "logits": "fp32 N(0,1), blank +1.5",
-                   "phrases_per_stream": cfg.n_phrases, "launches_per_step": n_launch},
+        "config": {"workload": "streaming greedy boosted decode, 64 calls of 16 steps",
+                   "B": B, "K": 1, "V": cfg.V, "T": T, "chunk": chunk,
+                   "logits": "fp32 N(0,1), blank +1.5", "phrases_per_stream": cfg.n_phrases,
+                   "launches_per_step": n_launch},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "greedy step", "alg_bytes_per_launch": alg_bytes,
-                     "avg_launch_us": avg_launch_s * 1e6},
-        "steps_per_s": T / (wall / args.steps),
-        "wall_GBps": (alg_bytes * n_launch) / (wall / args.steps) / 1e9,
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": profiling.load_traffic(TRAFFIC_FILE),
+                     "kernel": "greedy short-call kernel (one launch per 16-step chunk)",
+                     "alg_bytes_per_launch": alg_bytes, "avg_launch_us": avg_launch_s * 1e6},
+        "steps_per_s": T / step_s,
+        "whole_call": {"ms": whole_s * 1e3, "token_scores_per_s": token_scores / whole_s,
+                       "achieved_GBps": whole_bytes / whole_s / 1e9,
+                       "frac": whole_bytes / whole_s / 1e9 / HBM_PEAK_GBS,
+                       "kernels": "segmented greedy kernel + boundary fix-up",
+                       "outputs_equal_chunked": bool(same)},
         "compile_s": compile_s,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, args.cpu_streams)
+        result["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(result), flush=True)
     return 0
 

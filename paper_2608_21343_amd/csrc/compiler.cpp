@@ -393,14 +393,34 @@ extern "C" int tb_validate_image(const void* host_image, const tb_arena_layout* 
         if (lb[fc[s] + j] <= lb[fc[s] + j - 1])
           return fail(TB_ERANGE, "children labels not ascending");
     }
+    // root rows: the root move of a token is the root's child on its class,
+    // else the root itself; its psi is that state's psi; the blank column is 0
     const int32_t* rd = I32(L.off_root_dst) + (int64_t)m * V1;
-    for (int32_t v = 0; v < V1; ++v)
-      if (rd[v] < 0 || rd[v] >= n) return fail(TB_ERANGE, "root row target out of range");
+    const float* rp = reinterpret_cast<const float*>(img + L.off_root_psi) + (int64_t)m * V1;
+    const float* ps = reinterpret_cast<const float*>(img + L.off_psi) + off;
+    std::vector<int32_t> child_on(V, 0);
+    for (int32_t j = 0; j < nc[0]; ++j) child_on[lb[fc[0] + j]] = fc[0] + j;
+    for (int32_t v = 0; v < V; ++v) {
+      const int32_t want = cm[v] >= 0 ? child_on[cm[v]] : 0;
+      if (rd[v] != want || !(rp[v] == ps[want]))
+        return fail(TB_ERANGE, "root row of model " + std::to_string(m) + " inconsistent at token " +
+                                   std::to_string(v));
+    }
+    if (rd[V] != 0 || rp[V] != 0.f) return fail(TB_ERANGE, "root row blank column not zero");
   }
   if (expect_off != L.n_states) return fail(TB_ERANGE, "state count mismatch");
   const int32_t* cp = I32(L.off_cls_ptr);
   if (cp[0] != 0) return fail(TB_ERANGE, "cls_ptr[0] != 0");
   for (int32_t c = 0; c < V; ++c)
     if (cp[c + 1] < cp[c] || cp[c + 1] > V) return fail(TB_ERANGE, "cls_ptr not monotone");
+  // class members: every token of class c listed once under c, ascending
+  const int32_t* ct = I32(L.off_cls_tok);
+  int32_t n_member = 0;
+  for (int32_t v = 0; v < V; ++v) n_member += cm[v] >= 0;
+  if (cp[V] != n_member) return fail(TB_ERANGE, "cls_ptr total differs from the classed tokens");
+  for (int32_t c = 0; c < V; ++c)
+    for (int32_t q = cp[c]; q < cp[c + 1]; ++q)
+      if (ct[q] < 0 || ct[q] >= V || cm[ct[q]] != c || (q > cp[c] && ct[q] <= ct[q - 1]))
+        return fail(TB_ERANGE, "class member list of class " + std::to_string(c) + " inconsistent");
   return TB_OK;
 }

@@ -148,6 +148,15 @@ def test_validate_rejects_corrupt_images():
     corrupt(L.off_n_child, 10_000)            # child range past the model
     corrupt(L.off_root_dst + 4 * 7, 1 << 20)  # root row target out of range
     corrupt(L.off_model_n, 0)                 # model table
+    # root rows must agree with the root's children
+    rd7 = int(np.frombuffer(good, dtype=np.int32, count=1, offset=L.off_root_dst + 4 * 7)[0])
+    corrupt(L.off_root_dst + 4 * 7, 1 if rd7 != 1 else 2)
+    corrupt(L.off_root_psi + 4 * 7, int(np.float32(123.0).view(np.int32)))
+    corrupt(L.off_root_psi + 4 * cfg.V, int(np.float32(1.0).view(np.int32)))  # blank column
+    # class member lists must list each classed token under its own class
+    ct0 = int(np.frombuffer(good, dtype=np.int32, count=1, offset=L.off_cls_tok)[0])
+    other = int(np.nonzero(cm[:cfg.V] != cm[ct0])[0][0])
+    corrupt(L.off_cls_tok, other)
     capi.tb_validate_image(good, L)
 
 

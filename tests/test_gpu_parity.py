@@ -293,3 +293,48 @@ def test_segments_longer_than_the_kept_trajectory():
     compare_greedy(gpu, ref, sample, ATOL, ref_streams=range(len(sample)))
     assert np.array_equal(gpu[3][sample], ref[3])
     assert np.max(ref[1][:, 0]) >= 100
+
+
+def test_chunk_loop_graph_replay_matches_eager():
+    """The streaming chunk loop captured in a HIP graph: every replay (with
+    eager work and synchronisation in between) reproduces the eager outputs."""
+    import torch
+    from paper_2608_21343_amd import capi
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg = W.config_by_name("streaming")
+    T, B, chunk = 96, cfg.B, 16
+    dec = _decoder(cfg, W.phrases(cfg))
+    logits = to_device_logits(W.logits(cfg, 0, T)[:, :, 0, :])
+    mids, states, _ = dec.start(W.model_ids(cfg))
+    tok = torch.empty((T, B), dtype=torch.int32, device="cuda")
+    sst = torch.empty_like(tok)
+    sc = torch.empty((T, B), dtype=torch.float32, device="cuda")
+
+    def run():
+        capi.tb_init_states(dec.arena, B, 1, mids, states)
+        for ta in range(0, T, chunk):
+            capi.tb_boost_step_greedy(dec.arena, logits[ta:ta + chunk], mids, states,
+                                      tok[ta:ta + chunk], sst[ta:ta + chunk], sc[ta:ta + chunk])
+
+    run()
+    torch.cuda.synchronize()
+    ref = [x.clone() for x in (tok, sst, sc, states)]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    for rep in range(3):
+        tok.fill_(-7)
+        sst.fill_(-7)
+        sc.fill_(0.5)
+        states.fill_(3)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip((tok, sst, sc, states), ref):
+            assert torch.equal(a, b), f"replay {rep} differs from the eager run"
