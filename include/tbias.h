@@ -73,6 +73,13 @@ typedef struct tb_graphs tb_graphs;
  *   class_map   int32[V+1]        token -> case class (blank: -1)
  *   cls_ptr     int32[V+1]        CSR over classes: members of class c are
  *   cls_tok     int32[V]          cls_tok[cls_ptr[c] .. cls_ptr[c+1]-1], ascending
+ *   arc_mem     uint32[2*n_states] the class on the arc into every state with
+ *                                 its first three members m0 <= m1 <= m2
+ *                                 (repeating the last when the class is
+ *                                 smaller): word 0 = m0 | m1 << 16, word 1 =
+ *                                 m2 | class << 16 | (more than three
+ *                                 members ? 1 << 31 : 0); roots: 0, 0
+ *                                 (token ids and classes below 2^15)
  */
 typedef struct {
   int64_t total_bytes;
@@ -83,6 +90,7 @@ typedef struct {
   int64_t off_first_child, off_n_child, off_link, off_label, off_phi, off_psi;
   int64_t off_root_psi, off_root_dst;
   int64_t off_class_map, off_cls_ptr, off_cls_tok;
+  int64_t off_arc_mem;
   int32_t max_children;  /* largest out-degree of any state */
   int32_t max_depth;     /* deepest state (phrase length) */
 } tb_arena_layout;
@@ -109,6 +117,7 @@ typedef struct {
  *                     boosting weight, folded into phi and psi
  *   class_map         host int32[v_plus_blank]; class of every token (a token
  *                     id in [0, V)), class_map[V] must be -1
+ *   v_plus_blank      V + 1, in [2, 32768]
  *   semantics         TB_COMMIT (default reading) or TB_PURE_POTENTIAL
  *   n_threads         host threads to use (<= 0: hardware concurrency)
  *   out               receives the library-owned result; free with
@@ -116,8 +125,9 @@ typedef struct {
  *
  * An empty list gives a root-only graph (state 0, zero boost). Duplicate
  * phrases (after case folding) are merged. Errors: TB_EINVAL (null pointers,
- * non-monotone CSR), TB_ERANGE (token outside [0, V), a token whose class is
- * -1, an empty phrase, a class id outside [0, V)), TB_ENOMEM.
+ * non-monotone CSR, v_plus_blank < 2), TB_ERANGE (token outside [0, V), a
+ * token whose class is -1, an empty phrase, a class id outside [0, V),
+ * v_plus_blank > 32768), TB_ENOMEM.
  */
 int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_ptr,
                       const int64_t* phrase_tok_ptr, const int32_t* phrase_tokens,
@@ -144,7 +154,8 @@ void tb_graphs_free(tb_graphs* g);
 /*
  * Check a host copy of an arena image for consistency (every index in range,
  * suffix links pointing to smaller ids, children contiguous with ascending
- * labels, root rows consistent with the root's children). TB_OK or TB_ERANGE.
+ * labels, root rows consistent with the root's children, class member lists
+ * and arc member records consistent with the class map). TB_OK or TB_ERANGE.
  */
 int tb_validate_image(const void* host_image, const tb_arena_layout* layout);
 

@@ -36,6 +36,7 @@ class tb_arena_layout(C.Structure):
         ("off_phi", C.c_int64), ("off_psi", C.c_int64),
         ("off_root_psi", C.c_int64), ("off_root_dst", C.c_int64),
         ("off_class_map", C.c_int64), ("off_cls_ptr", C.c_int64), ("off_cls_tok", C.c_int64),
+        ("off_arc_mem", C.c_int64),
         ("max_children", C.c_int32),
         ("max_depth", C.c_int32),
     ]
@@ -304,4 +305,5 @@ def image_arrays(image: np.ndarray, layout: tb_arena_layout) -> dict:
         "class_map": arr(L.off_class_map, V1, np.int32),
         "cls_ptr": arr(L.off_cls_ptr, V1, np.int32),
         "cls_tok": arr(L.off_cls_tok, V1 - 1, np.int32),
+        "arc_mem": arr(L.off_arc_mem, 2 * L.n_states, np.uint32),
     }

@@ -218,6 +218,7 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   if (!model_phrase_ptr || !phrase_tok_ptr || !token_w || !end_bonus || !class_map)
     return fail(TB_EINVAL, "NULL input array");
   if (v_plus_blank < 2) return fail(TB_EINVAL, "v_plus_blank must be >= 2");
+  if (v_plus_blank > 32768) return fail(TB_ERANGE, "v_plus_blank must be <= 32768");
   if (semantics != TB_COMMIT && semantics != TB_PURE_POTENTIAL)
     return fail(TB_EINVAL, "unknown semantics");
   const int32_t V = v_plus_blank - 1;
@@ -300,6 +301,7 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   L.off_class_map = take(4 * (int64_t)v_plus_blank);
   L.off_cls_ptr = take(4 * (int64_t)v_plus_blank);
   L.off_cls_tok = take(4 * (int64_t)V);
+  L.off_arc_mem = take(8 * N);
   L.total_bytes = off;
   try {
     g->image.assign((size_t)off, 0);
@@ -339,6 +341,22 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   std::vector<int32_t> fillp(cp, cp + V);
   for (int32_t v = 0; v < V; ++v)
     if (class_map[v] >= 0) ct[fillp[class_map[v]]++] = v;
+  // member tokens of the class on the arc into every state (see arc_mem in tbias.h)
+  uint32_t* am = reinterpret_cast<uint32_t*>(img + L.off_arc_mem);
+  for (int64_t y = 0; y < N; ++y) {
+    const int32_t lab = I32(L.off_label)[y];
+    if (lab < 0) {  // a root
+      am[2 * y] = 0u;
+      am[2 * y + 1] = 0u;
+      continue;
+    }
+    const int32_t m0 = cp[lab], nm = cp[lab + 1] - cp[lab];
+    const uint32_t t0 = (uint32_t)ct[m0];
+    const uint32_t t1 = (uint32_t)ct[m0 + (nm > 1 ? 1 : 0)];
+    const uint32_t t2 = (uint32_t)ct[m0 + (nm > 2 ? 2 : nm - 1)];
+    am[2 * y] = t0 | (t1 << 16);
+    am[2 * y + 1] = t2 | ((uint32_t)lab << 16) | (nm > 3 ? 0x80000000u : 0u);
+  }
   *out = g;
   return TB_OK;
 }
@@ -422,5 +440,23 @@ extern "C" int tb_validate_image(const void* host_image, const tb_arena_layout* 
     for (int32_t q = cp[c]; q < cp[c + 1]; ++q)
       if (ct[q] < 0 || ct[q] >= V || cm[ct[q]] != c || (q > cp[c] && ct[q] <= ct[q - 1]))
         return fail(TB_ERANGE, "class member list of class " + std::to_string(c) + " inconsistent");
+  // arc member records agree with the labels and the class member lists
+  const uint32_t* am = reinterpret_cast<const uint32_t*>(img + L.off_arc_mem);
+  const int32_t* lab_all = I32(L.off_label);
+  for (int64_t y = 0; y < L.n_states; ++y) {
+    const int32_t lab = lab_all[y];
+    if (lab < 0) {
+      if (am[2 * y] != 0u || am[2 * y + 1] != 0u) return fail(TB_ERANGE, "root arc record not zero");
+      continue;
+    }
+    const int32_t m0 = cp[lab], nm = cp[lab + 1] - cp[lab];
+    if (nm < 1) return fail(TB_ERANGE, "arc label of a class without members");
+    const uint32_t t0 = (uint32_t)ct[m0];
+    const uint32_t t1 = (uint32_t)ct[m0 + (nm > 1 ? 1 : 0)];
+    const uint32_t t2 = (uint32_t)ct[m0 + (nm > 2 ? 2 : nm - 1)];
+    const uint32_t w1 = t2 | ((uint32_t)lab << 16) | (nm > 3 ? 0x80000000u : 0u);
+    if (am[2 * y] != (t0 | (t1 << 16)) || am[2 * y + 1] != w1)
+      return fail(TB_ERANGE, "arc member record of state " + std::to_string(y) + " inconsistent");
+  }
   return TB_OK;
 }

@@ -24,6 +24,7 @@ struct ArenaView {
   const int32_t* class_map;
   const int32_t* cls_ptr;
   const int32_t* cls_tok;
+  const uint32_t* arc_mem;  // two words per state (see tb_arena_layout)
   int32_t n_models;
   int32_t V1;  // V + 1
 };
@@ -45,6 +46,7 @@ inline ArenaView make_view(const tb_arena& a) {
   v.class_map = reinterpret_cast<const int32_t*>(b + L.off_class_map);
   v.cls_ptr = reinterpret_cast<const int32_t*>(b + L.off_cls_ptr);
   v.cls_tok = reinterpret_cast<const int32_t*>(b + L.off_cls_tok);
+  v.arc_mem = reinterpret_cast<const uint32_t*>(b + L.off_arc_mem);
   v.n_models = L.n_models;
   v.V1 = L.v_plus_blank;
   return v;

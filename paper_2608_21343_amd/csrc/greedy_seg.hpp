@@ -51,6 +51,20 @@ constexpr int32_t kStateTimeout = -3;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 
+// State-independent facts of one row: blank logit, best root move (key,
+// token, its class, target state, target psi and logit) and normaliser.
+struct RowSum {
+  float zb, ymax, lse, r1_psi, r1_z;
+  int32_t r1_tok, r1_cls, r1_dst;
+};
+
+// A lane's two best root moves (token ids; kNoTok when the lane has none),
+// tracked only by the short-call kernel.
+constexpr int32_t kNoTok = 0xffff;
+struct LaneTop {
+  int32_t i1, i2;
+};
+
 // Tables shared by the waves of one workgroup (one stream).
 template <int PER>
 struct alignas(16) Tables {
@@ -76,24 +90,23 @@ struct alignas(16) FixedLds {
   uint8_t stamps[W][64 * PER];
   Tables<PER> tab;
   int32_t traj[W][kTraj];  // state after each of the first kTraj steps
-  float rsum[W][4];        // short calls: per-row blank logit, best root key, normaliser, token
+  RowSum rsum[W];          // short calls: summary of row w
+  uint32_t rtop[W][64];    // short calls: each lane's two best root moves of row w
   int32_t fin_state[W];    // exact state after each segment
   int32_t fin_ready[W];
   int32_t abort_flag;
 };
 
 // Records of the first HOT states of a model (BFS order: the shallowest, the
-// most visited) held in LDS.
+// most visited) held in LDS: one 16-byte state record and the 8-byte record
+// of the arc into the state (its class and first three members, as arc_mem).
 template <int HOT>
 struct alignas(16) HotRecords {
-  int32_t fc[HOT];      // first child
-  uint32_t lknc[HOT];   // link | n_child << 16
-  float phi[HOT];
-  float psi[HOT];
-  uint16_t label[HOT];  // class on the arc into the state
+  int4 rec[HOT];   // first child, link | n_child << 16, phi bits, psi bits
+  uint2 mem[HOT];  // arc member record
 };
 
-constexpr int kHotRecordBytes = 4 + 4 + 4 + 4 + 2;
+constexpr int kHotRecordBytes = 16 + 8;
 template <int PER>
 constexpr int hot_states() {
   const int room = (Shape<PER>::kBudget - (int)sizeof(FixedLds<PER>)) / kHotRecordBytes;
@@ -154,35 +167,33 @@ struct RowShape {
 struct Graph {
   const ArenaView* A;
   int32_t off, nhot;
-  const int32_t* hs_fc;
-  const uint32_t* hs_lknc;
-  const float* hs_phi;
-  const float* hs_psi;
-  const uint16_t* hs_label;
+  const int4* hrec;
+  const uint2* hmem;
   template <int HOT>
   __device__ __forceinline__ Graph(const ArenaView& a, int32_t o, int32_t nh,
                                    const HotRecords<HOT>& h)
-      : A(&a), off(o), nhot(nh), hs_fc(h.fc), hs_lknc(h.lknc), hs_phi(h.phi), hs_psi(h.psi),
-        hs_label(h.label) {}
-  __device__ __forceinline__ float phi(int32_t x) const {
-    return x < nhot ? hs_phi[x] : sload(A->phi + off + x);
-  }
-  __device__ __forceinline__ float psi(int32_t x) const {
-    return x < nhot ? hs_psi[x] : sload(A->psi + off + x);
-  }
-  __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk) const {
+      : A(&a), off(o), nhot(nh), hrec(h.rec), hmem(h.mem) {}
+  // first child, child count, suffix link and phi of state x (uniform)
+  __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
+                                      float& phi) const {
     if (x < nhot) {
-      fc = hs_fc[x];
-      const uint32_t v = hs_lknc[x];
-      lnk = (int32_t)(v & 0xffffu);
-      nc = (int32_t)(v >> 16);
+      const int4 r = hrec[x];
+      fc = r.x;
+      lnk = (int32_t)((uint32_t)r.y & 0xffffu);
+      nc = (int32_t)((uint32_t)r.y >> 16);
+      phi = __int_as_float(r.z);
     } else {
       fc = sload(A->first_child + off + x);
       nc = sload(A->n_child + off + x);
       lnk = sload(A->link + off + x);
+      phi = sload(A->phi + off + x);
     }
   }
 };
+
+// Arc member record fields.
+__device__ __forceinline__ int32_t arc_class(uint2 m) { return (int32_t)((m.y >> 16) & 0x7fffu); }
+__device__ __forceinline__ bool arc_more(uint2 m) { return (m.y >> 31) != 0u; }
 
 // Records of states [0, nhot) of the model at off into LDS; NT threads.
 template <int HOT, int NT>
@@ -192,12 +203,14 @@ __device__ __forceinline__ void fill_hot(HotRecords<HOT>& h, const ArenaView& A,
   for (int k = 0; k < (HOT + NT - 1) / NT; ++k) {
     const int32_t i = k * NT + (int32_t)threadIdx.x;
     if (i < nhot) {
-      h.fc[i] = A.first_child[off + i];
-      h.lknc[i] = (uint32_t)A.link[off + i] | ((uint32_t)A.n_child[off + i] << 16);
-      h.phi[i] = A.phi[off + i];
-      h.psi[i] = A.psi[off + i];
-      const int32_t lab = A.label[off + i];
-      h.label[i] = (uint16_t)(lab < 0 ? 0 : lab);
+      int4 r;
+      r.x = A.first_child[off + i];
+      r.y = (int32_t)((uint32_t)A.link[off + i] | ((uint32_t)A.n_child[off + i] << 16));
+      r.z = __float_as_int(A.phi[off + i]);
+      r.w = __float_as_int(A.psi[off + i]);
+      h.rec[i] = r;
+      const int64_t q = 2 * ((int64_t)off + i);
+      h.mem[i] = make_uint2(A.arc_mem[q], A.arc_mem[q + 1]);
     }
   }
 }
@@ -211,118 +224,230 @@ __device__ __forceinline__ void load_row(float* dst, const typename Ld::T* row,
   dst[PER - 1] = Ld::get(row, rs.last_idx);
 }
 
-// The boosted step from state x on the row in zrow (LDS), given the row's best
-// root move. All lanes take part; the result is uniform.
+// Bumps the 8-bit tag of a wave's class-mark table, clearing it on wrap.
 template <int PER>
-__device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& tb,
-                                             const float* zrow, uint8_t* stamps, uint32_t& tag,
-                                             const RowShape<PER>& rs, int32_t x, float zb,
-                                             float r1_y, int32_t r1_tok, int32_t r1_dst,
-                                             int32_t r1_cls, int32_t V) {
-  const int lane = __lane_id();
-  if (++tag == 256u) {  // 8-bit tags: clear the table on wrap
+__device__ __forceinline__ uint8_t next_tag(uint8_t* stamps, uint32_t& tag) {
+  if (++tag == 256u) {
     uint32_t* w = reinterpret_cast<uint32_t*>(stamps);
-    for (int32_t i = lane; i < 16 * PER; i += 64) w[i] = 0u;
+    for (int32_t i = __lane_id(); i < 16 * PER; i += 64) w[i] = 0u;
     tag = 1;
   }
-  const uint8_t tg = (uint8_t)tag;
-  const float phi_x = G.phi(x);
+  return (uint8_t)tag;
+}
 
-  float lk = kNegInf;
-  int32_t lt = INT_MAX, lns = 0;
-  float lpsi = 0.f;
-  for (int32_t c = x; c != 0;) {
-    int32_t fc, nc, lnk;
-    G.rec(c, fc, nc, lnk);
-    if (fc + nc <= G.nhot) {
-      // children in LDS: one child per lane
+// Per-lane best override candidate.
+struct Cand {
+  float k, z, psi;
+  int32_t tok, ns;
+  __device__ __forceinline__ void offer(float kk, int32_t t, float zz, int32_t y, float py) {
+    if (better(kk, t, k, tok)) { k = kk; tok = t; z = zz; ns = y; psi = py; }
+  }
+};
+
+// Members of the arc class m into state y (psi py) offered by this lane.
+template <int PER>
+__device__ __forceinline__ void offer_members(Cand& c, const Tables<PER>& tb, const float* zrow,
+                                              uint2 m, int32_t y, float py) {
+  if (!arc_more(m)) {  // up to three members, ascending (repeats when fewer)
+    const int32_t t0 = (int32_t)(m.x & 0xffffu), t1 = (int32_t)(m.x >> 16);
+    const int32_t t2 = (int32_t)(m.y & 0xffffu);
+    const float z0 = zrow[t0], z1 = zrow[t1], z2 = zrow[t2];
+    c.offer(z0 + py, t0, z0, y, py);
+    c.offer(z1 + py, t1, z1, y, py);
+    c.offer(z2 + py, t2, z2, y, py);
+  } else {
+    const int32_t lab = arc_class(m);
+    for (int32_t q = tb.cls_ptr[lab]; q < tb.cls_ptr[lab + 1]; ++q) {
+      const int32_t t = tb.cls_tok[q];
+      const float z = zrow[t];
+      c.offer(z + py, t, z, y, py);
+    }
+  }
+}
+
+// Arc record and psi of child y (hot: LDS; else one vector load each).
+__device__ __forceinline__ void child_rec(const Graph& G, int32_t y, uint2& m, float& py) {
+  if (y < G.nhot) {
+    m = G.hmem[y];
+    py = __int_as_float(G.hrec[y].w);
+  } else {
+    const int64_t q = 2 * ((int64_t)G.off + y);
+    m = make_uint2(G.A->arc_mem[q], G.A->arc_mem[q + 1]);
+    py = G.A->psi[G.off + y];
+  }
+}
+
+// Marks the classes of the children [fc, fc+nc) in stamps.
+__device__ __forceinline__ void mark_children(const Graph& G, uint8_t* stamps, uint8_t tg,
+                                              int32_t fc, int32_t nc) {
+  for (int32_t j = __lane_id(); j < nc; j += 64) {
+    uint2 m;
+    float py;
+    child_rec(G, fc + j, m, py);
+    stamps[arc_class(m)] = tg;
+  }
+}
+
+// Best root move whose class is not marked (tag tg), from every lane's two
+// best root moves: a lane whose best is marked offers its runner-up. Returns
+// false when some lane's best two are both marked and its further moves could
+// still reach the result.
+template <int PER>
+__device__ __forceinline__ bool root_excluding(const Tables<PER>& tb, const float* zrow,
+                                               const uint8_t* stamps, uint8_t tg, LaneTop top,
+                                               float& rk, int32_t& rt) {
+  const bool h1 = top.i1 != kNoTok, h2 = top.i2 != kNoTok;
+  const int32_t i1 = h1 ? top.i1 : 0, i2 = h2 ? top.i2 : 0;
+  const int32_t c1 = tb.cls[i1], c2 = tb.cls[i2];
+  const float k1 = zrow[i1] + tb.rpsi[i1], k2 = zrow[i2] + tb.rpsi[i2];
+  const bool o1 = h1 && c1 != 0xffff && stamps[c1] == tg;
+  const bool o2 = h2 && c2 != 0xffff && stamps[c2] == tg;
+  const bool use1 = h1 && !o1, use2 = !use1 && h2 && !o2;
+  const float k = use1 ? k1 : (use2 ? k2 : kNegInf);
+  const int32_t t = use1 ? i1 : (use2 ? i2 : INT_MAX);
+  wave_argmax_dpp(k, t, rk, rt);
+  // A lane whose best two are both marked holds further moves with keys at
+  // most its runner-up's; they matter only if that key reaches the result
+  // (equal keys included: a lower index would win the tie).
+  return __ballot(o1 && o2 && !(k2 < rk)) == 0ull;
+}
+
+// Best root move whose class is not marked (tag tg), over the whole row
+// (unrolled over the row's chunks so that the table reads of several chunks
+// issue together).
+template <int PER>
+__device__ __forceinline__ void root_scan(const Tables<PER>& tb, const float* zrow,
+                                          const uint8_t* stamps, uint8_t tg,
+                                          const RowShape<PER>& rs, float& rk, int32_t& rt) {
+  const int lane = __lane_id();
+  float k2 = kNegInf;
+  int32_t t2 = INT_MAX;
+#pragma unroll 6
+  for (int j = 0; j < PER; ++j) {
+    const int32_t v = (j < PER - 1) ? 64 * j + lane : rs.last_idx;
+    const int32_t cv = tb.cls[v];
+    const bool ok_lane = (j < PER - 1) || rs.last_ok;
+    const float k = zrow[v] + tb.rpsi[v];  // -inf for the blank
+    const bool ov = cv != 0xffff && stamps[cv] == tg;
+    if (ok_lane && !ov && k > k2) { k2 = k; t2 = v; }
+  }
+  wave_argmax_dpp(k2, t2, rk, rt);
+}
+
+// The boosted step from state x on the row in zrow (LDS), given the row's
+// summary. All lanes take part; the result is uniform.
+//
+// The children of the states on x's suffix chain override the root move of
+// their class, deeper states first; every other token takes its root move
+// (the row's best of those is r.r1 unless its class is overridden); the blank
+// keeps the state. Class marks are needed only when the chain has more than
+// one state (to let deeper states win) or when r.r1's class is overridden.
+template <int PER>
+__device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>& tb,
+                                               const float* zrow, uint8_t* stamps, uint32_t& tag,
+                                               const RowShape<PER>& rs, int32_t x, const RowSum& r,
+                                               const LaneTop* top, int32_t V) {
+  const int lane = __lane_id();
+  int32_t fc, nc, lnk;
+  float phi_x;
+  G.rec(x, fc, nc, lnk, phi_x);
+  const int32_t fc0 = fc, nc0 = nc;
+  const bool multi = lnk != 0;
+  uint8_t tg = 0;
+  if (multi) tg = next_tag<PER>(stamps, tag);
+
+  Cand c;
+  c.k = kNegInf;
+  c.tok = INT_MAX;
+  c.z = 0.f;
+  c.psi = 0.f;
+  c.ns = 0;
+  bool over = false;
+  for (int32_t lvl = 0; x != 0; ++lvl) {
+    if (fc + nc <= G.nhot || nc > kScalarKids) {
+      // one child per lane
       for (int32_t j0 = 0; j0 < nc; j0 += 64) {
         const int32_t j = j0 + lane;
         if (j < nc) {
           const int32_t y = fc + j;
-          const int32_t lab = G.hs_label[y];
-          if (stamps[lab] != tg) {
-            stamps[lab] = tg;
-            const float py = G.hs_psi[y];
-            const int32_t m0 = tb.cls_ptr[lab], m1 = tb.cls_ptr[lab + 1];
-            for (int32_t q = m0; q < m1; ++q) {
-              const int32_t tok = tb.cls_tok[q];
-              const float k = zrow[tok] + py;
-              if (better(k, tok, lk, lt)) { lk = k; lt = tok; lns = y; lpsi = py; }
-            }
+          uint2 m;
+          float py;
+          child_rec(G, y, m, py);
+          const int32_t lab = arc_class(m);
+          bool take = true;
+          if (multi) {
+            take = lvl == 0 || stamps[lab] != tg;
+            if (take) stamps[lab] = tg;
           }
-        }
-      }
-    } else if (nc <= kScalarKids) {
-      // a few children in the arena: one child at a time by scalar loads, the
-      // members of its class across the lanes
-      for (int32_t j = 0; j < nc; ++j) {
-        const int32_t y = fc + j;
-        const int32_t lab = sload(G.A->label + G.off + y);
-        const float py = sload(G.A->psi + G.off + y);
-        if (stamps[lab] != tg) {  // uniform
-          stamps[lab] = tg;
-          const int32_t q = tb.cls_ptr[lab] + lane;
-          if (q < tb.cls_ptr[lab + 1]) {
-            const int32_t tok = tb.cls_tok[q];
-            const float k = zrow[tok] + py;
-            if (better(k, tok, lk, lt)) { lk = k; lt = tok; lns = y; lpsi = py; }
+          if (take) {
+            over |= lab == r.r1_cls;
+            offer_members<PER>(c, tb, zrow, m, y, py);
           }
         }
       }
     } else {
-      // many children in the arena: one child per lane
-      for (int32_t j0 = 0; j0 < nc; j0 += 64) {
-        const int32_t j = j0 + lane;
-        if (j < nc) {
-          const int32_t y = fc + j;
-          const int32_t lab = G.A->label[G.off + y];
-          if (stamps[lab] != tg) {
-            stamps[lab] = tg;
-            const float py = G.A->psi[G.off + y];
-            const int32_t m0 = tb.cls_ptr[lab], m1 = tb.cls_ptr[lab + 1];
-            for (int32_t q = m0; q < m1; ++q) {
-              const int32_t tok = tb.cls_tok[q];
-              const float k = zrow[tok] + py;
-              if (better(k, tok, lk, lt)) { lk = k; lt = tok; lns = y; lpsi = py; }
-            }
+      // a few children in the arena: one child at a time by scalar loads,
+      // its members across the lanes
+      for (int32_t j = 0; j < nc; ++j) {
+        const int32_t y = fc + j;
+        const int64_t q = 2 * ((int64_t)G.off + y);
+        const uint2 m = make_uint2(sload(G.A->arc_mem + q), sload(G.A->arc_mem + q + 1));
+        const float py = sload(G.A->psi + G.off + y);
+        const int32_t lab = arc_class(m);
+        bool take = true;
+        if (multi) {
+          take = lvl == 0 || stamps[lab] != tg;  // uniform
+          if (take) stamps[lab] = tg;
+        }
+        if (take) {
+          over |= lab == r.r1_cls;
+          int32_t t = -1;
+          if (!arc_more(m)) {
+            if (lane < 3) t = (int32_t)(lane == 0 ? (m.x & 0xffffu) : lane == 1 ? (m.x >> 16) : (m.y & 0xffffu));
+          } else {
+            const int32_t qq = tb.cls_ptr[lab] + lane;
+            if (qq < tb.cls_ptr[lab + 1]) t = tb.cls_tok[qq];
+          }
+          if (t >= 0) {
+            const float z = zrow[t];
+            c.offer(z + py, t, z, y, py);
           }
         }
       }
     }
-    c = lnk;
+    if (lnk == 0) break;
+    float phi_unused;
+    G.rec(lnk, fc, nc, lnk, phi_unused);
   }
   float ok;
   int32_t ot;
-  const int32_t wl = wave_argmax_dpp(lk, lt, ok, ot);
-  const int32_t o_ns = rl(lns, wl);
-  const float o_psi = rlf(lpsi, wl);
+  const int32_t wl = wave_argmax_dpp(c.k, c.tok, ok, ot);
+  const int32_t o_ns = rl(c.ns, wl);
+  const float o_psi = rlf(c.psi, wl);
+  const float o_z = rlf(c.z, wl);
 
-  // best root move whose class is not overridden (unrolled over the row's
-  // chunks so that the table reads of several chunks issue together)
-  float rk = r1_y;
-  int32_t rt = r1_tok, r_ns = r1_dst;
-  if (r1_cls >= 0 && stamps[r1_cls] == tg) {
-    float k2 = kNegInf;
-    int32_t t2 = INT_MAX;
-#pragma unroll 6
-    for (int j = 0; j < PER; ++j) {
-      const int32_t v = (j < PER - 1) ? 64 * j + lane : rs.last_idx;
-      const int32_t c = tb.cls[v];
-      const bool ok_lane = (j < PER - 1) || rs.last_ok;
-      const float k = zrow[v] + tb.rpsi[v];  // -inf for the blank
-      const bool over = c != 0xffff && stamps[c] == tg;
-      if (ok_lane && !over && k > k2) { k2 = k; t2 = v; }
+  // best root move whose class is not overridden
+  float rk = r.ymax;
+  int32_t rt = r.r1_tok, r_ns = r.r1_dst;
+  float r_psi = r.r1_psi, r_z = r.r1_z;
+  if (__ballot(over) != 0ull) {
+    if (!multi) {
+      tg = next_tag<PER>(stamps, tag);
+      mark_children(G, stamps, tg, fc0, nc0);
     }
-    wave_argmax_dpp(k2, t2, rk, rt);
-    r_ns = (rt < V) ? tb.rdst[rt] : 0;
+    if (!(top && root_excluding<PER>(tb, zrow, stamps, tg, *top, rk, rt)))
+      root_scan<PER>(tb, zrow, stamps, tg, rs, rk, rt);
+    const int32_t rv = (rt < V) ? rt : 0;
+    r_ns = tb.rdst[rv];
+    r_psi = tb.rpsi[rv];
+    r_z = zrow[rv];
   }
   Answer a;
   a.tok = V;
   a.ns = x;
   a.b = 0.f;
-  a.zv = zb;
-  float bk = zb + phi_x;  // blank keeps the state
+  a.zv = r.zb;
+  float bk = r.zb + phi_x;  // blank keeps the state
   int32_t bt = V;
   if (better(ok, ot, bk, bt)) {
     bk = ok;
@@ -330,30 +455,148 @@ __device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& 
     a.tok = ot;
     a.ns = o_ns;
     a.b = o_psi - phi_x;
+    a.zv = o_z;
   }
   if (better(rk, rt, bk, bt)) {
-    bk = rk;
-    bt = rt;
     a.tok = rt;
     a.ns = r_ns;
-    a.b = G.psi(r_ns) - phi_x;
+    a.b = r_psi - phi_x;
+    a.zv = r_z;
   }
-  if (a.tok != V) a.zv = zrow[a.tok];
   return a;
 }
 
-// State-independent part of a step on a row held in registers (raw[j] as
-// loaded): copies the row to zrow (LDS), and returns the blank logit, the best
-// root move (key and token) and, if asked, the normaliser. rp holds this
-// lane's root-move psi (-inf for blank and masked lanes).
-struct RowSum {
-  float zb, ymax, lse;
-  int32_t r1_tok;
-};
-
+// Straight-line evaluation for the common shapes: at most four states on x's
+// suffix chain, at most 64 children in all, classes of at most three members.
+// Lane j takes child j of the concatenated child lists, x's first; a class is
+// taken from the deepest chain state that has it. Records come from LDS for
+// hot states, else from the arena (scalar loads for the chain, one vector
+// load per child). Returns false, with no output, on any other shape.
 template <int PER>
-__device__ __forceinline__ RowSum row_summary(float* zrow, const float* raw, const float* rp,
-                                              const RowShape<PER>& rs, int32_t V, bool need_lse) {
+__device__ __forceinline__ bool eval_fast(const Graph& G, const Tables<PER>& tb,
+                                          const float* zrow, uint8_t* stamps, uint32_t& tag,
+                                          int32_t x, const RowSum& r, const LaneTop* top,
+                                          int32_t V, Answer& a) {
+  const int lane = __lane_id();
+  int32_t f0 = 0, f1 = 0, f2 = 0, f3 = 0, n0 = 0, n1 = 0, n2 = 0, n3 = 0, levels = 0;
+  float phi_x;
+  {
+    int32_t fc, nc, lnk;
+    G.rec(x, fc, nc, lnk, phi_x);
+    // chain states' child ranges (the root's children are the dense root row)
+    if (x != 0) {
+      f0 = fc;
+      n0 = nc;
+      levels = 1;
+      while (lnk != 0) {
+        if (levels == 4) return false;
+        float phi_unused;
+        G.rec(lnk, fc, nc, lnk, phi_unused);
+        if (levels == 1) { f1 = fc; n1 = nc; }
+        else if (levels == 2) { f2 = fc; n2 = nc; }
+        else { f3 = fc; n3 = nc; }
+        ++levels;
+      }
+    }
+  }
+  const int32_t s1 = n0, s2 = s1 + n1, s3 = s2 + n2, total = s3 + n3;
+  if (total > 64) return false;
+  const bool valid = lane < total;
+  const int32_t lv = (lane >= s1) + (lane >= s2) + (lane >= s3);
+  const int32_t fb = lv == 0 ? f0 : lv == 1 ? f1 : lv == 2 ? f2 : f3;
+  const int32_t sb = lv == 0 ? 0 : lv == 1 ? s1 : lv == 2 ? s2 : s3;
+  const int32_t y = valid ? fb + (lane - sb) : 0;
+  uint2 m;
+  float py;
+  child_rec(G, y, m, py);
+  if (__ballot(valid && arc_more(m)) != 0ull) return false;
+  const int32_t lab = arc_class(m);
+  bool take = valid;
+  uint8_t tg = 0;
+  const bool marked = levels > 1;
+  if (marked) {
+    // level by level, deepest first: a class already marked is shadowed
+    // (LDS runs a wave's accesses in order, so each level sees the marks of
+    // the levels before it)
+    tg = next_tag<PER>(stamps, tag);
+    for (int32_t l = 0; l < levels; ++l) {
+      if (valid && lv == l) {
+        if (l > 0) take = stamps[lab] != tg;
+        if (take) stamps[lab] = tg;
+      }
+    }
+  }
+  const int32_t t0 = (int32_t)(m.x & 0xffffu), t1 = (int32_t)(m.x >> 16);
+  const int32_t t2 = (int32_t)(m.y & 0xffffu);
+  const float z0 = zrow[t0], z1 = zrow[t1], z2 = zrow[t2];
+  float kb = z0 + py, zb_ = z0;
+  int32_t tk = t0;
+  const float k1 = z1 + py, k2 = z2 + py;
+  if (k1 > kb) { kb = k1; tk = t1; zb_ = z1; }  // members ascend: ties keep the lower
+  if (k2 > kb) { kb = k2; tk = t2; zb_ = z2; }
+  const bool over = take && lab == r.r1_cls;
+  float ok;
+  int32_t ot;
+  const int32_t wl = wave_argmax_dpp(take ? kb : kNegInf, take ? tk : INT_MAX, ok, ot);
+  const int32_t o_ns = rl(y, wl);
+  const float o_psi = rlf(py, wl);
+  const float o_z = rlf(zb_, wl);
+
+  float rk = r.ymax;
+  int32_t rt = r.r1_tok, r_ns = r.r1_dst;
+  float r_psi = r.r1_psi, r_z = r.r1_z;
+  if (__ballot(over) != 0ull) {
+    // mark every overriding class, then take the best unmarked root move
+    if (!marked) tg = next_tag<PER>(stamps, tag);
+    if (take) stamps[lab] = tg;
+    if (!(top && root_excluding<PER>(tb, zrow, stamps, tg, *top, rk, rt))) return false;
+    const int32_t rv = (rt < V) ? rt : 0;
+    r_ns = tb.rdst[rv];
+    r_psi = tb.rpsi[rv];
+    r_z = zrow[rv];
+  }
+  a.tok = V;
+  a.ns = x;
+  a.b = 0.f;
+  a.zv = r.zb;
+  float bk = r.zb + phi_x;  // blank keeps the state
+  int32_t bt = V;
+  if (better(ok, ot, bk, bt)) {
+    bk = ok;
+    bt = ot;
+    a.tok = ot;
+    a.ns = o_ns;
+    a.b = o_psi - phi_x;
+    a.zv = o_z;
+  }
+  if (better(rk, rt, bk, bt)) {
+    a.tok = rt;
+    a.ns = r_ns;
+    a.b = r_psi - phi_x;
+    a.zv = r_z;
+  }
+  return true;
+}
+
+// The boosted step from state x: the straight-line path when it applies, else
+// the general one.
+template <int PER>
+__device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& tb,
+                                             const float* zrow, uint8_t* stamps, uint32_t& tag,
+                                             const RowShape<PER>& rs, int32_t x, const RowSum& r,
+                                             const LaneTop* top, int32_t V) {
+  Answer a;
+  if (eval_fast<PER>(G, tb, zrow, stamps, tag, x, r, top, V, a)) return a;
+  return eval_general<PER>(G, tb, zrow, stamps, tag, rs, x, r, top, V);
+}
+
+// State-independent part of a step on a row held in registers (raw[j] as
+// loaded): copies the row to zrow (LDS) and summarises it. rp holds this
+// lane's root-move psi (-inf for blank and masked lanes).
+template <int PER, bool kTop2 = false>
+__device__ __forceinline__ RowSum row_summary(float* zrow, const Tables<PER>& tb, const float* raw,
+                                              const float* rp, const RowShape<PER>& rs, int32_t V,
+                                              bool need_lse, LaneTop* top = nullptr) {
   const int lane = __lane_id();
   float cur[PER];
 #pragma unroll
@@ -368,20 +611,34 @@ __device__ __forceinline__ RowSum row_summary(float* zrow, const float* raw, con
   asm volatile("" ::: "memory");
 
   // best root move per lane: strict > keeps the lowest chunk, hence the lowest index
-  float zmax = kNegInf, yb = kNegInf;
-  int32_t jb = 0;
+  float zmax = kNegInf, yb = kNegInf, y2 = kNegInf;
+  int32_t jb = 0, j2 = -1;
 #pragma unroll
   for (int j = 0; j < PER; ++j) {
     zmax = __builtin_fmaxf(zmax, cur[j]);
     const float yj = cur[j] + rp[j];
     const bool gt = yj > yb;
+    if (kTop2) {  // the runner-up, in the same (key, index) order
+      const bool gt2 = yj > y2;
+      y2 = gt ? yb : (gt2 ? yj : y2);
+      j2 = gt ? (yb > kNegInf ? jb : -1) : (gt2 ? j : j2);
+    }
     yb = gt ? yj : yb;
     jb = gt ? j : jb;
   }
   const int32_t idx = (jb == PER - 1) ? rs.last_idx : 64 * jb + lane;
+  if (kTop2) {
+    top->i1 = (yb > kNegInf) ? idx : kNoTok;
+    top->i2 = (j2 < 0 || !(y2 > kNegInf)) ? kNoTok : ((j2 == PER - 1) ? rs.last_idx : 64 * j2 + lane);
+  }
   zmax = wave_max_dpp(zmax);
   wave_argmax_dpp(yb, idx, r.ymax, r.r1_tok);
   if (r.r1_tok >= V) r.r1_tok = 0;  // only with -inf / nan logits: keep indices in range
+  const int32_t c16 = tb.cls[r.r1_tok];
+  r.r1_cls = c16 == 0xffff ? -1 : c16;
+  r.r1_dst = tb.rdst[r.r1_tok];
+  r.r1_psi = tb.rpsi[r.r1_tok];
+  r.r1_z = zrow[r.r1_tok];
   r.lse = 0.f;
   if (need_lse) {  // warm-up rows only need the state
     const float mL = zmax * kLog2e;
@@ -399,9 +656,9 @@ template <int PER>
 __device__ __forceinline__ Answer step_from(const Graph& G, const Tables<PER>& tb,
                                             const float* zrow, uint8_t* stamps, uint32_t& tag,
                                             const RowShape<PER>& rs, const RowSum& r, int32_t s,
-                                            int mode, int32_t V) {
-  Answer a;
+                                            int mode, int32_t V, const LaneTop* top = nullptr) {
   if (mode != 1) {
+    Answer a;
     const bool blank = !better(r.ymax, r.r1_tok, r.zb, V);
     a.tok = blank ? V : r.r1_tok;
     a.ns = s;
@@ -409,9 +666,7 @@ __device__ __forceinline__ Answer step_from(const Graph& G, const Tables<PER>& t
     a.zv = blank ? r.zb : r.ymax;
     return a;
   }
-  const int32_t c16 = tb.cls[r.r1_tok];
-  return eval_state<PER>(G, tb, zrow, stamps, tag, rs, s, r.zb, r.ymax, r.r1_tok,
-                         tb.rdst[r.r1_tok], c16 == 0xffff ? -1 : c16, V);
+  return eval_state<PER>(G, tb, zrow, stamps, tag, rs, s, r, top, V);
 }
 
 // One complete step on a row held in registers.
@@ -420,7 +675,7 @@ __device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& t
                                             uint8_t* stamps, uint32_t& tag, const float* raw,
                                             const float* rp, const RowShape<PER>& rs, int32_t s,
                                             int mode, int32_t V, bool need_lse, float& lse) {
-  const RowSum r = row_summary<PER>(zrow, raw, rp, rs, V, need_lse);
+  const RowSum r = row_summary<PER>(zrow, tb, raw, rp, rs, V, need_lse);
   lse = r.lse;
   return step_from<PER>(G, tb, zrow, stamps, tag, rs, r, s, mode, V);
 }
@@ -778,13 +1033,10 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   if (w < T) {
     float rp[PER];
     root_psi_regs<PER>(rp, S.tab, rs);
-    const RowSum r = row_summary<PER>(S.zbuf[w], raw, rp, rs, V, true);
-    if (lane == 0) {
-      S.rsum[w][0] = r.zb;
-      S.rsum[w][1] = r.ymax;
-      S.rsum[w][2] = r.lse;
-      S.rsum[w][3] = __int_as_float(r.r1_tok);
-    }
+    LaneTop top;
+    const RowSum r = row_summary<PER, true>(S.zbuf[w], S.tab, raw, rp, rs, V, true, &top);
+    if (lane == 0) S.rsum[w] = r;
+    S.rtop[w][lane] = (uint32_t)top.i1 | ((uint32_t)top.i2 << 16);
   }
   __syncthreads();
   if (w != 0) return;
@@ -794,13 +1046,18 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   int32_t s = (mode == 1) ? s0 : ((mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID);
   int32_t o_tok = 0, o_st = 0;
   float o_sc = 0.f;
+  RowSum rn = S.rsum[0];
+  uint32_t tpn = S.rtop[0][lane];
   for (int32_t t = 0; t < T; ++t) {
-    RowSum r;
-    r.zb = S.rsum[t][0];
-    r.ymax = S.rsum[t][1];
-    r.lse = S.rsum[t][2];
-    r.r1_tok = __float_as_int(S.rsum[t][3]);
-    const Answer a = step_from<PER>(Gr, S.tab, S.zbuf[t], S.stamps[0], tag, rs, r, s, mode, V);
+    const RowSum r = rn;
+    const uint32_t tp = tpn;
+    if (t + 1 < T) {  // the next row's summary is read while this step runs
+      rn = S.rsum[t + 1];
+      tpn = S.rtop[t + 1][lane];
+    }
+    const LaneTop top = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16)};
+    const Answer a =
+        step_from<PER>(Gr, S.tab, S.zbuf[t], S.stamps[0], tag, rs, r, s, mode, V, &top);
     const bool mine = lane == t;
     o_tok = mine ? a.tok : o_tok;
     o_st = mine ? a.ns : o_st;

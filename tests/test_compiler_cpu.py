@@ -153,6 +153,8 @@ def test_validate_rejects_corrupt_images():
     corrupt(L.off_root_dst + 4 * 7, 1 if rd7 != 1 else 2)
     corrupt(L.off_root_psi + 4 * 7, int(np.float32(123.0).view(np.int32)))
     corrupt(L.off_root_psi + 4 * cfg.V, int(np.float32(1.0).view(np.int32)))  # blank column
+    # arc member records must agree with the labels
+    corrupt(L.off_arc_mem + 8 * 3, 0)
     # class member lists must list each classed token under its own class
     ct0 = int(np.frombuffer(good, dtype=np.int32, count=1, offset=L.off_cls_tok)[0])
     other = int(np.nonzero(cm[:cfg.V] != cm[ct0])[0][0])
@@ -219,3 +221,35 @@ def test_step_calls_reject_bad_arguments_before_launch():
     assert L.tb_init_states(C.byref(ar), 0, 1, buf, buf, None, None) == capi.TB_EINVAL
     bad = capi.tb_arena()
     assert L.tb_init_states(C.byref(bad), 1, 1, buf, buf, None, None) == capi.TB_EINVAL
+
+
+def test_arc_member_records_list_the_arc_class_members():
+    """arc_mem of every state = its arc class and the first three members of
+    that class (ascending, the last repeated), recomputed from the class map."""
+    cfg = W.config_by_name("batched")
+    cm = W.class_map(cfg)
+    mp, tp, tk = W.phrase_csr(W.phrases(cfg, [0, 1, 2]))
+    g = capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm)
+    a = capi.image_arrays(g.host_image(), g.layout)
+    am = a["arc_mem"].reshape(-1, 2)
+    members = {}
+    for v in range(cfg.V):
+        members.setdefault(int(cm[v]), []).append(v)
+    for y, lab in enumerate(a["label"]):
+        if lab < 0:
+            assert am[y, 0] == 0 and am[y, 1] == 0
+            continue
+        mem = members[int(lab)]
+        m0, m1, m2 = mem[0], mem[min(1, len(mem) - 1)], mem[min(2, len(mem) - 1)]
+        assert am[y, 0] == (m0 | (m1 << 16)), y
+        assert am[y, 1] == (m2 | (int(lab) << 16) | ((1 << 31) if len(mem) > 3 else 0)), y
+
+
+def test_compile_rejects_vocabularies_beyond_the_arc_records():
+    V1 = 32769
+    cm = np.arange(V1, dtype=np.int32)
+    cm[-1] = -1
+    with pytest.raises(capi.TbError) as e:
+        capi.tb_compile_graphs(np.array([0, 1], np.int64), np.array([0, 1], np.int64),
+                               np.array([5], np.int32), 1.0, 2.0, cm)
+    assert e.value.code == capi.TB_ERANGE
