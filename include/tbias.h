@@ -93,6 +93,8 @@ typedef struct {
   int64_t off_arc_mem;
   int32_t max_children;  /* largest out-degree of any state */
   int32_t max_depth;     /* deepest state (phrase length) */
+  int32_t max_override;  /* most tokens any state overrides: the members of the
+                            classes of the children along its suffix chain */
 } tb_arena_layout;
 
 /* A device-resident arena: the layout plus the device address of the image. */

@@ -39,6 +39,7 @@ class tb_arena_layout(C.Structure):
         ("off_arc_mem", C.c_int64),
         ("max_children", C.c_int32),
         ("max_depth", C.c_int32),
+        ("max_override", C.c_int32),
     ]
 
 

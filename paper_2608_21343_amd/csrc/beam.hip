@@ -10,6 +10,10 @@
 // graph states (Sec. II-C: scores and states carried across calls).
 #include <climits>
 
+#include <cstdlib>
+#include <cstring>
+
+#include "beam_fast.hpp"
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -272,10 +276,26 @@ void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int3
 
 }  // namespace
 
+// The one-wave-per-hypothesis kernel serves K <= 8, V+1 <= 2048 and arenas
+// whose override sets fit its lists; TBIAS_BEAM_KERNEL=ref selects the
+// reference kernel (used to test both paths).
 hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, int32_t T, int32_t B,
                        int32_t K, int64_t row_stride, const int32_t* model_ids, int32_t* states,
                        float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
                        float* out_step, float* out_cum, hipStream_t st) {
+  const char* e = std::getenv("TBIAS_BEAM_KERNEL");
+  const bool ref = e && std::strcmp(e, "ref") == 0;
+  if (!ref && K <= 8 && A.V1 >= 2 && A.V1 <= 64 * 32 && A.max_override <= beamk::kOverCap) {
+    const int per = (A.V1 + 63) / 64;
+    const int maxk = K <= 2 ? 2 : (K <= 4 ? 4 : 8);
+    beamk::BeamLaunch f = per <= 8    ? beamk::beam_launcher_1_8(per, maxk, dtype)
+                          : per <= 16 ? beamk::beam_launcher_9_16(per, maxk, dtype)
+                          : per <= 24 ? beamk::beam_launcher_17_24(per, maxk, dtype)
+                                      : beamk::beam_launcher_25_32(per, maxk, dtype);
+    if (f)
+      return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
+               out_state, out_step, out_cum, st);
+  }
   if (dtype == TB_F32)
     launch_k<LoadF32>(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok,
                       out_parent, out_state, out_step, out_cum, st);

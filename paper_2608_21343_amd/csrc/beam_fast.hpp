@@ -1,0 +1,495 @@
+// Boosted beam step for V+1 <= 64*PER: one workgroup per stream, one wave per
+// hypothesis (templates; instantiated per chunk count in beam_fast_*.hip).
+//
+// Per step, wave k takes hypothesis k and its own logit row [t, b, k] (the
+// row of a slot does not depend on the selection, so the next step's row is
+// prefetched while this one is scored):
+//
+//  * the row's normaliser: max in float32, sum of exponentials and log in
+//    float64, rounded once to float32 (beam scores are carried and compared,
+//    so they follow the exact reading);
+//  * c_k = (S_k - lse_k) - phi(s_k), and the candidates c_k + key over the row:
+//    root moves z + psi(root move) from registers (tokens whose class is
+//    overridden in s_k excluded through a class-mark table), the override
+//    members of the classes of the children along s_k's suffix chain (deepest
+//    state first) listed in LDS, and the blank c_k + z[V] + phi(s_k);
+//  * the K best of all K*(V+1) candidates (larger first, ties to the lower
+//    flat index k*(V+1)+v): every wave's K-th largest lane maximum bounds the
+//    K-th best from below; the largest bound theta is taken, every candidate
+//    >= theta is compacted into LDS and one wave selects the K best exactly.
+//    When too many candidates tie at theta, K rounds of a workgroup argmax
+//    select them instead;
+//  * slot j takes the j-th best: its parent, token, advanced state (blank
+//    keeps it), step score (z - lse) + boost and cumulative score.
+#pragma once
+
+#include <climits>
+
+#include "device.hpp"
+#include "greedy_seg.hpp"
+
+namespace tbias {
+namespace beamk {
+
+using seg::HotRecords;
+using seg::kNegInf;
+using seg::RowShape;
+using seg::Tables;
+
+constexpr int kOverCap = 256;  // override members listed per hypothesis
+constexpr int kCandCap = 128;  // candidates compacted for the final selection
+
+template <int PER, int MAXK>
+struct alignas(16) BeamFixed {
+  Tables<PER> tab;
+  float zbuf[MAXK][64 * PER];  // row of every hypothesis
+  uint8_t stamps[MAXK][64 * PER];
+  float ov_val[MAXK][kOverCap];  // override candidates of hypothesis k
+  int32_t ov_tok[MAXK][kOverCap];
+  int32_t ov_dst[MAXK][kOverCap];
+  float cand_val[kCandCap];
+  int32_t cand_f[kCandCap];
+  int32_t cand_dst[kCandCap];
+  int32_t hyp_s[2][MAXK];  // states and scores of the hypotheses, double buffered
+  float hyp_S[2][MAXK];
+  float hyp_lse[MAXK];
+  float hyp_phi[MAXK];
+  float theta_w[MAXK];
+  int32_t cnt_w[MAXK];
+  float sel_val[MAXK];
+  int32_t sel_f[MAXK];
+  int32_t sel_dst[MAXK];
+  float red_val[MAXK];
+  int32_t red_f[MAXK];
+  int32_t red_dst[MAXK];
+  int32_t bad;
+};
+
+template <int PER, int MAXK>
+constexpr int beam_hot() {
+  const int budget = 160 * 1024 - 1024;
+  const int room = (budget - (int)sizeof(BeamFixed<PER, MAXK>)) / seg::kHotRecordBytes;
+  const int h = (room / 64) * 64;
+  return h > 4096 ? 4096 : (h < 0 ? 0 : h);
+}
+
+template <int PER, int MAXK>
+struct alignas(16) BeamLds : BeamFixed<PER, MAXK> {
+  static constexpr int HOT = beam_hot<PER, MAXK>() > 64 ? beam_hot<PER, MAXK>() : 64;
+  HotRecords<HOT> hot;
+};
+
+// Exclusive prefix sum over the lanes of a wave (lane i gets sum of lanes < i)
+// and the wave total.
+__device__ __forceinline__ int32_t wave_excl_scan(int32_t v, int32_t& total) {
+  const int lane = __lane_id();
+  int32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  total = __builtin_amdgcn_readlane(x, 63);
+  return x - v;
+}
+
+// (value, flat index) order of the selection: larger value, then lower index.
+__device__ __forceinline__ bool cbetter(float a, int32_t fa, float b, int32_t fb) {
+  return a > b || (a == b && fa < fb);
+}
+
+template <class Ld, int PER, int MAXK>
+__global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
+    ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int32_t K,
+    int64_t stride, const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
+    float* __restrict__ scores, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_parent,
+    int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum) {
+  constexpr int HOT = BeamLds<PER, MAXK>::HOT;
+  __shared__ BeamLds<PER, MAXK> S;
+  const int32_t V1 = A.V1, V = V1 - 1;
+  const int nt = (int)blockDim.x;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // hypothesis / slot
+  const int lane = __lane_id();
+  const int32_t b = blockIdx.x;
+  const int64_t tstride = (int64_t)B * K * stride;  // row (t, b, w) = base + t * tstride
+  const typename Ld::T* base = logits + ((int64_t)b * K + w) * stride;
+
+  const int32_t m = model_ids[b];
+  int mode = (m == -1) ? 0 : ((m < -1 || m >= A.n_models) ? -1 : 1);
+  int32_t off = 0, n = 0;
+  if (mode == 1) {
+    off = A.model_off[m];
+    n = A.model_n[m];
+  }
+  if (threadIdx.x == 0) S.bad = 0;
+  __syncthreads();
+  if (threadIdx.x < K) {
+    const int32_t s = states[(int64_t)b * K + threadIdx.x];
+    S.hyp_s[0][threadIdx.x] = s;
+    S.hyp_S[0][threadIdx.x] = scores[(int64_t)b * K + threadIdx.x];
+    if (mode == 1 && (s < 0 || s >= n)) S.bad = 1;
+  }
+  const RowShape<PER> rs(V1);
+  float cur[PER], nxt[PER];
+  if (T > 0) seg::load_row<Ld, PER>(cur, base, rs);
+
+  // tables: root row, class map and members; hot records; marks
+  {
+    const int32_t mm = (mode == 1) ? m : 0;
+    const float* gpsi = A.root_psi + (int64_t)mm * V1;
+    const int32_t* gdst = A.root_dst + (int64_t)mm * V1;
+    for (int32_t i = threadIdx.x; i < 64 * PER; i += nt) {
+      S.tab.rpsi[i] = (i < V) ? (mode == 1 ? gpsi[i] : 0.f) : kNegInf;
+      S.tab.rdst[i] = (i < V && mode == 1) ? gdst[i] : 0;
+      const int32_t c = (i < V1) ? A.class_map[i] : -1;
+      S.tab.cls[i] = c < 0 ? (uint16_t)0xffff : (uint16_t)c;
+      S.tab.cls_ptr[i] = (i < V1) ? (uint16_t)A.cls_ptr[i] : (uint16_t)0;
+      S.tab.cls_tok[i] = (i < V) ? (uint16_t)A.cls_tok[i] : (uint16_t)0;
+    }
+    const int32_t nhot0 = (mode == 1) ? (n < HOT ? n : HOT) : 0;
+    for (int32_t i = threadIdx.x; i < nhot0; i += nt) {
+      int4 r;
+      r.x = A.first_child[off + i];
+      r.y = (int32_t)((uint32_t)A.link[off + i] | ((uint32_t)A.n_child[off + i] << 16));
+      r.z = __float_as_int(A.phi[off + i]);
+      r.w = __float_as_int(A.psi[off + i]);
+      S.hot.rec[i] = r;
+      const int64_t q = 2 * ((int64_t)off + i);
+      S.hot.mem[i] = make_uint2(A.arc_mem[q], A.arc_mem[q + 1]);
+    }
+    for (int32_t i = threadIdx.x; i < MAXK * 16 * PER; i += nt)
+      reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
+  }
+  __syncthreads();
+  if (mode == 1 && S.bad) mode = -1;  // uniform: every thread read the same flag
+  const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
+  const seg::Graph G(A, off, nhot, S.hot);
+  float* zrow = S.zbuf[w];
+  uint8_t* stamps = S.stamps[w];
+  uint32_t tag = 0;
+  float rp[PER];
+  uint32_t clsr[PER];  // class of every element of this lane (0xffff: none)
+#pragma unroll
+  for (int j = 0; j < PER - 1; ++j) {
+    rp[j] = S.tab.rpsi[64 * j + lane];
+    clsr[j] = S.tab.cls[64 * j + lane];
+  }
+  rp[PER - 1] = rs.last_ok ? S.tab.rpsi[rs.last_idx] : kNegInf;
+  clsr[PER - 1] = S.tab.cls[rs.last_idx];
+
+  for (int32_t t = 0; t < T; ++t) {
+    const int par = t & 1;
+    {  // prefetch this slot's next row (the last row is read again at the end)
+      const int32_t tn = (t + 1 < T) ? t + 1 : t;
+      seg::load_row<Ld, PER>(nxt, base + (int64_t)tn * tstride, rs);
+    }
+    const int32_t s_k = __builtin_amdgcn_readfirstlane(S.hyp_s[par][w]);
+    const float S_k = S.hyp_S[par][w];
+
+    // ---- row: copy to LDS, normaliser in float64
+#pragma unroll
+    for (int j = 0; j < PER - 1; ++j) zrow[64 * j + lane] = cur[j];
+    zrow[rs.last_idx] = cur[PER - 1];
+    const float zb = seg::rlf(cur[PER - 1], PER > 1 ? 63 : V);
+    float zmax = kNegInf;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const float zj = (j < PER - 1 || rs.last_ok) ? cur[j] : kNegInf;
+      zmax = __builtin_fmaxf(zmax, zj);
+    }
+    zmax = wave_max_dpp(zmax);
+    double se = 0.0;
+    const double zmd = (double)zmax;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const bool ok = (j < PER - 1) || rs.last_ok;
+      se += ok ? exp((double)cur[j] - zmd) : 0.0;
+    }
+    se = wave_sum_d(se);
+    const float lse = (float)(zmd + log(se));
+    const float phi_s = (mode == 1) ? G.phi_of(s_k) : 0.f;
+    const float c = (S_k - lse) - phi_s;
+    if (lane == 0) {
+      S.hyp_lse[w] = lse;
+      S.hyp_phi[w] = phi_s;
+    }
+
+    // ---- override members of s_k (classes of the children along its suffix
+    // chain, deepest state first), listed in LDS, their classes marked
+    int32_t n_ov = 0;
+    uint8_t tg = 0;
+    if (mode == 1 && s_k != 0) {
+      tg = seg::next_tag<PER>(stamps, tag);
+      int32_t fc, nc, lnk;
+      float phi_unused;
+      G.rec(s_k, fc, nc, lnk, phi_unused);
+      for (int32_t lvl = 0;; ++lvl) {
+        for (int32_t j0 = 0; j0 < nc; j0 += 64) {
+          const int32_t j = j0 + lane;
+          int32_t y = fc, lab = 0, nm = 0, q0 = 0;
+          uint2 mem = make_uint2(0u, 0u);
+          float py = 0.f;
+          bool take = false;
+          if (j < nc) {
+            y = fc + j;
+            seg::child_rec(G, y, mem, py);
+            lab = seg::arc_class(mem);
+            take = lvl == 0 || stamps[lab] != tg;
+            if (take) {
+              stamps[lab] = tg;
+              if (!seg::arc_more(mem)) {
+                const uint32_t t0 = mem.x & 0xffffu, t1 = mem.x >> 16, t2 = mem.y & 0xffffu;
+                nm = (t1 == t0) ? 1 : ((t2 == t1) ? 2 : 3);
+              } else {
+                q0 = S.tab.cls_ptr[lab];
+                nm = S.tab.cls_ptr[lab + 1] - q0;
+              }
+            }
+          }
+          int32_t tot;
+          const int32_t pos = n_ov + wave_excl_scan(nm, tot);
+          for (int32_t i = 0; i < nm; ++i) {
+            int32_t tok;
+            if (!seg::arc_more(mem)) {
+              tok = (int32_t)(i == 0 ? (mem.x & 0xffffu) : i == 1 ? (mem.x >> 16) : (mem.y & 0xffffu));
+            } else {
+              tok = S.tab.cls_tok[q0 + i];
+            }
+            if (pos + i < kOverCap) {
+              S.ov_val[w][pos + i] = c + (zrow[tok] + py);
+              S.ov_tok[w][pos + i] = tok;
+              S.ov_dst[w][pos + i] = y;
+            }
+          }
+          n_ov += tot;
+        }
+        if (lnk == 0) break;
+        G.rec(lnk, fc, nc, lnk, phi_unused);
+      }
+    }
+    // the launcher checks that the arena's largest override set fits the list
+    n_ov = n_ov < kOverCap ? n_ov : kOverCap;
+    uint32_t xm = 0u;  // bit j: this lane's element of chunk j is overridden
+    if (n_ov > 0) {
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        xm |= (clsr[j] != 0xffffu && stamps[clsr[j]] == tg) ? (1u << j) : 0u;
+    }
+
+    // ---- candidates of this lane: dense root moves (unless overridden), the
+    // lane's override entries and (lane 0) the blank
+    const float cb = c + (zb + phi_s);
+    const int32_t fbase = w * V1;
+    auto dense_val = [&](int j) -> float {
+      const bool okl = (j < PER - 1) || rs.last_ok;
+      const float v = c + (cur[j] + rp[j]);  // -inf for the blank and masked lanes
+      return (okl && !((xm >> j) & 1u)) ? v : kNegInf;
+    };
+    auto dense_f = [&](int j) -> int32_t {
+      return fbase + ((j < PER - 1) ? 64 * j + lane : rs.last_idx);
+    };
+    float head = (lane == 0) ? cb : kNegInf;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) head = __builtin_fmaxf(head, dense_val(j));
+    for (int32_t i = lane; i < n_ov; i += 64) head = __builtin_fmaxf(head, S.ov_val[w][i]);
+
+    // this wave's K-th largest lane maximum (a lower bound of the K-th best)
+    float th = kNegInf;
+    {
+      float h = head;
+      int32_t rem = K;
+      for (int r = 0; r < MAXK; ++r) {
+        const float mx = wave_max_dpp(h);
+        if (!(mx > kNegInf)) break;
+        const int32_t cnt = __builtin_popcountll(__ballot(h == mx));
+        if (cnt >= rem) { th = mx; break; }
+        rem -= cnt;
+        h = (h == mx) ? kNegInf : h;
+      }
+    }
+    if (lane == 0) S.theta_w[w] = th;
+    __syncthreads();
+    float theta = kNegInf;
+    for (int k = 0; k < K; ++k) theta = __builtin_fmaxf(theta, S.theta_w[k]);
+
+    // count and compact every candidate >= theta
+    int32_t mine = 0;
+    if (theta > kNegInf) {
+      mine = (lane == 0 && cb >= theta) ? 1 : 0;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) mine += dense_val(j) >= theta;
+      for (int32_t i = lane; i < n_ov; i += 64) mine += S.ov_val[w][i] >= theta;
+    }
+    int32_t wtot;
+    const int32_t wpre = wave_excl_scan(mine, wtot);
+    if (lane == 0) S.cnt_w[w] = wtot;
+    __syncthreads();
+    int32_t total = 0, woff = 0;
+    for (int k = 0; k < K; ++k) {
+      const int32_t ck = S.cnt_w[k];
+      woff += (k < w) ? ck : 0;
+      total += ck;
+    }
+    const bool fast = theta > kNegInf && total <= kCandCap;
+    if (fast) {
+      int32_t p = woff + wpre;
+      if (lane == 0 && cb >= theta) {
+        S.cand_val[p] = cb;
+        S.cand_f[p] = fbase + V;
+        S.cand_dst[p] = -1;
+        ++p;
+      }
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const float v = dense_val(j);
+        if (v >= theta) {
+          S.cand_val[p] = v;
+          S.cand_f[p] = dense_f(j);
+          S.cand_dst[p] = -1;
+          ++p;
+        }
+      }
+      for (int32_t i = lane; i < n_ov; i += 64) {
+        const float v = S.ov_val[w][i];
+        if (v >= theta) {
+          S.cand_val[p] = v;
+          S.cand_f[p] = fbase + S.ov_tok[w][i];
+          S.cand_dst[p] = S.ov_dst[w][i];
+          ++p;
+        }
+      }
+      __syncthreads();
+      if (w == 0) {  // exact K best of the compacted candidates
+        float v0 = kNegInf, v1 = kNegInf;
+        int32_t f0 = INT_MAX, f1 = INT_MAX, d0 = -1, d1 = -1;
+        if (lane < total) { v0 = S.cand_val[lane]; f0 = S.cand_f[lane]; d0 = S.cand_dst[lane]; }
+        if (lane + 64 < total) {
+          v1 = S.cand_val[lane + 64]; f1 = S.cand_f[lane + 64]; d1 = S.cand_dst[lane + 64];
+        }
+        for (int32_t j = 0; j < K; ++j) {
+          const bool first = cbetter(v0, f0, v1, f1);
+          float hv = first ? v0 : v1;
+          int32_t hf = first ? f0 : f1, hd = first ? d0 : d1;
+          float bv;
+          int32_t bf;
+          const int32_t wl = wave_argmax_dpp(hv, hf, bv, bf);
+          const int32_t bd = __builtin_amdgcn_readlane(hd, wl);
+          if (lane == wl) {  // the winner leaves its lane's list
+            if (first) { v0 = kNegInf; f0 = INT_MAX; } else { v1 = kNegInf; f1 = INT_MAX; }
+          }
+          if (lane == 0) {
+            S.sel_val[j] = bv;
+            S.sel_f[j] = bf;
+            S.sel_dst[j] = bd;
+          }
+        }
+      }
+    } else {
+      // K rounds of a workgroup argmax over every candidate not yet taken
+      for (int32_t j = 0; j < K; ++j) {
+        float bv = kNegInf;
+        int32_t bf = INT_MAX, bd = -1;
+        auto offer = [&](float v, int32_t f, int32_t d) {
+          for (int32_t q = 0; q < j; ++q)
+            if (S.sel_f[q] == f) return;
+          if (cbetter(v, f, bv, bf)) { bv = v; bf = f; bd = d; }
+        };
+        if (lane == 0) offer(cb, fbase + V, -1);
+#pragma unroll
+        for (int jj = 0; jj < PER; ++jj) offer(dense_val(jj), dense_f(jj), -1);
+        for (int32_t i = lane; i < n_ov; i += 64)
+          offer(S.ov_val[w][i], fbase + S.ov_tok[w][i], S.ov_dst[w][i]);
+        float wv;
+        int32_t wf;
+        const int32_t wl = wave_argmax_dpp(bv, bf, wv, wf);
+        const int32_t wd = __builtin_amdgcn_readlane(bd, wl);
+        if (lane == 0) {
+          S.red_val[w] = wv;
+          S.red_f[w] = wf;
+          S.red_dst[w] = wd;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          float gv = S.red_val[0];
+          int32_t gf = S.red_f[0], gd = S.red_dst[0];
+          for (int k = 1; k < K; ++k)
+            if (cbetter(S.red_val[k], S.red_f[k], gv, gf)) {
+              gv = S.red_val[k];
+              gf = S.red_f[k];
+              gd = S.red_dst[k];
+            }
+          S.sel_val[j] = gv;
+          S.sel_f[j] = gf;
+          S.sel_dst[j] = gd;
+        }
+        __syncthreads();
+      }
+    }
+    __syncthreads();
+
+    // ---- slot w takes the w-th best
+    {
+      int32_t f = __builtin_amdgcn_readfirstlane(S.sel_f[w]);
+      if (f < 0 || f >= K * V1) f = 0;  // only reachable with nan logits
+      const int32_t k = f / V1, v = f - k * V1;
+      const int32_t sp = S.hyp_s[par][k];
+      const float phi_k = S.hyp_phi[k];
+      int32_t ns;
+      float bst = 0.f;
+      if (mode == 1) {
+        if (v == V) {
+          ns = sp;
+        } else {
+          const int32_t d = __builtin_amdgcn_readfirstlane(S.sel_dst[w]);
+          ns = (d >= 0) ? d : S.tab.rdst[v];
+          bst = ((d >= 0) ? G.psi_of(ns) : S.tab.rpsi[v]) - phi_k;
+        }
+      } else {
+        ns = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+      }
+      const float z = S.zbuf[k][v];
+      const float val = S.sel_val[w];
+      if (lane == 0) {
+        const int64_t o = ((int64_t)t * B + b) * K + w;
+        out_tok[o] = v;
+        out_parent[o] = k;
+        out_state[o] = ns;
+        out_step[o] = (z - S.hyp_lse[k]) + bst;
+        out_cum[o] = val;
+        S.hyp_s[par ^ 1][w] = ns;
+        S.hyp_S[par ^ 1][w] = val;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < PER; ++j) cur[j] = nxt[j];
+  }
+  if (lane == 0 && T > 0) {
+    states[(int64_t)b * K + w] = S.hyp_s[T & 1][w];
+    scores[(int64_t)b * K + w] = S.hyp_S[T & 1][w];
+  }
+}
+
+template <class Ld, int PER, int MAXK>
+hipError_t launch_beam_fast_t(const ArenaView& A, const void* logits, int32_t T, int32_t B,
+                              int32_t K, int64_t stride, const int32_t* model_ids,
+                              int32_t* states, float* scores, int32_t* out_tok,
+                              int32_t* out_parent, int32_t* out_state, float* out_step,
+                              float* out_cum, hipStream_t st) {
+  static_assert(sizeof(BeamLds<PER, MAXK>) <= 160 * 1024, "LDS budget");
+  hipLaunchKernelGGL((beam_fast_kernel<Ld, PER, MAXK>), dim3(B), dim3(64 * K), 0, st, A,
+                     static_cast<const typename Ld::T*>(logits), T, B, K, stride, model_ids,
+                     states, scores, out_tok, out_parent, out_state, out_step, out_cum);
+  return hipGetLastError();
+}
+
+typedef hipError_t (*BeamLaunch)(const ArenaView&, const void*, int32_t, int32_t, int32_t,
+                                 int64_t, const int32_t*, int32_t*, float*, int32_t*, int32_t*,
+                                 int32_t*, float*, float*, hipStream_t);
+BeamLaunch beam_launcher_1_8(int per, int maxk, int32_t dtype);
+BeamLaunch beam_launcher_9_16(int per, int maxk, int32_t dtype);
+BeamLaunch beam_launcher_17_24(int per, int maxk, int32_t dtype);
+BeamLaunch beam_launcher_25_32(int per, int maxk, int32_t dtype);
+
+}  // namespace beamk
+}  // namespace tbias

@@ -341,6 +341,28 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   std::vector<int32_t> fillp(cp, cp + V);
   for (int32_t v = 0; v < V; ++v)
     if (class_map[v] >= 0) ct[fillp[class_map[v]]++] = v;
+  // largest override set: over all states, the member tokens of the classes
+  // of the children along the state's suffix chain (root excluded), each
+  // class counted once
+  {
+    std::vector<int32_t> seen(V, -1);
+    int32_t gen = 0;
+    int64_t s0m = 0;
+    for (int32_t m = 0; m < n_models; ++m) {
+      const ModelGraph& mg = graphs[m];
+      for (int32_t x = 1; x < mg.n; ++x, ++gen) {
+        int32_t members = 0;
+        for (int32_t c = x; c != 0; c = mg.link[c])
+          for (int32_t j = 0; j < mg.n_child[c]; ++j) {
+            const int32_t lab = mg.label[mg.first_child[c] + j];
+            if (seen[lab] == gen) continue;
+            seen[lab] = gen;
+            members += cp[lab + 1] - cp[lab];
+          }
+        L.max_override = std::max(L.max_override, members);
+      }
+    }
+  }
   // member tokens of the class on the arc into every state (see arc_mem in tbias.h)
   uint32_t* am = reinterpret_cast<uint32_t*>(img + L.off_arc_mem);
   for (int64_t y = 0; y < N; ++y) {

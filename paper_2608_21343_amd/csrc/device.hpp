@@ -26,7 +26,8 @@ struct ArenaView {
   const int32_t* cls_tok;
   const uint32_t* arc_mem;  // two words per state (see tb_arena_layout)
   int32_t n_models;
-  int32_t V1;  // V + 1
+  int32_t V1;            // V + 1
+  int32_t max_override;  // most tokens any state overrides
 };
 
 inline ArenaView make_view(const tb_arena& a) {
@@ -49,6 +50,7 @@ inline ArenaView make_view(const tb_arena& a) {
   v.arc_mem = reinterpret_cast<const uint32_t*>(b + L.off_arc_mem);
   v.n_models = L.n_models;
   v.V1 = L.v_plus_blank;
+  v.max_override = L.max_override;
   return v;
 }
 

@@ -173,6 +173,12 @@ struct Graph {
   __device__ __forceinline__ Graph(const ArenaView& a, int32_t o, int32_t nh,
                                    const HotRecords<HOT>& h)
       : A(&a), off(o), nhot(nh), hrec(h.rec), hmem(h.mem) {}
+  __device__ __forceinline__ float phi_of(int32_t x) const {
+    return x < nhot ? __int_as_float(hrec[x].z) : sload(A->phi + off + x);
+  }
+  __device__ __forceinline__ float psi_of(int32_t x) const {
+    return x < nhot ? __int_as_float(hrec[x].w) : sload(A->psi + off + x);
+  }
   // first child, child count, suffix link and phi of state x (uniform)
   __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
                                       float& phi) const {

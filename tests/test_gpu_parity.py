@@ -338,3 +338,57 @@ def test_chunk_loop_graph_replay_matches_eager():
         torch.cuda.synchronize()
         for a, b in zip((tok, sst, sc, states), ref):
             assert torch.equal(a, b), f"replay {rep} differs from the eager run"
+
+
+@pytest.mark.parametrize("kernel", ["fast", "ref"])
+@pytest.mark.parametrize("K,dtype", [(2, "f32"), (3, "bf16"), (8, "f32")])
+def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, monkeypatch):
+    """Both beam kernels against the oracle: ragged V+1 = 301, model -1, an
+    empty list and an out-of-range id (decoded unbiased, states -2)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    if kernel == "ref":
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", "ref")
+    cfg, lists, rows = _small_case(6, B=6, V=300, K=K, T=40, dtype=dtype)
+    lists = list(lists[:4]) + [[]]
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, -1, 4, 2, 99, 3], np.int32)
+    say(f"[beam-{kernel}] K={K} {dtype}")
+    gpu = gpu_beam(dec, to_device_logits(rows), mids, 40)
+    ok = [0, 1, 2, 3, 5]
+    graphs = oracle_graphs(cfg, lists, ok, mids)
+    st0, S0 = oracle.init_carry(np.where(mids == 99, -1, mids), K)
+    st0[mids == 99] = 0
+    ref = oracle.beam_decode(graphs, np.where(mids == 99, -1, mids), rows, st0, S0)
+    compare_beam(gpu, ref, ok, ATOL)
+    # the out-of-range stream: unbiased beam search (tokens, parents and
+    # accumulated scores of the oracle's model -1 run), states -2
+    for i in (0, 1, 4):
+        assert np.array_equal(gpu[i][:, 4], ref[i][:, 4]), i
+    assert np.all(gpu[2][:, 4] == -2)
+
+
+@pytest.mark.parametrize("kernel", ["fast", "ref"])
+def test_beam_inside_long_phrases(kernel, monkeypatch):
+    """Beam hypotheses deep inside 40-token phrases (chains of several suffix
+    states, override sets of dozens of classes)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    if kernel == "ref":
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", "ref")
+    V, B, T, K = 64, 4, 200, 4
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    phrase = list(range(1, 41))
+    lists = [[phrase, list(range(3, 20)), [5, 6, 7, 8]], [phrase, list(range(10, 50))],
+             [list(range(1, 11)), [2, 3], [4, 5, 6]], [phrase]]
+    base = _phrase_following_rows(np.random.default_rng(9), T, B, V, 40)
+    rng = np.random.default_rng(10)
+    rows = np.repeat(base[:, :, None, :], K, axis=2) + rng.normal(0, 0.3, (T, B, K, V + 1)).astype(np.float32)
+    rows = np.ascontiguousarray(rows.astype(np.float32))
+    mids = np.arange(B, dtype=np.int32)
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    say(f"[beam-{kernel}] long phrases")
+    gpu = gpu_beam(dec, to_device_logits(rows), mids, 64)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    st0, S0 = oracle.init_carry(mids, K)
+    ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+    compare_beam(gpu, ref, range(B), ATOL)
+    assert np.max(ref[2]) >= 20
