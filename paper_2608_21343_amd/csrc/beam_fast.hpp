@@ -37,7 +37,7 @@ using seg::RowShape;
 using seg::Tables;
 
 constexpr int kOverCap = 256;  // override members listed per hypothesis
-constexpr int kCandCap = 128;  // candidates compacted for the final selection
+constexpr int kCandCap = 128;  // candidates compacted for the final selection (multiple of 8)
 
 template <int PER, int MAXK>
 struct alignas(16) BeamFixed {
@@ -54,7 +54,7 @@ struct alignas(16) BeamFixed {
   float hyp_S[2][MAXK];
   float hyp_lse[MAXK];
   float hyp_phi[MAXK];
-  float theta_w[MAXK];
+  float theta_w[MAXK * MAXK];  // every wave's K largest lane maxima
   int32_t cnt_w[MAXK];
   float sel_val[MAXK];
   int32_t sel_f[MAXK];
@@ -79,18 +79,48 @@ struct alignas(16) BeamLds : BeamFixed<PER, MAXK> {
   HotRecords<HOT> hot;
 };
 
-// Exclusive prefix sum over the lanes of a wave (lane i gets sum of lanes < i)
-// and the wave total.
+// Exclusive prefix sum over the lanes of a wave (lane i gets the sum of lanes
+// < i) and the wave total: row shifts within rows of 16 lanes, then the gfx9
+// row broadcasts; every lane of the wave must be active.
 __device__ __forceinline__ int32_t wave_excl_scan(int32_t v, int32_t& total) {
-  const int lane = __lane_id();
   int32_t x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int32_t y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  x += dpp_i<0x111, 0xf>(0, x);  // row_shr:1
+  x += dpp_i<0x112, 0xf>(0, x);  // row_shr:2
+  x += dpp_i<0x114, 0xf>(0, x);  // row_shr:4
+  x += dpp_i<0x118, 0xf>(0, x);  // row_shr:8
+  x += dpp_i<0x142, 0xa>(0, x);  // row_bcast:15 into rows 1 and 3
+  x += dpp_i<0x143, 0xc>(0, x);  // row_bcast:31 into rows 2 and 3
   total = __builtin_amdgcn_readlane(x, 63);
   return x - v;
+}
+
+// e^x for x <= 0 in float64 (x = -inf and x < -745 give 0): e^x = 2^k e^r with
+// k = rint(x / ln 2) and r = x - k ln 2, ln 2 split in a high part with
+// trailing zero bits (k * ln2_hi is exact for |k| < 2^11) and a low part
+// (Cody and Waite's reduction); e^r is summed as its Taylor series to degree
+// 12, whose truncation error for |r| <= ln(2)/2 is below 2e-16 relative.
+__device__ __forceinline__ double exp_nonpos(double x) {
+  const double kInvLn2 = 1.4426950408889634074;
+  const double kLn2Hi = 6.93147180369123816490e-01;
+  const double kLn2Lo = 1.90821492927058770002e-10;
+  const bool tiny = !(x >= -745.0);
+  x = tiny ? -745.0 : x;  // keeps k finite; the result is selected below
+  const double k = __builtin_rint(x * kInvLn2);
+  const double r = __builtin_fma(-k, kLn2Lo, __builtin_fma(-k, kLn2Hi, x));
+  double p = 1.0 / 479001600.0;  // 1/12!
+  p = __builtin_fma(p, r, 1.0 / 39916800.0);
+  p = __builtin_fma(p, r, 1.0 / 3628800.0);
+  p = __builtin_fma(p, r, 1.0 / 362880.0);
+  p = __builtin_fma(p, r, 1.0 / 40320.0);
+  p = __builtin_fma(p, r, 1.0 / 5040.0);
+  p = __builtin_fma(p, r, 1.0 / 720.0);
+  p = __builtin_fma(p, r, 1.0 / 120.0);
+  p = __builtin_fma(p, r, 1.0 / 24.0);
+  p = __builtin_fma(p, r, 1.0 / 6.0);
+  p = __builtin_fma(p, r, 0.5);
+  p = __builtin_fma(p, r, 1.0);
+  p = __builtin_fma(p, r, 1.0);
+  return tiny ? 0.0 : __builtin_ldexp(p, (int)k);
 }
 
 // (value, flat index) order of the selection: larger value, then lower index.
@@ -203,7 +233,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
       const bool ok = (j < PER - 1) || rs.last_ok;
-      se += ok ? exp((double)cur[j] - zmd) : 0.0;
+      se += ok ? exp_nonpos((double)cur[j] - zmd) : 0.0;
     }
     se = wave_sum_d(se);
     const float lse = (float)(zmd + log(se));
@@ -293,24 +323,40 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     for (int j = 0; j < PER; ++j) head = __builtin_fmaxf(head, dense_val(j));
     for (int32_t i = lane; i < n_ov; i += 64) head = __builtin_fmaxf(head, S.ov_val[w][i]);
 
-    // this wave's K-th largest lane maximum (a lower bound of the K-th best)
-    float th = kNegInf;
+    // theta = the K-th largest of all lane maxima (a lower bound of the K-th
+    // best candidate): every wave lists its K largest lane maxima (values,
+    // with multiplicity), and the K-th largest of those lists is taken
     {
       float h = head;
+      int32_t got = 0;
+      for (int r = 0; r < MAXK && got < K; ++r) {
+        const float mx = wave_max_dpp(h);
+        const int32_t cnt = __builtin_popcountll(__ballot(h == mx));
+        // record min(cnt, K - got) copies of mx (-inf fills a short list)
+        if (lane >= got && lane < got + cnt && lane < K) S.theta_w[w * MAXK + lane] = mx;
+        got += cnt;
+        h = (h == mx) ? kNegInf : h;
+        if (!(mx > kNegInf)) {
+          if (lane >= got && lane < K) S.theta_w[w * MAXK + lane] = kNegInf;
+          got = K;
+        }
+      }
+    }
+    __syncthreads();
+    float theta;
+    {
+      float h = (lane < K * K) ? S.theta_w[(lane / K) * MAXK + (lane % K)] : kNegInf;
+      theta = kNegInf;
       int32_t rem = K;
       for (int r = 0; r < MAXK; ++r) {
         const float mx = wave_max_dpp(h);
         if (!(mx > kNegInf)) break;
         const int32_t cnt = __builtin_popcountll(__ballot(h == mx));
-        if (cnt >= rem) { th = mx; break; }
+        if (cnt >= rem) { theta = mx; break; }
         rem -= cnt;
         h = (h == mx) ? kNegInf : h;
       }
     }
-    if (lane == 0) S.theta_w[w] = th;
-    __syncthreads();
-    float theta = kNegInf;
-    for (int k = 0; k < K; ++k) theta = __builtin_fmaxf(theta, S.theta_w[k]);
 
     // count and compact every candidate >= theta
     int32_t mine = 0;
@@ -358,30 +404,29 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           ++p;
         }
       }
+      // pad the list to a multiple of 8 with entries that beat nothing
+      const int32_t total8 = (total + 7) & ~7;
+      if ((int32_t)threadIdx.x < total8 - total) {
+        S.cand_val[total + threadIdx.x] = kNegInf;
+        S.cand_f[total + threadIdx.x] = INT_MAX;
+      }
       __syncthreads();
-      if (w == 0) {  // exact K best of the compacted candidates
-        float v0 = kNegInf, v1 = kNegInf;
-        int32_t f0 = INT_MAX, f1 = INT_MAX, d0 = -1, d1 = -1;
-        if (lane < total) { v0 = S.cand_val[lane]; f0 = S.cand_f[lane]; d0 = S.cand_dst[lane]; }
-        if (lane + 64 < total) {
-          v1 = S.cand_val[lane + 64]; f1 = S.cand_f[lane + 64]; d1 = S.cand_dst[lane + 64];
+      // exact K best of the compacted candidates: the rank of a candidate is
+      // the number of candidates before it in (value, flat index) order, and
+      // flat indices are distinct, so ranks are distinct
+      for (int32_t i = threadIdx.x; i < total; i += nt) {
+        const float vi = S.cand_val[i];
+        const int32_t fi = S.cand_f[i];
+        int32_t rank = 0;
+        for (int32_t q0 = 0; q0 < total8; q0 += 8) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            rank += cbetter(S.cand_val[q0 + q], S.cand_f[q0 + q], vi, fi);
         }
-        for (int32_t j = 0; j < K; ++j) {
-          const bool first = cbetter(v0, f0, v1, f1);
-          float hv = first ? v0 : v1;
-          int32_t hf = first ? f0 : f1, hd = first ? d0 : d1;
-          float bv;
-          int32_t bf;
-          const int32_t wl = wave_argmax_dpp(hv, hf, bv, bf);
-          const int32_t bd = __builtin_amdgcn_readlane(hd, wl);
-          if (lane == wl) {  // the winner leaves its lane's list
-            if (first) { v0 = kNegInf; f0 = INT_MAX; } else { v1 = kNegInf; f1 = INT_MAX; }
-          }
-          if (lane == 0) {
-            S.sel_val[j] = bv;
-            S.sel_f[j] = bf;
-            S.sel_dst[j] = bd;
-          }
+        if (rank < K) {
+          S.sel_val[rank] = vi;
+          S.sel_f[rank] = fi;
+          S.sel_dst[rank] = S.cand_dst[i];
         }
       }
     } else {
