@@ -80,6 +80,20 @@ typedef struct tb_graphs tb_graphs;
  *                                 m2 | class << 16 | (more than three
  *                                 members ? 1 << 31 : 0); roots: 0, 0
  *                                 (token ids and classes below 2^15)
+ *   value_tab   float[n_models*512]  per model the distinct psi values
+ *                                 (entries 0..255, ascending) and the
+ *                                 distinct phi values (entries 256..511)
+ *   state_rec   uint32[3*n_states]  a packed record of every state x:
+ *                 word 0 = first_child & 0xffff | min(n_child, 255) << 16 |
+ *                          psi index << 24
+ *                 word 1 = link & 0xffff | cls_ptr[label] << 16 (the first
+ *                          member of the arc class in cls_tok; roots: 0)
+ *                 word 2 = class size (<= 255) | phi index << 8 |
+ *                          label << 16 (15 bits; roots: 0) | flag << 31
+ *               The flag is set when a field does not fit (first child, link
+ *               or class size >= 2^16 / 255, n_child >= 255, or more than
+ *               256 distinct psi or phi values in the model); the record is
+ *               then not used and the plain arrays above are read instead.
  */
 typedef struct {
   int64_t total_bytes;
@@ -95,6 +109,7 @@ typedef struct {
   int32_t max_depth;     /* deepest state (phrase length) */
   int32_t max_override;  /* most tokens any state overrides: the members of the
                             classes of the children along its suffix chain */
+  int64_t off_value_tab, off_state_rec;
 } tb_arena_layout;
 
 /* A device-resident arena: the layout plus the device address of the image. */

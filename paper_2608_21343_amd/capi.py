@@ -40,6 +40,7 @@ class tb_arena_layout(C.Structure):
         ("max_children", C.c_int32),
         ("max_depth", C.c_int32),
         ("max_override", C.c_int32),
+        ("off_value_tab", C.c_int64), ("off_state_rec", C.c_int64),
     ]
 
 
@@ -307,4 +308,6 @@ def image_arrays(image: np.ndarray, layout: tb_arena_layout) -> dict:
         "cls_ptr": arr(L.off_cls_ptr, V1, np.int32),
         "cls_tok": arr(L.off_cls_tok, V1 - 1, np.int32),
         "arc_mem": arr(L.off_arc_mem, 2 * L.n_states, np.uint32),
+        "value_tab": arr(L.off_value_tab, 512 * M, np.float32).reshape(M, 512),
+        "state_rec": arr(L.off_state_rec, 3 * N, np.uint32).reshape(N, 3),
     }

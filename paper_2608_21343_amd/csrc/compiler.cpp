@@ -58,6 +58,42 @@ inline int32_t child_of(const ModelGraph& g, int32_t s, int32_t c) {
   return -1;
 }
 
+// Per-model value tables (distinct psi and phi values, ascending) and the
+// packed state records of one model (see state_rec in tbias.h). fc, nc, lk,
+// lb, phi, psi and out point at the model's first state.
+void state_records(int32_t n, const int32_t* fc, const int32_t* nc, const int32_t* lk,
+                   const int32_t* lb, const float* phi, const float* psi, const int32_t* cls_ptr,
+                   float vtab[512], uint32_t* out) {
+  std::vector<float> vp(psi, psi + n), vf(phi, phi + n);
+  for (auto* v : {&vp, &vf}) {
+    std::sort(v->begin(), v->end());
+    v->erase(std::unique(v->begin(), v->end()), v->end());
+  }
+  for (int i = 0; i < 512; ++i) vtab[i] = 0.f;
+  for (size_t i = 0; i < vp.size() && i < 256; ++i) vtab[i] = vp[i];
+  for (size_t i = 0; i < vf.size() && i < 256; ++i) vtab[256 + i] = vf[i];
+  for (int32_t x = 0; x < n; ++x) {
+    const size_t ip = std::lower_bound(vp.begin(), vp.end(), psi[x]) - vp.begin();
+    const size_t iq = std::lower_bound(vf.begin(), vf.end(), phi[x]) - vf.begin();
+    const int32_t f = nc[x] > 0 ? fc[x] : 0;
+    const int32_t lab = lb[x];
+    const int32_t ms = lab >= 0 ? cls_ptr[lab] : 0;
+    const int32_t mc = lab >= 0 ? cls_ptr[lab + 1] - cls_ptr[lab] : 0;
+    const bool flag = f >= 65536 || nc[x] >= 255 || lk[x] >= 65536 || ms >= 65536 || mc > 255 ||
+                      ip >= 256 || iq >= 256;
+    if (flag) {
+      out[3 * (int64_t)x] = 0u;
+      out[3 * (int64_t)x + 1] = 0u;
+      out[3 * (int64_t)x + 2] = 0x80000000u;
+      continue;
+    }
+    out[3 * (int64_t)x] = (uint32_t)f | ((uint32_t)nc[x] << 16) | ((uint32_t)ip << 24);
+    out[3 * (int64_t)x + 1] = (uint32_t)lk[x] | ((uint32_t)ms << 16);
+    out[3 * (int64_t)x + 2] =
+        (uint32_t)mc | ((uint32_t)iq << 8) | ((uint32_t)(lab >= 0 ? lab : 0) << 16);
+  }
+}
+
 }  // namespace
 
 int compile_model(const int32_t* toks, const int64_t* tok_ptr, int64_t n_phrases,
@@ -302,6 +338,8 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   L.off_cls_ptr = take(4 * (int64_t)v_plus_blank);
   L.off_cls_tok = take(4 * (int64_t)V);
   L.off_arc_mem = take(8 * N);
+  L.off_value_tab = take(4 * 512 * M);
+  L.off_state_rec = take(12 * N);
   L.total_bytes = off;
   try {
     g->image.assign((size_t)off, 0);
@@ -347,7 +385,6 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   {
     std::vector<int32_t> seen(V, -1);
     int32_t gen = 0;
-    int64_t s0m = 0;
     for (int32_t m = 0; m < n_models; ++m) {
       const ModelGraph& mg = graphs[m];
       for (int32_t x = 1; x < mg.n; ++x, ++gen) {
@@ -378,6 +415,14 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
     const uint32_t t2 = (uint32_t)ct[m0 + (nm > 2 ? 2 : nm - 1)];
     am[2 * y] = t0 | (t1 << 16);
     am[2 * y + 1] = t2 | ((uint32_t)lab << 16) | (nm > 3 ? 0x80000000u : 0u);
+  }
+  // value tables and packed state records
+  for (int32_t m = 0; m < n_models; ++m) {
+    const int32_t so = I32(L.off_model_off)[m];
+    state_records(graphs[m].n, I32(L.off_first_child) + so, I32(L.off_n_child) + so,
+                  I32(L.off_link) + so, I32(L.off_label) + so, F32(L.off_phi) + so,
+                  F32(L.off_psi) + so, cp, F32(L.off_value_tab) + 512 * (int64_t)m,
+                  reinterpret_cast<uint32_t*>(img + L.off_state_rec) + 3 * (int64_t)so);
   }
   *out = g;
   return TB_OK;
@@ -479,6 +524,27 @@ extern "C" int tb_validate_image(const void* host_image, const tb_arena_layout* 
     const uint32_t w1 = t2 | ((uint32_t)lab << 16) | (nm > 3 ? 0x80000000u : 0u);
     if (am[2 * y] != (t0 | (t1 << 16)) || am[2 * y + 1] != w1)
       return fail(TB_ERANGE, "arc member record of state " + std::to_string(y) + " inconsistent");
+  }
+  // value tables and state records equal the ones derived from the arrays above
+  {
+    std::vector<uint32_t> want;
+    float vt[512];
+    for (int32_t m = 0; m < L.n_models; ++m) {
+      const int32_t so = I32(L.off_model_off)[m], n = I32(L.off_model_n)[m];
+      want.assign(3 * (size_t)n, 0u);
+      state_records(n, I32(L.off_first_child) + so, I32(L.off_n_child) + so,
+                    I32(L.off_link) + so, lab_all + so,
+                    reinterpret_cast<const float*>(img + L.off_phi) + so,
+                    reinterpret_cast<const float*>(img + L.off_psi) + so, cp, vt, want.data());
+      const float* vimg = reinterpret_cast<const float*>(img + L.off_value_tab) + 512 * (int64_t)m;
+      if (std::memcmp(vt, vimg, sizeof(vt)) != 0)
+        return fail(TB_ERANGE, "value table of model " + std::to_string(m) + " inconsistent");
+      const uint32_t* sr = reinterpret_cast<const uint32_t*>(img + L.off_state_rec) + 3 * (int64_t)so;
+      for (int32_t x = 0; x < n; ++x)
+        if (std::memcmp(&want[3 * (size_t)x], sr + 3 * (int64_t)x, 12) != 0)
+          return fail(TB_ERANGE, "state record of state " + std::to_string(x) + " of model " +
+                                     std::to_string(m) + " inconsistent");
+    }
   }
   return TB_OK;
 }

@@ -25,6 +25,8 @@ struct ArenaView {
   const int32_t* cls_ptr;
   const int32_t* cls_tok;
   const uint32_t* arc_mem;  // two words per state (see tb_arena_layout)
+  const float* value_tab;      // per model: 256 psi values, 256 phi values
+  const uint32_t* state_rec;   // three words per state (see tb_arena_layout)
   int32_t n_models;
   int32_t V1;            // V + 1
   int32_t max_override;  // most tokens any state overrides
@@ -48,6 +50,8 @@ inline ArenaView make_view(const tb_arena& a) {
   v.cls_ptr = reinterpret_cast<const int32_t*>(b + L.off_cls_ptr);
   v.cls_tok = reinterpret_cast<const int32_t*>(b + L.off_cls_tok);
   v.arc_mem = reinterpret_cast<const uint32_t*>(b + L.off_arc_mem);
+  v.value_tab = reinterpret_cast<const float*>(b + L.off_value_tab);
+  v.state_rec = reinterpret_cast<const uint32_t*>(b + L.off_state_rec);
   v.n_models = L.n_models;
   v.V1 = L.v_plus_blank;
   v.max_override = L.max_override;

@@ -30,9 +30,11 @@
 // its lanes that repeat elements of chunk PER-2 are masked to -inf. The blank
 // logit z[V] is lane 63 of the last chunk.
 //
-// Per-wave LDS: the row and an 8-bit tag table marking the classes that are
-// overridden in the state being evaluated. Shared LDS: the model's root row,
-// the class tables and the records of the first (shallowest) states.
+// Per-wave LDS: the row and a bitmap marking the classes that are overridden
+// in the state being evaluated. Shared LDS: the model's root row, the class
+// tables, and the packed records of the model's first (shallowest) states
+// with its psi and phi value tables: every state of a model of a few
+// thousand states, so that a step reads LDS only.
 #pragma once
 
 #include <climits>
@@ -63,6 +65,7 @@ struct RowSum {
 constexpr int32_t kNoTok = 0xffff;
 struct LaneTop {
   int32_t i1, i2;
+  float k1, k2;
 };
 
 // Tables shared by the waves of one workgroup (one stream).
@@ -86,12 +89,16 @@ struct Shape {
 template <int PER>
 struct alignas(16) FixedLds {
   static constexpr int W = Shape<PER>::W;
+  static constexpr int kMarkWords = 2 * PER;  // one bit per token id / class id
   float zbuf[W][64 * PER];  // row of the step each wave evaluates
-  uint8_t stamps[W][64 * PER];
+  uint32_t marks[W][kMarkWords];
   Tables<PER> tab;
   int32_t traj[W][kTraj];  // state after each of the first kTraj steps
   RowSum rsum[W];          // short calls: summary of row w
-  uint32_t rtop[W][64];    // short calls: each lane's two best root moves of row w
+  uint32_t ltop[W][64];    // short calls: each lane's two best root moves of row w
+  int32_t spec_ns[2][W];   // short calls: state after row w's step from its guess (by round)
+  int32_t spec_x[W];       // short calls: row w's final guess and its answer
+  int4 spec_ans[W];
   int32_t fin_state[W];    // exact state after each segment
   int32_t fin_ready[W];
   int32_t abort_flag;
@@ -107,17 +114,32 @@ struct alignas(16) HotRecords {
 };
 
 constexpr int kHotRecordBytes = 16 + 8;
+
+// Packed records (see state_rec in tbias.h) of the first HOT states of a
+// model and the model's psi and phi value tables, held in LDS by the greedy
+// kernels.
+template <int HOT>
+struct alignas(16) StateHot {
+  uint32_t w0[HOT];
+  uint32_t w1[HOT];
+  uint32_t w2[HOT];
+  float vpsi[256];
+  float vphi[256];
+};
+constexpr int kStateHotBytes = 12;
+
 template <int PER>
 constexpr int hot_states() {
-  const int room = (Shape<PER>::kBudget - (int)sizeof(FixedLds<PER>)) / kHotRecordBytes;
+  const int room =
+      (Shape<PER>::kBudget - (int)sizeof(FixedLds<PER>) - 2048) / kStateHotBytes;
   const int h = (room / 64) * 64;
-  return h > 4096 ? 4096 : h;
+  return h > 8192 ? 8192 : h;
 }
 
 template <int PER>
 struct alignas(16) SegLds : FixedLds<PER> {
   static constexpr int HOT = hot_states<PER>();
-  HotRecords<HOT> hot;
+  StateHot<HOT> hot;
 };
 
 struct Answer {
@@ -143,6 +165,11 @@ __device__ __forceinline__ float rlf(float v, int32_t lane) {
 template <class T>
 __device__ __forceinline__ T sload(const T* p) {
   return *(const __attribute__((address_space(4))) T*)(p);
+}
+
+__device__ __forceinline__ uint4 sload4(const uint4* p) {
+  const uint32_t* q = reinterpret_cast<const uint32_t*>(p);
+  return make_uint4(sload(q), sload(q + 1), sload(q + 2), sload(q + 3));
 }
 
 // Lane geometry of the last chunk (see the row layout above).
@@ -197,6 +224,52 @@ struct Graph {
   }
 };
 
+// Graph records for the greedy kernels: packed records from LDS for states <
+// nhot whose record is usable, else the plain arena arrays by scalar loads
+// (state ids are uniform; the arena is immutable while a step runs).
+struct SGraph {
+  const ArenaView* A;
+  int32_t off, nhot;
+  const uint32_t* w0;
+  const uint32_t* w1;
+  const uint32_t* w2;
+  const float* vpsi;
+  const float* vphi;
+  const uint16_t* cls_tok;  // class members (LDS copy of the arena's cls_tok)
+  template <int HOT, int PER>
+  __device__ __forceinline__ SGraph(const ArenaView& a, int32_t o, int32_t nh,
+                                    const StateHot<HOT>& h, const Tables<PER>& tb)
+      : A(&a), off(o), nhot(nh), w0(h.w0), w1(h.w1), w2(h.w2), vpsi(h.vpsi), vphi(h.vphi),
+        cls_tok(tb.cls_tok) {}
+  // first child, child count, suffix link and phi of state x from LDS
+  // (uniform); false when x has no usable LDS record
+  __device__ __forceinline__ bool srec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
+                                       float& phi) const {
+    if (x >= nhot) return false;
+    // the three words are read together (one LDS round trip), then checked
+    const uint32_t a0 = w0[x], b0 = w1[x], c0 = w2[x];
+    const uint32_t c = __builtin_amdgcn_readfirstlane(c0);
+    const uint32_t a = __builtin_amdgcn_readfirstlane(a0);
+    const uint32_t b = __builtin_amdgcn_readfirstlane(b0);
+    if (c >> 31) return false;
+    fc = (int32_t)(a & 0xffffu);
+    nc = (int32_t)((a >> 16) & 0xffu);
+    lnk = (int32_t)(b & 0xffffu);
+    phi = vphi[(c >> 8) & 0xffu];
+    return true;
+  }
+  // the same, from the arena when x has no usable LDS record
+  __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
+                                      float& phi) const {
+    if (!srec(x, fc, nc, lnk, phi)) {
+      fc = sload(A->first_child + off + x);
+      nc = sload(A->n_child + off + x);
+      lnk = sload(A->link + off + x);
+      phi = sload(A->phi + off + x);
+    }
+  }
+};
+
 // Arc member record fields.
 __device__ __forceinline__ int32_t arc_class(uint2 m) { return (int32_t)((m.y >> 16) & 0x7fffu); }
 __device__ __forceinline__ bool arc_more(uint2 m) { return (m.y >> 31) != 0u; }
@@ -221,6 +294,30 @@ __device__ __forceinline__ void fill_hot(HotRecords<HOT>& h, const ArenaView& A,
   }
 }
 
+// Packed records of states [0, nhot) of the model at off and its value
+// tables (model m) into LDS; NT threads.
+template <int HOT, int NT>
+__device__ __forceinline__ void fill_state_hot(StateHot<HOT>& h, const ArenaView& A, int32_t m,
+                                               int32_t off, int32_t nhot) {
+  const uint32_t* src = A.state_rec + 3 * (int64_t)off;
+#pragma unroll
+  for (int k = 0; k < (HOT + NT - 1) / NT; ++k) {
+    const int32_t i = k * NT + (int32_t)threadIdx.x;
+    if (i < nhot) {
+      h.w0[i] = src[3 * i];
+      h.w1[i] = src[3 * i + 1];
+      h.w2[i] = src[3 * i + 2];
+    }
+  }
+  if (nhot > 0) {
+    const float* vt = A.value_tab + 512 * (int64_t)m;
+    for (int32_t i = threadIdx.x; i < 512; i += NT) {
+      if (i < 256) h.vpsi[i] = vt[i];
+      else h.vphi[i - 256] = vt[i];
+    }
+  }
+}
+
 template <class Ld, int PER>
 __device__ __forceinline__ void load_row(float* dst, const typename Ld::T* row,
                                          const RowShape<PER>& rs) {
@@ -240,6 +337,23 @@ __device__ __forceinline__ uint8_t next_tag(uint8_t* stamps, uint32_t& tag) {
   }
   return (uint8_t)tag;
 }
+
+// Class-mark bitmaps (one bit per class id) of the greedy kernels. Marks are
+// set with LDS atomics and read by the same wave afterwards; a wave's LDS
+// operations complete in order.
+template <int PER>
+__device__ __forceinline__ void marks_clear(uint32_t* bits) {
+  if (__lane_id() < 2 * PER) bits[__lane_id()] = 0u;
+  asm volatile("" ::: "memory");
+}
+__device__ __forceinline__ void mark(uint32_t* bits, int32_t c) {
+  __hip_atomic_fetch_or(bits + (c >> 5), 1u << (c & 31), __ATOMIC_RELAXED,
+                        __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ bool is_marked(const uint32_t* bits, int32_t c) {
+  return (bits[c >> 5] >> (c & 31)) & 1u;
+}
+__device__ __forceinline__ void marks_fence() { asm volatile("" ::: "memory"); }
 
 // Per-lane best override candidate.
 struct Cand {
@@ -283,31 +397,52 @@ __device__ __forceinline__ void child_rec(const Graph& G, int32_t y, uint2& m, f
   }
 }
 
-// Marks the classes of the children [fc, fc+nc) in stamps.
-__device__ __forceinline__ void mark_children(const Graph& G, uint8_t* stamps, uint8_t tg,
-                                              int32_t fc, int32_t nc) {
+// Arc record (as arc_mem) and psi of child y: rebuilt from its LDS record
+// when it has a usable one, else read from the arena.
+__device__ __forceinline__ void child_rec(const SGraph& G, int32_t y, uint2& m, float& py) {
+  if (y < G.nhot) {
+    const uint32_t a = G.w0[y], b = G.w1[y], c = G.w2[y];
+    if (!(c >> 31)) {
+      const int32_t mc = (int32_t)(c & 0xffu), ms = (int32_t)(b >> 16);
+      const uint32_t t0 = G.cls_tok[ms];
+      const uint32_t t1 = G.cls_tok[ms + (mc > 1 ? 1 : 0)];
+      const uint32_t t2 = G.cls_tok[ms + (mc > 2 ? 2 : (mc > 1 ? 1 : 0))];
+      m = make_uint2(t0 | (t1 << 16), t2 | (c & 0x7fff0000u) | (mc > 3 ? 0x80000000u : 0u));
+      py = G.vpsi[a >> 24];
+      return;
+    }
+  }
+  const int64_t q = 2 * ((int64_t)G.off + y);
+  m = make_uint2(G.A->arc_mem[q], G.A->arc_mem[q + 1]);
+  py = G.A->psi[G.off + y];
+}
+
+// Marks the classes of the children [fc, fc+nc).
+__device__ __forceinline__ void mark_children(const SGraph& G, uint32_t* marks, int32_t fc,
+                                              int32_t nc) {
   for (int32_t j = __lane_id(); j < nc; j += 64) {
     uint2 m;
     float py;
     child_rec(G, fc + j, m, py);
-    stamps[arc_class(m)] = tg;
+    mark(marks, arc_class(m));
   }
+  marks_fence();
 }
 
-// Best root move whose class is not marked (tag tg), from every lane's two
-// best root moves: a lane whose best is marked offers its runner-up. Returns
-// false when some lane's best two are both marked and its further moves could
-// still reach the result.
+// Best root move whose class is not marked, from every lane's two best root
+// moves: a lane whose best is marked offers its runner-up. Returns false when
+// some lane's best two are both marked and its further moves could still
+// reach the result.
 template <int PER>
 __device__ __forceinline__ bool root_excluding(const Tables<PER>& tb, const float* zrow,
-                                               const uint8_t* stamps, uint8_t tg, LaneTop top,
-                                               float& rk, int32_t& rt) {
+                                               const uint32_t* marks, LaneTop top, float& rk,
+                                               int32_t& rt) {
   const bool h1 = top.i1 != kNoTok, h2 = top.i2 != kNoTok;
   const int32_t i1 = h1 ? top.i1 : 0, i2 = h2 ? top.i2 : 0;
   const int32_t c1 = tb.cls[i1], c2 = tb.cls[i2];
   const float k1 = zrow[i1] + tb.rpsi[i1], k2 = zrow[i2] + tb.rpsi[i2];
-  const bool o1 = h1 && c1 != 0xffff && stamps[c1] == tg;
-  const bool o2 = h2 && c2 != 0xffff && stamps[c2] == tg;
+  const bool o1 = h1 && c1 != 0xffff && is_marked(marks, c1);
+  const bool o2 = h2 && c2 != 0xffff && is_marked(marks, c2);
   const bool use1 = h1 && !o1, use2 = !use1 && h2 && !o2;
   const float k = use1 ? k1 : (use2 ? k2 : kNegInf);
   const int32_t t = use1 ? i1 : (use2 ? i2 : INT_MAX);
@@ -318,13 +453,13 @@ __device__ __forceinline__ bool root_excluding(const Tables<PER>& tb, const floa
   return __ballot(o1 && o2 && !(k2 < rk)) == 0ull;
 }
 
-// Best root move whose class is not marked (tag tg), over the whole row
-// (unrolled over the row's chunks so that the table reads of several chunks
-// issue together).
+// Best root move whose class is not marked, over the whole row (unrolled
+// over the row's chunks so that the table reads of several chunks issue
+// together).
 template <int PER>
 __device__ __forceinline__ void root_scan(const Tables<PER>& tb, const float* zrow,
-                                          const uint8_t* stamps, uint8_t tg,
-                                          const RowShape<PER>& rs, float& rk, int32_t& rt) {
+                                          const uint32_t* marks, const RowShape<PER>& rs,
+                                          float& rk, int32_t& rt) {
   const int lane = __lane_id();
   float k2 = kNegInf;
   int32_t t2 = INT_MAX;
@@ -334,7 +469,7 @@ __device__ __forceinline__ void root_scan(const Tables<PER>& tb, const float* zr
     const int32_t cv = tb.cls[v];
     const bool ok_lane = (j < PER - 1) || rs.last_ok;
     const float k = zrow[v] + tb.rpsi[v];  // -inf for the blank
-    const bool ov = cv != 0xffff && stamps[cv] == tg;
+    const bool ov = cv != 0xffff && is_marked(marks, cv);
     if (ok_lane && !ov && k > k2) { k2 = k; t2 = v; }
   }
   wave_argmax_dpp(k2, t2, rk, rt);
@@ -349,8 +484,8 @@ __device__ __forceinline__ void root_scan(const Tables<PER>& tb, const float* zr
 // keeps the state. Class marks are needed only when the chain has more than
 // one state (to let deeper states win) or when r.r1's class is overridden.
 template <int PER>
-__device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>& tb,
-                                               const float* zrow, uint8_t* stamps, uint32_t& tag,
+__device__ __forceinline__ Answer eval_general(const SGraph& G, const Tables<PER>& tb,
+                                               const float* zrow, uint32_t* marks,
                                                const RowShape<PER>& rs, int32_t x, const RowSum& r,
                                                const LaneTop* top, int32_t V) {
   const int lane = __lane_id();
@@ -359,8 +494,7 @@ __device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>
   G.rec(x, fc, nc, lnk, phi_x);
   const int32_t fc0 = fc, nc0 = nc;
   const bool multi = lnk != 0;
-  uint8_t tg = 0;
-  if (multi) tg = next_tag<PER>(stamps, tag);
+  if (multi) marks_clear<PER>(marks);
 
   Cand c;
   c.k = kNegInf;
@@ -382,8 +516,8 @@ __device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>
           const int32_t lab = arc_class(m);
           bool take = true;
           if (multi) {
-            take = lvl == 0 || stamps[lab] != tg;
-            if (take) stamps[lab] = tg;
+            take = lvl == 0 || !is_marked(marks, lab);
+            if (take) mark(marks, lab);
           }
           if (take) {
             over |= lab == r.r1_cls;
@@ -402,8 +536,9 @@ __device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>
         const int32_t lab = arc_class(m);
         bool take = true;
         if (multi) {
-          take = lvl == 0 || stamps[lab] != tg;  // uniform
-          if (take) stamps[lab] = tg;
+          take = lvl == 0 || !is_marked(marks, lab);  // uniform
+          if (take) mark(marks, lab);
+          marks_fence();
         }
         if (take) {
           over |= lab == r.r1_cls;
@@ -421,6 +556,7 @@ __device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>
         }
       }
     }
+    marks_fence();  // the next level reads this level's marks
     if (lnk == 0) break;
     float phi_unused;
     G.rec(lnk, fc, nc, lnk, phi_unused);
@@ -438,11 +574,11 @@ __device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>
   float r_psi = r.r1_psi, r_z = r.r1_z;
   if (__ballot(over) != 0ull) {
     if (!multi) {
-      tg = next_tag<PER>(stamps, tag);
-      mark_children(G, stamps, tg, fc0, nc0);
+      marks_clear<PER>(marks);
+      mark_children(G, marks, fc0, nc0);
     }
-    if (!(top && root_excluding<PER>(tb, zrow, stamps, tg, *top, rk, rt)))
-      root_scan<PER>(tb, zrow, stamps, tg, rs, rk, rt);
+    if (!(top && root_excluding<PER>(tb, zrow, marks, *top, rk, rt)))
+      root_scan<PER>(tb, zrow, marks, rs, rk, rt);
     const int32_t rv = (rt < V) ? rt : 0;
     r_ns = tb.rdst[rv];
     r_psi = tb.rpsi[rv];
@@ -472,90 +608,103 @@ __device__ __forceinline__ Answer eval_general(const Graph& G, const Tables<PER>
   return a;
 }
 
-// Straight-line evaluation for the common shapes: at most four states on x's
-// suffix chain, at most 64 children in all, classes of at most three members.
-// Lane j takes child j of the concatenated child lists, x's first; a class is
-// taken from the deepest chain state that has it. Records come from LDS for
-// hot states, else from the arena (scalar loads for the chain, one vector
-// load per child). Returns false, with no output, on any other shape.
+// The step from state x from the packed state records in LDS. The children of
+// the states on x's suffix chain (x, link(x), ... up to four non-root states,
+// at most 64 children in all) are the override candidates, one per lane; a
+// child is dropped when a deeper chain state has a child on the same class.
+// Every other token takes its root move: the row's best root move unless its
+// class is overridden, else the best unmarked one from the lanes' two best
+// root moves (top) or a masked scan of the row. The blank keeps the state.
+// Returns false, with no output, on any other shape (a state or child without
+// a usable LDS record, a class of more than three members).
 template <int PER>
-__device__ __forceinline__ bool eval_fast(const Graph& G, const Tables<PER>& tb,
-                                          const float* zrow, uint8_t* stamps, uint32_t& tag,
-                                          int32_t x, const RowSum& r, const LaneTop* top,
-                                          int32_t V, Answer& a) {
+__device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb,
+                                          const float* zrow, uint32_t* marks,
+                                          const RowShape<PER>& rs, int32_t x, const RowSum& r,
+                                          const LaneTop* top, int32_t V, Answer& a) {
   const int lane = __lane_id();
-  int32_t f0 = 0, f1 = 0, f2 = 0, f3 = 0, n0 = 0, n1 = 0, n2 = 0, n3 = 0, levels = 0;
+  int32_t fc, nc, lnk;
   float phi_x;
-  {
-    int32_t fc, nc, lnk;
-    G.rec(x, fc, nc, lnk, phi_x);
-    // chain states' child ranges (the root's children are the dense root row)
-    if (x != 0) {
-      f0 = fc;
-      n0 = nc;
-      levels = 1;
-      while (lnk != 0) {
-        if (levels == 4) return false;
-        float phi_unused;
-        G.rec(lnk, fc, nc, lnk, phi_unused);
-        if (levels == 1) { f1 = fc; n1 = nc; }
-        else if (levels == 2) { f2 = fc; n2 = nc; }
-        else { f3 = fc; n3 = nc; }
-        ++levels;
-      }
+  if (!G.srec(x, fc, nc, lnk, phi_x)) return false;
+  int32_t f0 = 0, f1 = 0, f2 = 0, f3 = 0, n0 = 0, n1 = 0, n2 = 0, n3 = 0, levels = 0;
+  if (x != 0) {  // the root's children are the dense root row
+    f0 = fc;
+    n0 = nc;
+    levels = 1;
+    while (lnk != 0) {
+      if (levels == 4) return false;
+      float phi_unused;
+      if (!G.srec(lnk, fc, nc, lnk, phi_unused)) return false;
+      if (levels == 1) { f1 = fc; n1 = nc; }
+      else if (levels == 2) { f2 = fc; n2 = nc; }
+      else { f3 = fc; n3 = nc; }
+      ++levels;
     }
   }
   const int32_t s1 = n0, s2 = s1 + n1, s3 = s2 + n2, total = s3 + n3;
   if (total > 64) return false;
-  const bool valid = lane < total;
-  const int32_t lv = (lane >= s1) + (lane >= s2) + (lane >= s3);
-  const int32_t fb = lv == 0 ? f0 : lv == 1 ? f1 : lv == 2 ? f2 : f3;
-  const int32_t sb = lv == 0 ? 0 : lv == 1 ? s1 : lv == 2 ? s2 : s3;
-  const int32_t y = valid ? fb + (lane - sb) : 0;
-  uint2 m;
-  float py;
-  child_rec(G, y, m, py);
-  if (__ballot(valid && arc_more(m)) != 0ull) return false;
-  const int32_t lab = arc_class(m);
-  bool take = valid;
-  uint8_t tg = 0;
-  const bool marked = levels > 1;
-  if (marked) {
-    // level by level, deepest first: a class already marked is shadowed
-    // (LDS runs a wave's accesses in order, so each level sees the marks of
-    // the levels before it)
-    tg = next_tag<PER>(stamps, tag);
-    for (int32_t l = 0; l < levels; ++l) {
-      if (valid && lv == l) {
-        if (l > 0) take = stamps[lab] != tg;
-        if (take) stamps[lab] = tg;
+
+  // best override candidate (none when the chain has no children)
+  float ok = kNegInf, o_psi = 0.f, o_z = 0.f;
+  int32_t ot = INT_MAX, o_ns = 0;
+  bool over = false;
+  if (total > 0) {
+    const bool in = lane < total;
+    const int32_t lv = (lane >= s1) + (lane >= s2) + (lane >= s3);
+    const int32_t fb = lv == 0 ? f0 : lv == 1 ? f1 : lv == 2 ? f2 : f3;
+    const int32_t sb = lv == 0 ? 0 : lv == 1 ? s1 : lv == 2 ? s2 : s3;
+    const int32_t y = in ? fb + (lane - sb) : 0;
+    uint32_t c0 = 0u, c1 = 0u, c2 = 0x80000000u;
+    if (in && y < G.nhot) {
+      c0 = G.w0[y];
+      c1 = G.w1[y];
+      c2 = G.w2[y];
+    }
+    const int32_t mc = (int32_t)(c2 & 0xffu);
+    if (__ballot(in && ((c2 >> 31) != 0u || mc > 3)) != 0ull) return false;
+    const int32_t lab = (int32_t)((c2 >> 16) & 0x7fffu);
+    const int32_t ms = in ? (int32_t)(c1 >> 16) : 0;
+    const float py = G.vpsi[c0 >> 24];
+    const int32_t t0 = tb.cls_tok[ms];
+    const int32_t t1 = tb.cls_tok[ms + (mc > 1 ? 1 : 0)];
+    const int32_t t2 = tb.cls_tok[ms + (mc > 2 ? 2 : (mc > 1 ? 1 : 0))];
+    const float z0 = zrow[t0], z1 = zrow[t1], z2 = zrow[t2];
+    float kb = z0 + py, zb_ = z0;
+    int32_t tk = t0;
+    const float k1 = z1 + py, k2 = z2 + py;
+    if (k1 > kb) { kb = k1; tk = t1; zb_ = z1; }  // members ascend: ties keep the lower
+    if (k2 > kb) { kb = k2; tk = t2; zb_ = z2; }
+    bool take = in;
+    if (levels > 1) {
+      // a class that a deeper chain state (a lower level) also has is shadowed
+      const int32_t last = levels == 2 ? s1 : (levels == 3 ? s2 : s3);
+      for (int32_t j = 0; j < last; ++j) {
+        const int32_t cj = __builtin_amdgcn_readlane(lab, j);
+        const int32_t lvj = (j >= s1) + (j >= s2) + (j >= s3);
+        take = take && !(lvj < lv && cj == lab);
       }
     }
+    if (__ballot(take) != 0ull) {
+      const int32_t wl = wave_argmax_dpp(take ? kb : kNegInf, take ? tk : INT_MAX, ok, ot);
+      o_ns = rl(y, wl);
+      o_psi = rlf(py, wl);
+      o_z = rlf(zb_, wl);
+    }
+    over = __ballot(take && lab == r.r1_cls) != 0ull;
+    if (over) {
+      marks_clear<PER>(marks);
+      if (take) mark(marks, lab);
+      marks_fence();
+    }
   }
-  const int32_t t0 = (int32_t)(m.x & 0xffffu), t1 = (int32_t)(m.x >> 16);
-  const int32_t t2 = (int32_t)(m.y & 0xffffu);
-  const float z0 = zrow[t0], z1 = zrow[t1], z2 = zrow[t2];
-  float kb = z0 + py, zb_ = z0;
-  int32_t tk = t0;
-  const float k1 = z1 + py, k2 = z2 + py;
-  if (k1 > kb) { kb = k1; tk = t1; zb_ = z1; }  // members ascend: ties keep the lower
-  if (k2 > kb) { kb = k2; tk = t2; zb_ = z2; }
-  const bool over = take && lab == r.r1_cls;
-  float ok;
-  int32_t ot;
-  const int32_t wl = wave_argmax_dpp(take ? kb : kNegInf, take ? tk : INT_MAX, ok, ot);
-  const int32_t o_ns = rl(y, wl);
-  const float o_psi = rlf(py, wl);
-  const float o_z = rlf(zb_, wl);
 
+  // best root move whose class is not overridden
   float rk = r.ymax;
   int32_t rt = r.r1_tok, r_ns = r.r1_dst;
   float r_psi = r.r1_psi, r_z = r.r1_z;
-  if (__ballot(over) != 0ull) {
-    // mark every overriding class, then take the best unmarked root move
-    if (!marked) tg = next_tag<PER>(stamps, tag);
-    if (take) stamps[lab] = tg;
-    if (!(top && root_excluding<PER>(tb, zrow, stamps, tg, *top, rk, rt))) return false;
+  if (over) {
+    if (!(top && root_excluding<PER>(tb, zrow, marks, *top, rk, rt)))
+      root_scan<PER>(tb, zrow, marks, rs, rk, rt);
     const int32_t rv = (rt < V) ? rt : 0;
     r_ns = tb.rdst[rv];
     r_psi = tb.rpsi[rv];
@@ -584,16 +733,16 @@ __device__ __forceinline__ bool eval_fast(const Graph& G, const Tables<PER>& tb,
   return true;
 }
 
-// The boosted step from state x: the straight-line path when it applies, else
-// the general one.
+// The boosted step from state x: from the LDS records when they apply, else
+// the general path.
 template <int PER>
-__device__ __forceinline__ Answer eval_state(const Graph& G, const Tables<PER>& tb,
-                                             const float* zrow, uint8_t* stamps, uint32_t& tag,
+__device__ __forceinline__ Answer eval_state(const SGraph& G, const Tables<PER>& tb,
+                                             const float* zrow, uint32_t* marks,
                                              const RowShape<PER>& rs, int32_t x, const RowSum& r,
                                              const LaneTop* top, int32_t V) {
   Answer a;
-  if (eval_fast<PER>(G, tb, zrow, stamps, tag, x, r, top, V, a)) return a;
-  return eval_general<PER>(G, tb, zrow, stamps, tag, rs, x, r, top, V);
+  if (eval_walk<PER>(G, tb, zrow, marks, rs, x, r, top, V, a)) return a;
+  return eval_general<PER>(G, tb, zrow, marks, rs, x, r, top, V);
 }
 
 // State-independent part of a step on a row held in registers (raw[j] as
@@ -636,6 +785,8 @@ __device__ __forceinline__ RowSum row_summary(float* zrow, const Tables<PER>& tb
   if (kTop2) {
     top->i1 = (yb > kNegInf) ? idx : kNoTok;
     top->i2 = (j2 < 0 || !(y2 > kNegInf)) ? kNoTok : ((j2 == PER - 1) ? rs.last_idx : 64 * j2 + lane);
+    top->k1 = yb;
+    top->k2 = y2;
   }
   zmax = wave_max_dpp(zmax);
   wave_argmax_dpp(yb, idx, r.ymax, r.r1_tok);
@@ -659,8 +810,8 @@ __device__ __forceinline__ RowSum row_summary(float* zrow, const Tables<PER>& tb
 
 // The step from state s on a summarised row (zrow in LDS).
 template <int PER>
-__device__ __forceinline__ Answer step_from(const Graph& G, const Tables<PER>& tb,
-                                            const float* zrow, uint8_t* stamps, uint32_t& tag,
+__device__ __forceinline__ Answer step_from(const SGraph& G, const Tables<PER>& tb,
+                                            const float* zrow, uint32_t* marks,
                                             const RowShape<PER>& rs, const RowSum& r, int32_t s,
                                             int mode, int32_t V, const LaneTop* top = nullptr) {
   if (mode != 1) {
@@ -672,18 +823,18 @@ __device__ __forceinline__ Answer step_from(const Graph& G, const Tables<PER>& t
     a.zv = blank ? r.zb : r.ymax;
     return a;
   }
-  return eval_state<PER>(G, tb, zrow, stamps, tag, rs, s, r, top, V);
+  return eval_state<PER>(G, tb, zrow, marks, rs, s, r, top, V);
 }
 
 // One complete step on a row held in registers.
 template <int PER>
-__device__ __forceinline__ Answer full_step(const Graph& G, const Tables<PER>& tb, float* zrow,
-                                            uint8_t* stamps, uint32_t& tag, const float* raw,
+__device__ __forceinline__ Answer full_step(const SGraph& G, const Tables<PER>& tb, float* zrow,
+                                            uint32_t* marks, const float* raw,
                                             const float* rp, const RowShape<PER>& rs, int32_t s,
                                             int mode, int32_t V, bool need_lse, float& lse) {
   const RowSum r = row_summary<PER>(zrow, tb, raw, rp, rs, V, need_lse);
   lse = r.lse;
-  return step_from<PER>(G, tb, zrow, stamps, tag, rs, r, s, mode, V);
+  return step_from<PER>(G, tb, zrow, marks, rs, r, s, mode, V);
 }
 
 // Root row and class tables of model m (mode 1) into LDS; NT threads.
@@ -725,8 +876,8 @@ __device__ __forceinline__ void root_psi_regs(float* rp, const Tables<PER>& tb,
 // row t). emit(t, answer, lse) writes a row. Returns true when the
 // trajectories met; x is the exact state after the last recomputed row.
 template <class Ld, int PER, bool kTwoAhead, class OldFn, class EmitFn>
-__device__ __forceinline__ bool repair_run(const Graph& G, const Tables<PER>& tb, float* zrow,
-                                           uint8_t* stamps, uint32_t& tag, const float* rp,
+__device__ __forceinline__ bool repair_run(const SGraph& G, const Tables<PER>& tb, float* zrow,
+                                           uint32_t* marks, const float* rp,
                                            const RowShape<PER>& rs,
                                            const typename Ld::T* col, int64_t tstride,
                                            int32_t t, int32_t t_end, int32_t& x, int mode,
@@ -737,7 +888,7 @@ __device__ __forceinline__ bool repair_run(const Graph& G, const Tables<PER>& tb
     const int32_t tn = (tt + kAhead < t_end) ? tt + kAhead : t_end - 1;
     load_row<Ld, PER>(pf, col + (int64_t)tn * tstride, rs);
     float lse;
-    const Answer a = full_step<PER>(G, tb, zrow, stamps, tag, cur, rp, rs, x, mode, V, true, lse);
+    const Answer a = full_step<PER>(G, tb, zrow, marks, cur, rp, rs, x, mode, V, true, lse);
     const int32_t old = old_state(tt);
     emit(tt, a, lse);
     x = __builtin_amdgcn_readfirstlane(a.ns);
@@ -796,9 +947,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
 
   fill_tables<PER, NT>(S.tab, A, m, mode);
   const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
-  fill_hot<HOT, NT>(S.hot, A, off, nhot);
-  for (int32_t i = threadIdx.x; i < (int32_t)sizeof(S.stamps) / 4; i += NT)
-    reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
+  fill_state_hot<HOT, NT>(S.hot, A, m, off, nhot);
   if (threadIdx.x < W) {
     S.fin_ready[threadIdx.x] = 0;
     S.fin_state[threadIdx.x] = 0;
@@ -806,10 +955,9 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   if (threadIdx.x == 0) S.abort_flag = 0;
   __syncthreads();
 
-  const Graph Gr(A, off, nhot, S.hot);
+  const SGraph Gr(A, off, nhot, S.hot, S.tab);
   float* zrow = S.zbuf[w];
-  uint8_t* stamps = S.stamps[w];
-  uint32_t tag = 0;
+  uint32_t* marks = S.marks[w];
   float rp[PER];
   root_psi_regs<PER>(rp, S.tab, rs);
 
@@ -831,7 +979,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
       if (t == t0) assumed = s;
       float lse;
       const Answer a =
-          full_step<PER>(Gr, S.tab, zrow, stamps, tag, cur, rp, rs, s, mode, V, t >= t0, lse);
+          full_step<PER>(Gr, S.tab, zrow, marks, cur, rp, rs, s, mode, V, t >= t0, lse);
       if (t >= t0) {
         const int32_t i = t - t0;
         const int32_t ln = i & 63;
@@ -895,7 +1043,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
       };
       int32_t x = exact;
       const bool met =
-          repair_run<Ld, PER, false>(Gr, S.tab, zrow, stamps, tag, rp, rs, col, tstride, t0, t1,
+          repair_run<Ld, PER, false>(Gr, S.tab, zrow, marks, rp, rs, col, tstride, t0, t1,
                                      x, mode, V, ra, rb, nullptr, old_state, emit);
       fin = met ? s : x;
     }
@@ -914,14 +1062,14 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
 // until the stored trajectory is met. Four waves fill the tables, wave 0
 // repairs. Writes the carry.
 constexpr int kFixThreads = 256;
-constexpr int kFixHot = 2048;
+constexpr int kFixHot = 6144;
 
 template <int PER>
 struct alignas(16) FixLds {
   Tables<PER> tab;
   float zrow[64 * PER];
-  uint8_t stamps[64 * PER];
-  HotRecords<kFixHot> hot;
+  uint32_t marks[2 * PER];
+  StateHot<kFixHot> hot;
 };
 
 template <class Ld, int PER>
@@ -953,13 +1101,10 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
     const int32_t off = A.model_off[m], n = A.model_n[m];
     const int32_t nhot = n < kFixHot ? n : kFixHot;
     fill_tables<PER, kFixThreads>(S.tab, A, m, 1);
-    fill_hot<kFixHot, kFixThreads>(S.hot, A, off, nhot);
-    for (int32_t i = threadIdx.x; i < 16 * PER; i += kFixThreads)
-      reinterpret_cast<uint32_t*>(S.stamps)[i] = 0u;
+    fill_state_hot<kFixHot, kFixThreads>(S.hot, A, m, off, nhot);
     __syncthreads();
     if (threadIdx.x >= 64) return;  // no barrier follows
-    const Graph Gr(A, off, nhot, S.hot);
-    uint32_t tag = 0;
+    const SGraph Gr(A, off, nhot, S.hot, S.tab);
     float rp[PER];
     root_psi_regs<PER>(rp, S.tab, rs);
     auto old_state = [&](int32_t t) -> int32_t {
@@ -993,7 +1138,7 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
         emit(t, a, lse);
         t_stop = t + 1;
       };
-      repair_run<Ld, PER, true>(Gr, S.tab, S.zrow, S.stamps, tag, rp, rs, col, tstride, tb0, T,
+      repair_run<Ld, PER, true>(Gr, S.tab, S.zrow, S.marks, rp, rs, col, tstride, tb0, T,
                                 x, 1, V, ra, rb, rc, old_state, emit_track);
       done = t_stop;
     }
@@ -1002,9 +1147,24 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
     states[b] = timed_out ? kStateTimeout : out_state[(int64_t)(T - 1) * B + b];
 }
 
-// Short calls (T <= W steps, a streaming chunk): no speculation. Wave w
-// summarises row w (normaliser, best root move, row copy in LDS) in parallel;
-// then wave 0 takes the T state-dependent steps in order from LDS.
+// Short calls (T <= W steps, a streaming chunk). Wave w owns row w: it
+// summarises the row (normaliser, best root moves, row copy in LDS), then
+// evaluates the step of row w from a guessed start state x_w, all rows in
+// parallel:
+//
+//   x_0 = the carried state (exact);
+//   x_w (w >= 1) starts as the target of row w-1's best root move, the move
+//   taken from most states; after each of kSpecRounds rounds, x_w <- the
+//   state reached by row w-1's step from x_{w-1} (rows whose guess did not
+//   change are not evaluated again).
+//
+// Wave 0 then walks the rows in order from the exact carried state: a row
+// whose guess equals the exact state keeps its answer, any other row is
+// evaluated again from the exact state. Mostly the guesses hold, so the
+// sequential part is a few comparisons plus the rows inside long phrase
+// matches.
+constexpr int kSpecRounds = 2;
+
 template <class Ld, int PER>
 __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
@@ -1026,55 +1186,85 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   int32_t off = 0, n = 0;
   const int mode = resolve_stream(A, m, s0, off, n);
   const RowShape<PER> rs(V1);
+  const bool own = w < T;  // this wave has a row
   float raw[PER];
-  if (w < T) load_row<Ld, PER>(raw, col + (int64_t)w * tstride, rs);
+  if (own) load_row<Ld, PER>(raw, col + (int64_t)w * tstride, rs);
 
   fill_tables<PER, NT>(S.tab, A, m, mode);
   const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
-  fill_hot<HOT, NT>(S.hot, A, off, nhot);
-  for (int32_t i = threadIdx.x; i < 16 * PER; i += NT)
-    reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
+  fill_state_hot<HOT, NT>(S.hot, A, m, off, nhot);
   __syncthreads();
 
-  if (w < T) {
+  RowSum r = {};
+  LaneTop top = {kNoTok, kNoTok, kNegInf, kNegInf};
+  if (own) {
     float rp[PER];
     root_psi_regs<PER>(rp, S.tab, rs);
-    LaneTop top;
-    const RowSum r = row_summary<PER, true>(S.zbuf[w], S.tab, raw, rp, rs, V, true, &top);
+    r = row_summary<PER, true>(S.zbuf[w], S.tab, raw, rp, rs, V, true, &top);
     if (lane == 0) S.rsum[w] = r;
-    S.rtop[w][lane] = (uint32_t)top.i1 | ((uint32_t)top.i2 << 16);
+    S.ltop[w][lane] = (uint32_t)top.i1 | ((uint32_t)top.i2 << 16);
+  }
+  __syncthreads();
+
+  const SGraph Gr(A, off, nhot, S.hot, S.tab);
+  const int32_t fixed = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+  int32_t x;  // guessed start state of row w
+  if (mode != 1) {
+    x = fixed;  // unbiased rows: the step does not depend on the state
+  } else if (w == 0) {
+    x = s0;
+  } else {
+    x = own ? __builtin_amdgcn_readfirstlane(S.rsum[w - 1].r1_dst) : 0;
+  }
+  Answer a = {0, 0, 0.f, 0.f};
+  bool need = own;
+#pragma unroll
+  for (int round = 0; round < kSpecRounds; ++round) {
+    if (need) a = step_from<PER>(Gr, S.tab, S.zbuf[w], S.marks[w], rs, r, x, mode, V, &top);
+    if (own && lane == 0) lds_st(&S.spec_ns[round & 1][w], a.ns);
+    __syncthreads();
+    if (round + 1 < kSpecRounds) {
+      int32_t xn = x;
+      if (own && w > 0 && mode == 1)
+        xn = __builtin_amdgcn_readfirstlane(lds_ld(&S.spec_ns[round & 1][w - 1]));
+      need = xn != x;
+      x = xn;
+    }
+  }
+  if (own && lane == 0) {
+    S.spec_x[w] = x;
+    S.spec_ans[w] = make_int4(a.tok, a.ns, __float_as_int(a.b), __float_as_int(a.zv));
   }
   __syncthreads();
   if (w != 0) return;
 
-  const Graph Gr(A, off, nhot, S.hot);
-  uint32_t tag = 0;
-  int32_t s = (mode == 1) ? s0 : ((mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID);
-  int32_t o_tok = 0, o_st = 0;
-  float o_sc = 0.f;
-  RowSum rn = S.rsum[0];
-  uint32_t tpn = S.rtop[0][lane];
+  // lane t holds row t's answer; rows off the exact trajectory are redone
+  int4 ans = make_int4(0, 0, 0, 0);
+  int32_t gx = INT_MIN;
+  if (lane < T) {
+    ans = S.spec_ans[lane];
+    gx = S.spec_x[lane];
+  }
+  int32_t s = (mode == 1) ? s0 : fixed;
   for (int32_t t = 0; t < T; ++t) {
-    const RowSum r = rn;
-    const uint32_t tp = tpn;
-    if (t + 1 < T) {  // the next row's summary is read while this step runs
-      rn = S.rsum[t + 1];
-      tpn = S.rtop[t + 1][lane];
+    int32_t ns;
+    if (rl(gx, t) == s) {
+      ns = rl(ans.y, t);
+    } else {
+      const RowSum rt = S.rsum[t];
+      const uint32_t tp = S.ltop[t][lane];
+      const LaneTop tt = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16), 0.f, 0.f};
+      const Answer e = step_from<PER>(Gr, S.tab, S.zbuf[t], S.marks[0], rs, rt, s, mode, V, &tt);
+      if (lane == t) ans = make_int4(e.tok, e.ns, __float_as_int(e.b), __float_as_int(e.zv));
+      ns = __builtin_amdgcn_readfirstlane(e.ns);
     }
-    const LaneTop top = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16)};
-    const Answer a =
-        step_from<PER>(Gr, S.tab, S.zbuf[t], S.stamps[0], tag, rs, r, s, mode, V, &top);
-    const bool mine = lane == t;
-    o_tok = mine ? a.tok : o_tok;
-    o_st = mine ? a.ns : o_st;
-    o_sc = mine ? (a.zv - r.lse) + a.b : o_sc;
-    s = __builtin_amdgcn_readfirstlane(a.ns);
+    s = ns;
   }
   if (lane < T) {
     const int64_t oi = (int64_t)lane * B + b;
-    out_tok[oi] = o_tok;
-    out_state[oi] = o_st;
-    out_score[oi] = o_sc;
+    out_tok[oi] = ans.x;
+    out_state[oi] = ans.y;
+    out_score[oi] = (__int_as_float(ans.w) - S.rsum[lane].lse) + __int_as_float(ans.z);
   }
   if (lane == 0) states[b] = s;
 }

@@ -155,6 +155,10 @@ def test_validate_rejects_corrupt_images():
     corrupt(L.off_root_psi + 4 * cfg.V, int(np.float32(1.0).view(np.int32)))  # blank column
     # arc member records must agree with the labels
     corrupt(L.off_arc_mem + 8 * 3, 0)
+    # packed state records and value tables must agree with the state arrays
+    corrupt(L.off_state_rec + 12 * 5, 7)          # state 5, word 0
+    corrupt(L.off_state_rec + 12 * 9 + 8, 1)      # state 9, word 2
+    corrupt(L.off_value_tab + 4 * 3, int(np.float32(99.0).view(np.int32)))
     # class member lists must list each classed token under its own class
     ct0 = int(np.frombuffer(good, dtype=np.int32, count=1, offset=L.off_cls_tok)[0])
     other = int(np.nonzero(cm[:cfg.V] != cm[ct0])[0][0])
@@ -253,3 +257,48 @@ def test_compile_rejects_vocabularies_beyond_the_arc_records():
         capi.tb_compile_graphs(np.array([0, 1], np.int64), np.array([0, 1], np.int64),
                                np.array([5], np.int32), 1.0, 2.0, cm)
     assert e.value.code == capi.TB_ERANGE
+
+
+@pytest.mark.parametrize("name,streams", [("batched", [0, 5]), ("streaming", [0, 127]),
+                                          ("stress_greedy", [3])])
+def test_state_records_unpack_to_the_oracle_graph(name, streams):
+    """Every packed state record unpacks to the oracle's graph: first child,
+    child count, suffix link, the arc class and its member list, and psi/phi
+    through the model's value tables (exact float32 values)."""
+    cfg = W.config_by_name(name)
+    cm = W.class_map(cfg)
+    lists = W.phrases(cfg, streams)
+    mp, tp, tk = W.phrase_csr(lists)
+    g = capi.tb_compile_graphs(mp, tp, tk, cfg.token_w, cfg.end_bonus, cm)
+    A = capi.image_arrays(g.host_image(), g.layout)
+    members = {}
+    for v in range(cfg.V):
+        members.setdefault(int(cm[v]), []).append(v)
+    for m, lst in enumerate(lists):
+        og = oracle.build_graph(lst, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+        off = int(A["model_off"][m])
+        vt = A["value_tab"][m]
+        many = len(set(og.psi32.tolist())) > 256 or len(set(og.phi32.tolist())) > 256
+        for x in range(og.n_states):
+            w0, w1, w2 = (int(v) for v in A["state_rec"][off + x])
+            kids = sorted(og.goto[x].values())
+            cls_n = len(members[og.strings[x][-1]]) if x > 0 else 0
+            fits = (len(kids) < 255 and (not kids or kids[0] < 65536) and og.link[x] < 65536
+                    and cls_n <= 255 and not many)
+            assert bool(w2 >> 31) == (not fits), x
+            if not fits:
+                assert w0 == 0 and w1 == 0 and w2 == 1 << 31
+                continue
+            assert (w0 >> 16) & 0xff == len(kids)
+            if kids:
+                assert w0 & 0xffff == kids[0]
+            assert w1 & 0xffff == og.link[x]
+            assert vt[w0 >> 24] == og.psi32[x]
+            assert vt[256 + ((w2 >> 8) & 0xff)] == og.phi32[x]
+            if x > 0:
+                c = og.strings[x][-1]
+                assert (w2 >> 16) & 0x7fff == c
+                mem = members[c]
+                assert w2 & 0xff == len(mem)
+                ms = w1 >> 16
+                assert list(A["cls_tok"][ms:ms + len(mem)]) == mem
