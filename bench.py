@@ -1,24 +1,30 @@
-"""Benchmark of the boosted greedy decode step on one MI355X.
+"""Benchmark of the boosted decode step on one MI355X.
 
-Workload: streaming greedy decoding -- B=128 streams, V=1024 tokens + blank,
-T=1024 steps fed as 64 calls of 16 steps each with the graph states carried
-from call to call; fp32 joint logits N(0,1) with a +1.5 blank offset; every
-stream has its own list of 1000 phrases (lengths 1-10, Zipf 1.1) and a
-case-insensitive token map. All inputs are synthetic and seeded
-(workloads.logit_chunks) and are resident in HBM before the timed region.
+Default workload (the headline): streaming greedy decoding -- B=128 streams,
+V=1024 tokens + blank, T=1024 steps fed as 64 calls of 16 steps each with the
+graph states carried from call to call; fp32 joint logits N(0,1) with a +1.5
+blank offset; every stream has its own list of 1000 phrases (lengths 1-10,
+Zipf 1.1) and a case-insensitive token map. All inputs are synthetic and
+seeded (workloads.logit_chunks) and are resident in HBM before the timed
+region.
 
-One bench step = one pass of the whole hot path over that workload: state
-initialisation plus the 64 chunk calls. ``value`` is token-scores per second
-(T*B*K*(V+1) per step / step time). ``roofline`` describes the greedy
-short-call kernel (one launch per 16-step chunk): algorithmic bytes per launch
-over its mean duration, timed with HIP events around every launch of the
-timed region. ``whole_call`` times the same workload decoded by one call over
-all 1024 steps (the segmented kernel plus its boundary fix-up), for context.
-``cpu_baseline`` times the CPU oracle on the whole workload over a process
-pool (decode only).
+One bench step = one pass of the whole hot path over the workload: state
+initialisation plus the workload's calls (64 calls of 16 steps for streaming,
+one call of T steps for the others), states carried between calls. ``value``
+is token-scores per second (T*B*K*(V+1) per step / step time). ``roofline``
+describes the workload's step kernel: algorithmic bytes per launch over its
+mean duration, timed with HIP events around every launch of the timed region
+on the launch stream. For streaming, ``whole_call`` times the same workload
+decoded by one call over all 1024 steps (the segmented kernel plus its
+boundary fix-up), for context. ``cpu_baseline`` times the CPU oracle over a
+process pool on a bounded sample of the same workload (decode only).
+
+Other workloads (--workload): batched, beam, stress_greedy, stress_beam, each
+in its own launch pattern, for context; stress_beam prepares 4.3 GB of
+logits on the host first (about two minutes).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                       [--copy-probe]
+                       [--copy-probe] [--workload NAME]
 """
 
 from __future__ import annotations
@@ -35,13 +41,29 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-WORKLOAD = "streaming"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_chunk_streaming_traffic.json")
+
+KERNELS = {
+    "streaming": "greedy short-call kernel (one launch per 16-step chunk)",
+    "batched": "segmented greedy kernel + boundary fix-up (one call of 500 steps)",
+    "beam": "beam kernel, one workgroup per stream (one call of 256 steps)",
+    "stress_greedy": "reference greedy kernel, one workgroup per stream (one call of 256 steps)",
+    "stress_beam": "reference beam kernel, one workgroup per stream (one call of 256 steps)",
+}
+
+# CPU oracle sample per workload: (streams, steps); None = all
+CPU_SAMPLE = {
+    "streaming": (None, None),
+    "batched": (None, None),
+    "beam": (32, None),
+    "stress_greedy": (64, 64),
+    "stress_beam": (32, 16),
+}
 
 
 def _cpu_worker(args):
-    """Oracle greedy decode of some streams; returns (rows, seconds of decode)."""
-    name, streams = args
+    """Oracle decode of some streams over steps [0, t1); returns (rows, seconds of decode)."""
+    name, streams, t1 = args
     import oracle
     import workloads as W
     cfg = W.config_by_name(name)
@@ -49,32 +71,42 @@ def _cpu_worker(args):
     lists = W.phrases(cfg, streams)
     graphs = {i: oracle.build_graph(l, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
               for i, l in enumerate(lists)}
-    rows = W.logits(cfg, streams=streams)
+    rows = W.logits(cfg, 0, t1, streams=streams)
+    mids = list(range(len(streams)))
     t0 = time.perf_counter()
-    oracle.greedy_decode(graphs, list(range(len(streams))), rows,
-                         np.zeros(len(streams), np.int32))
-    return rows.shape[0] * rows.shape[1], time.perf_counter() - t0
+    if cfg.K == 1:
+        oracle.greedy_decode(graphs, mids, rows, np.zeros(len(streams), np.int32))
+    else:
+        st, S = oracle.init_carry(mids, cfg.K)
+        oracle.beam_decode(graphs, mids, rows, st, S)
+    return rows.shape[0] * rows.shape[1] * rows.shape[2], time.perf_counter() - t0
 
 
 def cpu_baseline(cfg):
-    """The CPU oracle on every stream of the workload, one process per core."""
+    """The CPU oracle on a sample of the workload, one process per core."""
     import multiprocessing as mp
-    cores = min(len(os.sched_getaffinity(0)), 16, cfg.B)
-    streams = list(range(cfg.B))
+    n_streams, n_steps = CPU_SAMPLE[cfg.name]
+    n_streams = cfg.B if n_streams is None else min(n_streams, cfg.B)
+    t1 = cfg.T if n_steps is None else min(n_steps, cfg.T)
+    cores = min(len(os.sched_getaffinity(0)), 16, n_streams)
+    streams = list(range(n_streams))
     parts = [streams[i::cores] for i in range(cores)]
     ctx = mp.get_context("spawn")
     with ctx.Pool(cores) as pool:
-        res = pool.map(_cpu_worker, [(cfg.name, p) for p in parts if p])
+        res = pool.map(_cpu_worker, [(cfg.name, p, t1) for p in parts if p])
     rows = sum(r for r, _ in res)
     secs = max(s for _, s in res)
+    whole = n_streams == cfg.B and t1 == cfg.T
+    what = "the whole workload" if whole else "a sample of the workload"
     return {
         "value": rows * cfg.Vp1 / secs,
         "unit": "token-scores/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": f"the whole workload: all {cfg.B} streams x {cfg.T} steps ({rows} rows), "
-                  f"streams split over {cores} processes; decode time only (graph "
-                  f"building and logit generation untimed); wall = slowest process",
+        "sample": f"{what}: {n_streams} of {cfg.B} streams x {t1} of {cfg.T} steps "
+                  f"({rows} rows of {cfg.Vp1} logits), streams split over {cores} processes; "
+                  f"decode time only (graph building and logit generation untimed); "
+                  f"wall = slowest process",
         "seconds": secs,
     }
 
@@ -87,6 +119,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run one plain 256 MiB device copy (counter calibration)")
+    ap.add_argument("--workload", default="streaming", choices=sorted(KERNELS))
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the "
@@ -111,30 +144,47 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    cfg = W.config_by_name(WORKLOAD)
-    T, B, V1, chunk = cfg.T, cfg.B, cfg.Vp1, cfg.chunk
+    cfg = W.config_by_name(args.workload)
+    T, B, K, V1, chunk = cfg.T, cfg.B, cfg.K, cfg.Vp1, cfg.chunk
+    item = 4 if cfg.dtype == "f32" else 2
     lists = W.phrases(cfg)
     t0 = time.perf_counter()
     dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
     compile_s = time.perf_counter() - t0
-    logits = torch.empty((T, B, V1), dtype=torch.float32, device="cuda")
-    for ta, tb, rows in W.logit_chunks(cfg, 64):
-        logits[ta:tb].copy_(torch.from_numpy(rows[:, :, 0, :]).cuda())
-    mids, states, _ = dec.start(W.model_ids(cfg))
-    tok = torch.empty((T, B), dtype=torch.int32, device="cuda")
-    sst = torch.empty_like(tok)
-    sc = torch.empty((T, B), dtype=torch.float32, device="cuda")
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    logits = torch.empty((T, B, K, V1), dtype=dt, device="cuda")
+    for ta, tb, rows in W.logit_chunks(cfg, 16):
+        h = torch.from_numpy(rows if cfg.dtype == "f32" else rows.view(np.int16))
+        logits[ta:tb].copy_(h.cuda().view(dt))
+        del h, rows
+    mids, states, scores = dec.start(W.model_ids(cfg), K)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+    if K == 1:
+        rows_dev = logits[:, :, 0, :]
+        outs = (torch.empty((T, B), **i32), torch.empty((T, B), **i32),
+                torch.empty((T, B), **f32))
+    else:
+        rows_dev = logits
+        outs = tuple(torch.empty((T, B, K), **i32) for _ in range(3)) + \
+            tuple(torch.empty((T, B, K), **f32) for _ in range(2))
     n_launch = (T + chunk - 1) // chunk
     stream = torch.cuda.current_stream()
 
+    def call(ta, tb):
+        sl = tuple(o[ta:tb] for o in outs)
+        if K == 1:
+            capi.tb_boost_step_greedy(dec.arena, rows_dev[ta:tb], mids, states, *sl)
+        else:
+            capi.tb_boost_step_beam(dec.arena, rows_dev[ta:tb], mids, states, scores, *sl)
+
     def run_step(events=None):
-        capi.tb_init_states(dec.arena, B, 1, mids, states)
+        capi.tb_init_states(dec.arena, B, K, mids, states, scores)
         for i in range(n_launch):
             ta, tb = i * chunk, min(T, (i + 1) * chunk)
             if events is not None:
                 events[i][0].record(stream)
-            capi.tb_boost_step_greedy(dec.arena, logits[ta:tb], mids, states, tok[ta:tb],
-                                      sst[ta:tb], sc[ta:tb])
+            call(ta, tb)
             if events is not None:
                 events[i][1].record(stream)
 
@@ -151,30 +201,18 @@ def main() -> int:
     wall = time.perf_counter() - t0
     launch_ms = [a.elapsed_time(b) for step in ev for (a, b) in step]
     avg_launch_s = float(np.mean(launch_ms)) / 1e3
-    chunked = (tok.clone(), sst.clone(), sc.clone())
+    kept = tuple(o.clone() for o in outs)
 
     step_s = wall / args.steps
-    token_scores = T * B * cfg.K * V1
-    # algorithmic bytes per launch: the chunk's logit rows read once, 12 B of
-    # outputs per row, and per stream the model id, the carried state read
-    # and the carried state written
-    alg_bytes = chunk * B * (V1 * 4 + 12) + B * 12
+    token_scores = T * B * K * V1
+    # algorithmic bytes per launch: the call's logit rows read once, the
+    # outputs of every row (token, state, score; beam also parent and
+    # cumulative score), and per stream the model id plus the carried states
+    # (and beam scores) read and written
+    out_b = 12 if K == 1 else 20
+    carry_b = 4 + K * (8 if K == 1 else 16)
+    alg_bytes = chunk * B * K * (V1 * item + out_b) + B * carry_b
     achieved = alg_bytes / avg_launch_s / 1e9
-
-    # context: the same workload as one call over all T steps
-    whole_ms = []
-    for rep in range(4):
-        capi.tb_init_states(dec.arena, B, 1, mids, states)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        capi.tb_boost_step_greedy(dec.arena, logits, mids, states, tok, sst, sc)
-        b.record(stream)
-        torch.cuda.synchronize()
-        if rep > 0:
-            whole_ms.append(a.elapsed_time(b))
-    whole_s = float(np.median(whole_ms)) / 1e3
-    whole_bytes = T * B * (V1 * 4 + 12) + B * 12
-    same = all(torch.equal(x, y) for x, y in zip(chunked[:2], (tok, sst)))
 
     result = {
         "metric": "boosted decode token-scores/s (B x K x (V+1) per step) with achieved HBM GB/s",
@@ -187,25 +225,45 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": "streaming greedy boosted decode, 64 calls of 16 steps",
-                   "B": B, "K": 1, "V": cfg.V, "T": T, "chunk": chunk,
-                   "logits": "fp32 N(0,1), blank +1.5", "phrases_per_stream": cfg.n_phrases,
-                   "launches_per_step": n_launch},
+        "config": {"workload": f"{cfg.name}: {'greedy' if K == 1 else f'beam K={K}'} boosted decode, "
+                               f"{n_launch} call{'s' if n_launch > 1 else ''} of {chunk} steps",
+                   "B": B, "K": K, "V": cfg.V, "T": T, "chunk": chunk,
+                   "logits": f"{cfg.dtype} N(0,{cfg.logit_std:g})"
+                             + (f", blank +{cfg.blank_offset:g}" if cfg.blank_offset else ""),
+                   "phrases_per_stream": cfg.n_phrases, "launches_per_step": n_launch},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": profiling.load_traffic(TRAFFIC_FILE),
-                     "kernel": "greedy short-call kernel (one launch per 16-step chunk)",
+                     "traffic": (profiling.load_traffic(TRAFFIC_FILE)
+                                 if cfg.name == "streaming" else None),
+                     "kernel": KERNELS[cfg.name],
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_us": avg_launch_s * 1e6},
         "steps_per_s": T / step_s,
-        "whole_call": {"ms": whole_s * 1e3, "token_scores_per_s": token_scores / whole_s,
-                       "achieved_GBps": whole_bytes / whole_s / 1e9,
-                       "frac": whole_bytes / whole_s / 1e9 / HBM_PEAK_GBS,
-                       "kernels": "segmented greedy kernel + boundary fix-up",
-                       "outputs_equal_chunked": bool(same)},
         "compile_s": compile_s,
     }
+
+    if cfg.name == "streaming":
+        # context: the same workload as one call over all T steps
+        whole_ms = []
+        for rep in range(4):
+            capi.tb_init_states(dec.arena, B, 1, mids, states)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            call(0, T)
+            b.record(stream)
+            torch.cuda.synchronize()
+            if rep > 0:
+                whole_ms.append(a.elapsed_time(b))
+        whole_s = float(np.median(whole_ms)) / 1e3
+        whole_bytes = T * B * (V1 * item + out_b) + B * carry_b
+        same = all(torch.equal(x, y) for x, y in zip(kept[:2], outs[:2]))
+        result["whole_call"] = {"ms": whole_s * 1e3, "token_scores_per_s": token_scores / whole_s,
+                                "achieved_GBps": whole_bytes / whole_s / 1e9,
+                                "frac": whole_bytes / whole_s / 1e9 / HBM_PEAK_GBS,
+                                "kernels": "segmented greedy kernel + boundary fix-up",
+                                "outputs_equal_chunked": bool(same)}
+    del logits, rows_dev
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(result), flush=True)
