@@ -169,7 +169,8 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
 
 namespace {
 // TBIAS_GREEDY_KERNEL selects a kernel for testing: "ref" (one workgroup per
-// stream, any V), "pipe" (pipelined), anything else the segmented kernel.
+// stream, any V), "pipe" (pipelined), anything else the segmented kernels
+// (waves as segments for V+1 <= 2048, workgroups as segments above).
 int greedy_kernel_choice() {
   const char* e = std::getenv("TBIAS_GREEDY_KERNEL");
   if (e && std::strcmp(e, "ref") == 0) return 0;
@@ -190,6 +191,10 @@ hipError_t launch_greedy(const ArenaView& A, const void* logits, int32_t dtype, 
                                            out_tok, out_state, out_score, st);
     if (e != hipErrorNotSupported) return e;
     (void)hipGetLastError();  // clear the sticky "not supported" before the fallback
+    e = launch_greedy_wide(A, logits, dtype, T, B, row_stride, model_ids, states, out_tok,
+                           out_state, out_score, st);
+    if (e != hipErrorNotSupported) return e;
+    (void)hipGetLastError();
   }
   const size_t lds = (size_t)6 * (A.V1 - 1) + 4;
   if (dtype == TB_F32) {

@@ -35,6 +35,13 @@ hipError_t launch_greedy_seg(const ArenaView& A, const void* logits, int32_t dty
                              int32_t* states, int32_t* out_tok, int32_t* out_state,
                              float* out_score, hipStream_t st);
 
+// Segmented greedy kernel for wide vocabularies (V+1 > 2048, one workgroup
+// per segment); hipErrorNotSupported outside its range.
+hipError_t launch_greedy_wide(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                              int32_t B, int64_t row_stride, const int32_t* model_ids,
+                              int32_t* states, int32_t* out_tok, int32_t* out_state,
+                              float* out_score, hipStream_t st);
+
 // Largest V+1 the step kernels accept (LDS tables are sized by it).
 constexpr int32_t kMaxV1 = 10241;
 

@@ -392,3 +392,62 @@ def test_beam_inside_long_phrases(kernel, monkeypatch):
     ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
     compare_beam(gpu, ref, range(B), ATOL)
     assert np.max(ref[2]) >= 20
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_wide_vocabulary_mixed_streams_and_chunks(dtype, monkeypatch):
+    """Wide rows (V+1 = 3001, not a multiple of 256): the workgroup-segmented
+    kernel against the oracle with model -1, an empty list and an
+    out-of-range id, for whole calls (several segments per stream and the
+    boundary fix-up) and chunked calls; tokens, states and carries equal the
+    reference kernel's."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg = W.Config(107, "small", B=7, K=1, V=3000, T=96, chunk=96, dtype=dtype, n_phrases=200,
+                   len_lo=1, len_hi=6, token_dist="zipf", zipf_s=1.1, logit_std=1.0,
+                   blank_offset=1.0, n_case=300)
+    lists = W.phrases(cfg)
+    rows = W.logits(cfg)
+    lists = list(lists[:5]) + [[]]
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, -1, 5, 3, 99, 4, 1], np.int32)
+    dev = to_device_logits(rows[:, :, 0, :])
+    ok = [0, 1, 2, 3, 5, 6]
+    graphs = oracle_graphs(cfg, lists, ok, mids)
+    st0 = np.array([0, -1, 0, 0, 0, 0, 0], np.int32)
+    ref = oracle.greedy_decode(graphs, mids, rows, st0, streams=ok)
+    outs = {}
+    for chunk in (96, 37, 7, 1):
+        say(f"[wide] {dtype} chunk={chunk}")
+        gpu = gpu_greedy(dec, dev, mids, chunk)
+        compare_greedy(gpu, ref, ok, ATOL)
+        assert np.array_equal(gpu[3][ok], ref[3][ok])
+        assert np.all(gpu[1][:, 1] == -1) and np.all(gpu[1][:, 4] == -2)
+        assert np.all(gpu[1][:, 2] == 0)
+        z = oracle.widen(rows[:, 4, 0, :])
+        assert np.array_equal(gpu[0][:, 4], np.argmax(z, axis=1))
+        outs[chunk] = gpu
+    monkeypatch.setenv("TBIAS_GREEDY_KERNEL", "ref")
+    r = gpu_greedy(dec, dev, mids, 96)
+    assert np.array_equal(outs[96][0], r[0]) and np.array_equal(outs[96][1], r[1])
+    assert np.array_equal(outs[96][3], r[3])
+
+
+def test_wide_vocabulary_segments_inside_long_phrases():
+    """Wide rows whose boosted path stays inside a 40-token phrase: every
+    guessed segment start is wrong, so the boundary fix-up recomputes across
+    whole segments."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V, B, T = 2600, 3, 400
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    phrase = list(range(1, 41))
+    lists = [[phrase], [phrase, list(range(5, 30))], [list(range(1, 11))]]
+    rows = _phrase_following_rows(np.random.default_rng(17), T, B, V, 40)
+    mids = np.array([0, 1, 2], np.int32)
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    say("[wide] long phrases")
+    gpu = gpu_greedy(dec, to_device_logits(rows), mids, T)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    ref = oracle.greedy_decode(graphs, mids, rows[:, :, None, :], np.zeros(B, np.int32))
+    compare_greedy(gpu, ref, range(B), ATOL)
+    assert np.array_equal(gpu[3], ref[3])
+    assert np.max(ref[1][:, 0]) >= 30
