@@ -47,8 +47,9 @@ KERNELS = {
     "streaming": "greedy short-call kernel (one launch per 16-step chunk)",
     "batched": "segmented greedy kernel + boundary fix-up (one call of 500 steps)",
     "beam": "beam kernel, one workgroup per stream (one call of 256 steps)",
-    "stress_greedy": "reference greedy kernel, one workgroup per stream (one call of 256 steps)",
-    "stress_beam": "reference beam kernel, one workgroup per stream (one call of 256 steps)",
+    "stress_greedy": "wide-row greedy kernel, one workgroup per time segment, + boundary fix-up "
+                     "(one call of 256 steps)",
+    "stress_beam": "wide-row beam kernel, one workgroup per stream (one call of 256 steps)",
 }
 
 # CPU oracle sample per workload: (streams, steps); None = all

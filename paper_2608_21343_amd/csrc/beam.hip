@@ -14,6 +14,7 @@
 #include <cstring>
 
 #include "beam_fast.hpp"
+#include "beam_wide.hpp"
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -277,8 +278,9 @@ void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int3
 }  // namespace
 
 // The one-wave-per-hypothesis kernel serves K <= 8, V+1 <= 2048 and arenas
-// whose override sets fit its lists; TBIAS_BEAM_KERNEL=ref selects the
-// reference kernel (used to test both paths).
+// whose override sets fit its lists; the wide-row kernel serves K <= 8 and
+// V+1 in (2048, 256 * 41]; TBIAS_BEAM_KERNEL=ref selects the reference
+// kernel (used to test every path).
 hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, int32_t T, int32_t B,
                        int32_t K, int64_t row_stride, const int32_t* model_ids, int32_t* states,
                        float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
@@ -292,6 +294,16 @@ hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, in
                           : per <= 16 ? beamk::beam_launcher_9_16(per, maxk, dtype)
                           : per <= 24 ? beamk::beam_launcher_17_24(per, maxk, dtype)
                                       : beamk::beam_launcher_25_32(per, maxk, dtype);
+    if (f)
+      return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
+               out_state, out_step, out_cum, st);
+  }
+  if (!ref && K <= 8 && A.V1 > 64 * 32 && A.V1 <= wide::kThreads * 41 &&
+      wide::lds_bytes(A) <= 60 * 1024) {
+    const int tpv = (A.V1 + wide::kThreads - 1) / wide::kThreads;
+    const int maxk = K <= 4 ? 4 : 8;
+    wide::BeamWideLaunch f = dtype == TB_F32 ? wide::beam_wide_launcher_f32(tpv, maxk)
+                                             : wide::beam_wide_launcher_bf16(tpv, maxk);
     if (f)
       return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
                out_state, out_step, out_cum, st);

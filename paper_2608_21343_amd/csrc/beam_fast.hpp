@@ -94,35 +94,6 @@ __device__ __forceinline__ int32_t wave_excl_scan(int32_t v, int32_t& total) {
   return x - v;
 }
 
-// e^x for x <= 0 in float64 (x = -inf and x < -745 give 0): e^x = 2^k e^r with
-// k = rint(x / ln 2) and r = x - k ln 2, ln 2 split in a high part with
-// trailing zero bits (k * ln2_hi is exact for |k| < 2^11) and a low part
-// (Cody and Waite's reduction); e^r is summed as its Taylor series to degree
-// 12, whose truncation error for |r| <= ln(2)/2 is below 2e-16 relative.
-__device__ __forceinline__ double exp_nonpos(double x) {
-  const double kInvLn2 = 1.4426950408889634074;
-  const double kLn2Hi = 6.93147180369123816490e-01;
-  const double kLn2Lo = 1.90821492927058770002e-10;
-  const bool tiny = !(x >= -745.0);
-  x = tiny ? -745.0 : x;  // keeps k finite; the result is selected below
-  const double k = __builtin_rint(x * kInvLn2);
-  const double r = __builtin_fma(-k, kLn2Lo, __builtin_fma(-k, kLn2Hi, x));
-  double p = 1.0 / 479001600.0;  // 1/12!
-  p = __builtin_fma(p, r, 1.0 / 39916800.0);
-  p = __builtin_fma(p, r, 1.0 / 3628800.0);
-  p = __builtin_fma(p, r, 1.0 / 362880.0);
-  p = __builtin_fma(p, r, 1.0 / 40320.0);
-  p = __builtin_fma(p, r, 1.0 / 5040.0);
-  p = __builtin_fma(p, r, 1.0 / 720.0);
-  p = __builtin_fma(p, r, 1.0 / 120.0);
-  p = __builtin_fma(p, r, 1.0 / 24.0);
-  p = __builtin_fma(p, r, 1.0 / 6.0);
-  p = __builtin_fma(p, r, 0.5);
-  p = __builtin_fma(p, r, 1.0);
-  p = __builtin_fma(p, r, 1.0);
-  return tiny ? 0.0 : __builtin_ldexp(p, (int)k);
-}
-
 // (value, flat index) order of the selection: larger value, then lower index.
 __device__ __forceinline__ bool cbetter(float a, int32_t fa, float b, int32_t fb) {
   return a > b || (a == b && fa < fb);

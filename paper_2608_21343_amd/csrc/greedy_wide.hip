@@ -21,74 +21,14 @@
 // greedy_wide_fix_kernel then repairs the segment boundaries in order from the
 // exact state, recomputing until the trajectory meets the stored one. The
 // outputs equal sequential decoding for any input.
-#include <climits>
-
-#include "device.hpp"
 #include "launch.hpp"
+#include "wide.hpp"
 
 namespace tbias {
 namespace wide {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
 constexpr int kWarm = 2;     // warm-up rows of a guessed segment start
 constexpr int kMinSeg = 16;  // shortest segment worth a workgroup
-constexpr float kNegInf = -__builtin_huge_valf();
-
-// Read-only load through the scalar cache (uniform address).
-template <class T>
-__device__ __forceinline__ T sld(const T* p) {
-  return *(const __attribute__((address_space(4))) T*)(p);
-}
-
-// The workgroup's view of one stream: arena, model and the LDS tables.
-struct Ctx {
-  const ArenaView* A;
-  int32_t off;           // first global state of the model
-  int mode;              // 1 biased, 0 model -1, -1 invalid model or state
-  int32_t fixed;         // state written for unbiased streams
-  int32_t cap;           // override list capacity
-  uint32_t* omark;       // [V]: tag << 16 | list slot of an overridden class
-  int32_t* olist_y;      // [cap] target state of an override
-  float* olist_psi;      // [cap] its psi
-  int32_t* nlist;        // list fill counter
-  uint32_t tag;
-};
-
-// Per-thread registers of its tokens v = tid + 256 j. The blank and the
-// positions past the row have root psi -inf, so they never win as tokens; the
-// blank is scored on its own (zb, held by the thread that owns it).
-template <int TPV>
-struct Own {
-  float z[TPV];
-  float zb;           // the blank's logit (thread (V mod 256) only)
-  int32_t cls[TPV];   // class of v (-1: none, blank or past the row)
-  float rps[TPV];     // psi of v's root move (0 when unbiased; -inf: blank, past the row)
-  int32_t rds[TPV];   // target of v's root move (the fixed state when unbiased)
-};
-
-// The row length passes through an empty asm each time it is used, so that
-// the compiler keeps the per-slot bounds tests where they are used instead of
-// hoisting 2*TPV lane masks out of the row loop (they would not fit in SGPRs).
-__device__ __forceinline__ int32_t opaque(int32_t x) {
-  asm volatile("" : "+s"(x));
-  return x;
-}
-
-template <class Ld, int TPV>
-__device__ __forceinline__ void load_row(float (&z)[TPV], float& zb, const typename Ld::T* row,
-                                         int32_t V1x) {
-  const int32_t V1 = opaque(V1x);
-  const int32_t V = V1 - 1;
-#pragma unroll
-  for (int j = 0; j < TPV; ++j) {
-    const int32_t v = (int32_t)threadIdx.x + kThreads * j;
-    z[j] = (v < V1) ? Ld::get(row, v) : kNegInf;
-  }
-  // the blank lies in this thread's slot V / 256 when the thread owns it
-  zb = ((int32_t)threadIdx.x == V % kThreads) ? Ld::get(row, V) : kNegInf;
-}
-
 struct Red {
   float k, z, psi, m, s;
   int32_t v, ns;
@@ -115,43 +55,10 @@ __device__ __forceinline__ void merge(Red& a, const Red& b) {
 // every thread. Contains workgroup barriers: all threads must call it.
 template <int TPV>
 __device__ __forceinline__ Red step(Ctx& C, const Own<TPV>& o, int32_t s, int32_t V1, Red* red) {
-  const ArenaView& A = *C.A;
   const int32_t V = V1 - 1;
   const int tid = threadIdx.x;
-  float phi_s = 0.f;
-  bool chain = false;
-  if (C.mode == 1) {
-    phi_s = sld(A.phi + C.off + s);
-    if (s != 0) {
-      chain = true;
-      if (++C.tag == 65536u) {  // uniform: clear the tags and restart
-        for (int32_t c = tid; c < V; c += kThreads) C.omark[c] = 0u;
-        C.tag = 1u;
-      }
-      if (tid == 0) *C.nlist = 0;
-      __syncthreads();
-      for (int32_t x = s; x != 0;) {
-        const int32_t fc = sld(A.first_child + C.off + x);
-        const int32_t nc = sld(A.n_child + C.off + x);
-        const int32_t lk = sld(A.link + C.off + x);
-        for (int32_t j = tid; j < nc; j += kThreads) {
-          const int32_t y = fc + j;
-          const int32_t c = A.label[C.off + y];
-          // a class already listed by a deeper chain state keeps that move
-          if ((C.omark[c] >> 16) != C.tag) {
-            const int32_t slot = atomicAdd(C.nlist, 1);
-            if (slot < C.cap) {
-              C.olist_y[slot] = y;
-              C.olist_psi[slot] = A.psi[C.off + y];
-              C.omark[c] = (C.tag << 16) | (uint32_t)slot;
-            }
-          }
-        }
-        __syncthreads();
-        x = lk;
-      }
-    }
-  }
+  float phi_s;
+  const bool chain = build_overrides(C, s, phi_s);
 
   float bk = kNegInf, bpsi = 0.f, bz = 0.f;
   int32_t bv = INT_MAX, bns = 0;
@@ -161,7 +68,7 @@ __device__ __forceinline__ Red step(Ctx& C, const Own<TPV>& o, int32_t s, int32_
   float se = 0.f;  // the blank's logit is also in its slot of o.z: counted once there
 #pragma unroll
   for (int j = 0; j < TPV; ++j) se += (o.z[j] == kNegInf) ? 0.f : __expf(o.z[j] - m);
-  auto offer = [&](int j, float p, int32_t ns) {
+  for_each_move<TPV>(C, o, chain, [&](int j, float p, int32_t ns) {
     const float key = o.z[j] + p;
     const bool gt = key > bk;  // tokens ascend: strict > keeps the lowest index on ties
     bk = gt ? key : bk;
@@ -169,41 +76,7 @@ __device__ __forceinline__ Red step(Ctx& C, const Own<TPV>& o, int32_t s, int32_
     bns = gt ? ns : bns;
     bpsi = gt ? p : bpsi;
     bz = gt ? o.z[j] : bz;
-  };
-  if (chain) {
-    // overridden classes: tag reads for 8 tokens, then their list entries
-    // (slot 0 when not overridden), one wait each
-    constexpr int kG = 8;
-#pragma unroll
-    for (int g0 = 0; g0 < TPV; g0 += kG) {
-      uint32_t e[kG];
-#pragma unroll
-      for (int i = 0; i < kG; ++i)
-        if (g0 + i < TPV) e[i] = C.omark[o.cls[g0 + i] > 0 ? o.cls[g0 + i] : 0];
-      float po[kG];
-      int32_t yo[kG];
-#pragma unroll
-      for (int i = 0; i < kG; ++i) {
-        if (g0 + i < TPV) {
-          const bool ov = o.cls[g0 + i] >= 0 && (e[i] >> 16) == C.tag;
-          const int32_t slot = ov ? (int32_t)(e[i] & 0xffffu) : 0;
-          po[i] = C.olist_psi[slot];
-          yo[i] = C.olist_y[slot];
-          e[i] = ov ? 1u : 0u;
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < kG; ++i) {
-        if (g0 + i < TPV) {
-          const int j = g0 + i;
-          offer(j, e[i] ? po[i] : o.rps[j], e[i] ? yo[i] : o.rds[j]);
-        }
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < TPV; ++j) offer(j, o.rps[j], o.rds[j]);
-  }
+  });
   if (tid == V % kThreads) {  // the blank keeps the state; phi[s] in its key, no boost
     const float key = o.zb + phi_s;
     if (better(key, V, bk, bv)) {
@@ -233,44 +106,10 @@ __device__ __forceinline__ Red step(Ctx& C, const Own<TPV>& o, int32_t s, int32_
   return f;
 }
 
-template <int TPV>
-__device__ __forceinline__ void own_tables(Own<TPV>& o, const ArenaView& A, int32_t m, int mode,
-                                           int32_t fixed) {
-  const int32_t V1 = A.V1, V = V1 - 1;
-  const float* gpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
-  const int32_t* gdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
-#pragma unroll
-  for (int j = 0; j < TPV; ++j) {
-    const int32_t v = (int32_t)threadIdx.x + kThreads * j;
-    const bool tok = v < V;
-    o.cls[j] = tok ? A.class_map[v] : -1;
-    o.rps[j] = tok ? (mode == 1 ? gpsi[v] : 0.f) : kNegInf;
-    o.rds[j] = (mode == 1) ? (tok ? gdst[v] : 0) : fixed;
-  }
-}
-
 struct Shared {
   Red red[kWaves];
   int32_t nlist;
 };
-
-__device__ __forceinline__ Ctx make_ctx(const ArenaView& A, int32_t off, int mode, Shared& sh,
-                                        unsigned char* dyn) {
-  const int32_t V = A.V1 - 1;
-  Ctx C;
-  C.A = &A;
-  C.off = off;
-  C.mode = mode;
-  C.fixed = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
-  C.cap = A.max_override > 0 ? A.max_override : 1;
-  C.omark = reinterpret_cast<uint32_t*>(dyn);
-  C.olist_y = reinterpret_cast<int32_t*>(dyn + 4 * (size_t)V);
-  C.olist_psi = reinterpret_cast<float*>(dyn + 4 * (size_t)V + 4 * (size_t)C.cap);
-  C.nlist = &sh.nlist;
-  C.tag = 0u;
-  for (int32_t c = threadIdx.x; c < V; c += kThreads) C.omark[c] = 0u;
-  return C;
-}
 
 template <class Ld, int TPV>
 __global__ __launch_bounds__(kThreads) void greedy_wide_kernel(
@@ -298,7 +137,7 @@ __global__ __launch_bounds__(kThreads) void greedy_wide_kernel(
   float zn[TPV], zbn = kNegInf;
   if (t0 < t1) load_row<Ld, TPV>(o.z, o.zb, col + (int64_t)tw * tstride, V1);
   own_tables<TPV>(o, A, m, mode, (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID);
-  Ctx C = make_ctx(A, off, mode, sh, dyn);
+  Ctx C = make_ctx(A, off, mode, &sh.nlist, dyn);
   __syncthreads();
 
   int32_t s = (mode == 1) ? (g == 0 ? s0 : 0) : C.fixed;
@@ -345,7 +184,7 @@ __global__ __launch_bounds__(kThreads) void greedy_wide_fix_kernel(
     Own<TPV> o;
     float zn[TPV], zbn = kNegInf;
     own_tables<TPV>(o, A, m, 1, 0);
-    Ctx C = make_ctx(A, off, 1, sh, dyn);
+    Ctx C = make_ctx(A, off, 1, &sh.nlist, dyn);
     __syncthreads();
     for (int32_t gg = 1; gg < G; ++gg) {
       const int32_t tb0 = gg * L;
@@ -400,9 +239,7 @@ hipError_t launch_t(const ArenaView& A, const void* logits, int32_t T, int32_t B
                     const int32_t* model_ids, int32_t* states, int32_t* out_tok,
                     int32_t* out_state, float* out_score, hipStream_t st) {
   typedef typename Ld::T TT;
-  const int32_t V = A.V1 - 1;
-  const int32_t cap = A.max_override > 0 ? A.max_override : 1;
-  const size_t lds = 4 * (size_t)V + 8 * (size_t)cap;
+  const size_t lds = lds_bytes(A);
   int32_t G, L;
   wide_geometry(T, B, G, L);
   hipLaunchKernelGGL((greedy_wide_kernel<Ld, TPV>), dim3(B * G), dim3(kThreads), lds, st, A,
@@ -425,9 +262,8 @@ hipError_t launch_greedy_wide(const ArenaView& A, const void* logits, int32_t dt
                               int32_t* states, int32_t* out_tok, int32_t* out_state,
                               float* out_score, hipStream_t st) {
   const int32_t V1 = A.V1;
-  const int32_t cap = A.max_override > 0 ? A.max_override : 1;
   if (V1 <= 2048 || V1 > wide::kThreads * 41) return hipErrorNotSupported;
-  if (4 * (size_t)(V1 - 1) + 8 * (size_t)cap > 60 * 1024) return hipErrorNotSupported;
+  if (wide::lds_bytes(A) > 60 * 1024) return hipErrorNotSupported;
   const int tpv = (V1 + wide::kThreads - 1) / wide::kThreads;
 #define TB_WIDE(N)                                                                           \
   if (tpv <= N)                                                                              \

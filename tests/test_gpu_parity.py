@@ -451,3 +451,39 @@ def test_wide_vocabulary_segments_inside_long_phrases():
     compare_greedy(gpu, ref, range(B), ATOL)
     assert np.array_equal(gpu[3], ref[3])
     assert np.max(ref[1][:, 0]) >= 30
+
+
+@pytest.mark.parametrize("K,dtype", [(3, "f32"), (8, "bf16")])
+def test_wide_vocabulary_beam_mixed_streams(K, dtype, monkeypatch):
+    """The wide-row beam kernel (V+1 = 3001) against the oracle: model -1, an
+    empty list and an out-of-range id (decoded unbiased, states -2), chunked
+    calls equal one call, and the reference kernel agrees."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg = W.Config(108, "small", B=6, K=K, V=3000, T=40, chunk=40, dtype=dtype, n_phrases=200,
+                   len_lo=1, len_hi=6, token_dist="zipf", zipf_s=1.1, logit_std=1.5,
+                   blank_offset=0.0, n_case=300)
+    lists = list(W.phrases(cfg)[:4]) + [[]]
+    rows = W.logits(cfg)
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, -1, 4, 2, 99, 3], np.int32)
+    dev = to_device_logits(rows)
+    say(f"[wide-beam] K={K} {dtype}")
+    gpu = gpu_beam(dec, dev, mids, 40)
+    ok = [0, 1, 2, 3, 5]
+    mm = np.where(mids == 99, -1, mids)
+    graphs = oracle_graphs(cfg, lists, ok, mids)
+    st0, S0 = oracle.init_carry(mm, K)
+    st0[mids == 99] = 0
+    ref = oracle.beam_decode(graphs, mm, rows, st0, S0)
+    compare_beam(gpu, ref, ok, ATOL)
+    for i in (0, 1, 4):
+        assert np.array_equal(gpu[i][:, 4], ref[i][:, 4]), i
+    assert np.all(gpu[2][:, 4] == -2)
+    for ch in (7, 16):
+        out = gpu_beam(dec, dev, mids, ch)
+        for a, b in zip(gpu, out):
+            assert np.array_equal(a, b), f"chunk {ch} differs"
+    monkeypatch.setenv("TBIAS_BEAM_KERNEL", "ref")
+    r = gpu_beam(dec, dev, mids, 40)
+    for i in range(5):
+        assert np.array_equal(gpu[i], r[i]) if i != 3 else np.max(np.abs(gpu[3] - r[3])) <= 1e-6
