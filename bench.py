@@ -154,10 +154,14 @@ def main() -> int:
     compile_s = time.perf_counter() - t0
     dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
     logits = torch.empty((T, B, K, V1), dtype=dt, device="cuda")
+    t0 = time.perf_counter()
     for ta, tb, rows in W.logit_chunks(cfg, 16):
         h = torch.from_numpy(rows if cfg.dtype == "f32" else rows.view(np.int16))
         logits[ta:tb].copy_(h.cuda().view(dt))
         del h, rows
+        if time.perf_counter() - t0 > 20:  # progress of long preparations (stderr)
+            print(f"bench: logits up to step {tb} of {T} on the device", file=sys.stderr, flush=True)
+            t0 = time.perf_counter()
     mids, states, scores = dec.start(W.model_ids(cfg), K)
     i32 = dict(dtype=torch.int32, device="cuda")
     f32 = dict(dtype=torch.float32, device="cuda")
