@@ -16,8 +16,12 @@ describes the workload's step kernel: algorithmic bytes per launch over its
 mean duration, timed with HIP events around every launch of the timed region
 on the launch stream. For streaming, ``whole_call`` times the same workload
 decoded by one call over all 1024 steps (the segmented kernel plus its
-boundary fix-up), for context. ``cpu_baseline`` times the CPU oracle over a
-process pool on a bounded sample of the same workload (decode only).
+boundary fix-up), for context. ``read_probe`` times a plain read of the same
+logit bytes, for context. Workloads whose logits are smaller than 512 MiB get
+replicated buffers, one per bench step in turn, so that the last-level cache
+does not hold a step's input. ``cpu_baseline`` times the CPU oracle over a
+process pool on a bounded sample of the same workload (decode only), with a
+single-process figure beside it.
 
 Other workloads (--workload): batched, beam, stress_greedy, stress_beam, each
 in its own launch pattern, for context; stress_beam prepares 4.3 GB of
@@ -41,6 +45,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+ROTATE_BYTES = 512 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_chunk_streaming_traffic.json")
 
 KERNELS = {
@@ -99,6 +104,9 @@ def cpu_baseline(cfg):
     secs = max(s for _, s in res)
     whole = n_streams == cfg.B and t1 == cfg.T
     what = "the whole workload" if whole else "a sample of the workload"
+    # one process on the streams of the first part, for the single-core rate
+    with ctx.Pool(1) as pool:
+        rows1, secs1 = pool.map(_cpu_worker, [(cfg.name, parts[0], t1)])[0]
     return {
         "value": rows * cfg.Vp1 / secs,
         "unit": "token-scores/s",
@@ -109,6 +117,8 @@ def cpu_baseline(cfg):
                   f"decode time only (graph building and logit generation untimed); "
                   f"wall = slowest process",
         "seconds": secs,
+        "single_thread": {"value": rows1 * cfg.Vp1 / secs1, "seconds": secs1,
+                          "sample": f"{len(parts[0])} streams x {t1} steps in one process"},
     }
 
 
@@ -162,34 +172,42 @@ def main() -> int:
         if time.perf_counter() - t0 > 20:  # progress of long preparations (stderr)
             print(f"bench: logits up to step {tb} of {T} on the device", file=sys.stderr, flush=True)
             t0 = time.perf_counter()
+    # Logits smaller than the 256 MB last-level cache are replicated so that
+    # consecutive bench steps read different buffers (at least 512 MiB apart).
+    n_buf = max(1, -(-ROTATE_BYTES // (logits.numel() * item)))
+    bufs = [logits] + [logits.clone() for _ in range(n_buf - 1)]
     mids, states, scores = dec.start(W.model_ids(cfg), K)
     i32 = dict(dtype=torch.int32, device="cuda")
     f32 = dict(dtype=torch.float32, device="cuda")
     if K == 1:
-        rows_dev = logits[:, :, 0, :]
+        rows_bufs = [x[:, :, 0, :] for x in bufs]
         outs = (torch.empty((T, B), **i32), torch.empty((T, B), **i32),
                 torch.empty((T, B), **f32))
     else:
-        rows_dev = logits
+        rows_bufs = bufs
         outs = tuple(torch.empty((T, B, K), **i32) for _ in range(3)) + \
             tuple(torch.empty((T, B, K), **f32) for _ in range(2))
     n_launch = (T + chunk - 1) // chunk
     stream = torch.cuda.current_stream()
 
-    def call(ta, tb):
+    def call(ta, tb, rows_dev):
         sl = tuple(o[ta:tb] for o in outs)
         if K == 1:
             capi.tb_boost_step_greedy(dec.arena, rows_dev[ta:tb], mids, states, *sl)
         else:
             capi.tb_boost_step_beam(dec.arena, rows_dev[ta:tb], mids, states, scores, *sl)
 
+    n_run = [0]
+
     def run_step(events=None):
+        rows_dev = rows_bufs[n_run[0] % n_buf]
+        n_run[0] += 1
         capi.tb_init_states(dec.arena, B, K, mids, states, scores)
         for i in range(n_launch):
             ta, tb = i * chunk, min(T, (i + 1) * chunk)
             if events is not None:
                 events[i][0].record(stream)
-            call(ta, tb)
+            call(ta, tb, rows_dev)
             if events is not None:
                 events[i][1].record(stream)
 
@@ -246,7 +264,24 @@ def main() -> int:
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_us": avg_launch_s * 1e6},
         "steps_per_s": T / step_s,
         "compile_s": compile_s,
+        "rotated_buffers": n_buf,
     }
+
+    # context: a plain read of the same logit bytes (torch's max reduction)
+    probe_ms = []
+    for rep in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        x = bufs[rep % n_buf]
+        a.record(stream)
+        torch.amax(x)
+        b.record(stream)
+        torch.cuda.synchronize()
+        if rep > 0:
+            probe_ms.append(a.elapsed_time(b))
+    probe_s = float(np.median(probe_ms)) / 1e3
+    result["read_probe"] = {"GBps": logits.numel() * item / probe_s / 1e9,
+                            "bytes": logits.numel() * item,
+                            "what": "torch.amax over the workload's logits, median of 3"}
 
     if cfg.name == "streaming":
         # context: the same workload as one call over all T steps
@@ -255,7 +290,7 @@ def main() -> int:
             capi.tb_init_states(dec.arena, B, 1, mids, states)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            call(0, T)
+            call(0, T, rows_bufs[0])
             b.record(stream)
             torch.cuda.synchronize()
             if rep > 0:
@@ -268,7 +303,7 @@ def main() -> int:
                                 "frac": whole_bytes / whole_s / 1e9 / HBM_PEAK_GBS,
                                 "kernels": "segmented greedy kernel + boundary fix-up",
                                 "outputs_equal_chunked": bool(same)}
-    del logits, rows_dev
+    del logits, bufs, rows_bufs
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(result), flush=True)
