@@ -14,6 +14,7 @@
 #include <cstring>
 
 #include "beam_fast.hpp"
+#include "beam_pipe.hpp"
 #include "beam_wide.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -277,16 +278,27 @@ void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int3
 
 }  // namespace
 
-// The one-wave-per-hypothesis kernel serves K <= 8, V+1 <= 2048 and arenas
-// whose override sets fit its lists; the wide-row kernel serves K <= 8 and
-// V+1 in (2048, 256 * 41]; TBIAS_BEAM_KERNEL=ref selects the reference
-// kernel (used to test every path).
+// The kernel with helper waves serves K <= 8 where a two-slot ring of rows
+// fits in LDS (V+1 <= 1088 for float32 and K > 4, up to 8256 for bfloat16 and
+// K <= 4); then the one-wave-per-hypothesis kernel (K <= 8, V+1 <= 2048,
+// override sets that fit its lists) and the wide-row kernel (K <= 8, V+1 in
+// (2048, 256 * 41]); the reference kernel serves the rest.
+// TBIAS_BEAM_KERNEL=ref selects the reference kernel and =nopipe skips the
+// helper-wave kernel (used to test every path).
 hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, int32_t T, int32_t B,
                        int32_t K, int64_t row_stride, const int32_t* model_ids, int32_t* states,
                        float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
                        float* out_step, float* out_cum, hipStream_t st) {
   const char* e = std::getenv("TBIAS_BEAM_KERNEL");
   const bool ref = e && std::strcmp(e, "ref") == 0;
+  const bool nopipe = e && std::strcmp(e, "nopipe") == 0;
+  if (!ref && !nopipe && K <= 8) {
+    bpipe::PipeLaunch f = dtype == TB_F32 ? bpipe::pipe_launcher_f32(A.V1, K)
+                                          : bpipe::pipe_launcher_bf16(A.V1, K);
+    if (f)
+      return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
+               out_state, out_step, out_cum, st);
+  }
   if (!ref && K <= 8 && A.V1 >= 2 && A.V1 <= 64 * 32 && A.max_override <= beamk::kOverCap) {
     const int per = (A.V1 + 63) / 64;
     const int maxk = K <= 2 ? 2 : (K <= 4 ? 4 : 8);

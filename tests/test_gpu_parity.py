@@ -340,14 +340,17 @@ def test_chunk_loop_graph_replay_matches_eager():
             assert torch.equal(a, b), f"replay {rep} differs from the eager run"
 
 
-@pytest.mark.parametrize("kernel", ["fast", "ref"])
+BEAM_KERNEL_ENV = {"default": None, "wide": "nopipe", "ref": "ref"}
+
+
+@pytest.mark.parametrize("kernel", ["default", "ref"])
 @pytest.mark.parametrize("K,dtype", [(2, "f32"), (3, "bf16"), (8, "f32")])
 def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, monkeypatch):
-    """Both beam kernels against the oracle: ragged V+1 = 301, model -1, an
+    """Every beam kernel against the oracle: ragged V+1 = 301, model -1, an
     empty list and an out-of-range id (decoded unbiased, states -2)."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if kernel == "ref":
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", "ref")
+    if BEAM_KERNEL_ENV[kernel]:
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
     cfg, lists, rows = _small_case(6, B=6, V=300, K=K, T=40, dtype=dtype)
     lists = list(lists[:4]) + [[]]
     dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
@@ -367,13 +370,13 @@ def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, monkeypatc
     assert np.all(gpu[2][:, 4] == -2)
 
 
-@pytest.mark.parametrize("kernel", ["fast", "ref"])
+@pytest.mark.parametrize("kernel", ["default", "ref"])
 def test_beam_inside_long_phrases(kernel, monkeypatch):
     """Beam hypotheses deep inside 40-token phrases (chains of several suffix
     states, override sets of dozens of classes)."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if kernel == "ref":
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", "ref")
+    if BEAM_KERNEL_ENV[kernel]:
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
     V, B, T, K = 64, 4, 200, 4
     cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
     phrase = list(range(1, 41))
@@ -453,12 +456,15 @@ def test_wide_vocabulary_segments_inside_long_phrases():
     assert np.max(ref[1][:, 0]) >= 30
 
 
-@pytest.mark.parametrize("K,dtype", [(3, "f32"), (8, "bf16")])
-def test_wide_vocabulary_beam_mixed_streams(K, dtype, monkeypatch):
-    """The wide-row beam kernel (V+1 = 3001) against the oracle: model -1, an
+@pytest.mark.parametrize("kernel", ["default", "wide"])
+@pytest.mark.parametrize("K,dtype", [(3, "f32"), (4, "bf16"), (8, "bf16")])
+def test_wide_vocabulary_beam_mixed_streams(kernel, K, dtype, monkeypatch):
+    """Beam kernels on wide rows (V+1 = 3001) against the oracle: model -1, an
     empty list and an out-of-range id (decoded unbiased, states -2), chunked
     calls equal one call, and the reference kernel agrees."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    if BEAM_KERNEL_ENV[kernel]:
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
     cfg = W.Config(108, "small", B=6, K=K, V=3000, T=40, chunk=40, dtype=dtype, n_phrases=200,
                    len_lo=1, len_hi=6, token_dist="zipf", zipf_s=1.1, logit_std=1.5,
                    blank_offset=0.0, n_case=300)
@@ -487,3 +493,59 @@ def test_wide_vocabulary_beam_mixed_streams(K, dtype, monkeypatch):
     r = gpu_beam(dec, dev, mids, 40)
     for i in range(5):
         assert np.array_equal(gpu[i], r[i]) if i != 3 else np.max(np.abs(gpu[3] - r[3])) <= 1e-6
+
+
+@pytest.mark.parametrize("kernel", ["default", "ref"])
+@pytest.mark.parametrize("K", [1, 4, 7])
+def test_beam_tiny_vocabulary(kernel, K, monkeypatch):
+    """V+1 = 8 with K up to 7: fewer root moves than a row list holds, most
+    candidates of a step in the K best, ties between equal logits."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    if BEAM_KERNEL_ENV[kernel]:
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    V, B, T = 7, 3, 30
+    cm = np.array([0, 0, 2, 3, 3, 5, 6, -1], np.int32)
+    lists = [[[0, 2], [3, 5, 6], [2]], [[6, 6, 6]], []]
+    rng = np.random.default_rng(21)
+    rows = np.round(rng.normal(0, 1, (T, B, K, V + 1)) * 2) / 2  # many equal logits
+    rows = np.ascontiguousarray(rows.astype(np.float32))
+    mids = np.array([0, 1, 2], np.int32)
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    say(f"[beam-{kernel}] tiny vocabulary K={K}")
+    gpu = gpu_beam(dec, to_device_logits(rows), mids, 11)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    st0, S0 = oracle.init_carry(mids, K)
+    ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+    compare_beam(gpu, ref, range(B), ATOL)
+
+
+@pytest.mark.parametrize("kernel", ["default", "wide"])
+@pytest.mark.parametrize("K,dtype", [(4, "bf16"), (2, "f32")])
+def test_wide_vocabulary_beam_inside_long_phrases(kernel, K, dtype, monkeypatch):
+    """Wide rows (V+1 = 2601) with hypotheses deep inside 40-token phrases
+    whose tokens have the largest logits: most of a row's listed root moves
+    are overridden, so the helper-wave kernel rescans rows too."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    if BEAM_KERNEL_ENV[kernel]:
+        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    V, B, T = 2600, 4, 120
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    phrase = list(range(1, 41))
+    lists = [[phrase, list(range(3, 20)), [5, 6, 7, 8]], [phrase, list(range(10, 50))],
+             [list(range(1, 11)), [2, 3], [4, 5, 6]], [phrase]]
+    base = _phrase_following_rows(np.random.default_rng(19), T, B, V, 40)
+    rng = np.random.default_rng(20)
+    rows = np.repeat(base[:, :, None, :], K, axis=2) + rng.normal(0, 0.3, (T, B, K, V + 1))
+    rows = np.ascontiguousarray(rows.astype(np.float32))
+    if dtype == "bf16":  # bfloat16 bits, rounded to nearest even
+        from workloads.synth import _f32_to_bf16_bits
+        rows = _f32_to_bf16_bits(rows)
+    mids = np.arange(B, dtype=np.int32)
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    say(f"[beam-{kernel}] wide long phrases K={K} {dtype}")
+    gpu = gpu_beam(dec, to_device_logits(rows), mids, 50)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    st0, S0 = oracle.init_carry(mids, K)
+    ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+    compare_beam(gpu, ref, range(B), ATOL)
+    assert np.max(ref[2]) >= 20
