@@ -13,8 +13,9 @@ initialisation plus the workload's calls (64 calls of 16 steps for streaming,
 one call of T steps for the others), states carried between calls. ``value``
 is token-scores per second (T*B*K*(V+1) per step / step time). ``roofline``
 describes the workload's step kernel: algorithmic bytes per launch over its
-mean duration, timed with HIP events around every launch of the timed region
-on the launch stream. For streaming, ``whole_call`` times the same workload
+mean duration, from HIP events on the launch stream around each step's calls
+in the timed region (their time over the number of calls, gaps between
+launches included). For streaming, ``whole_call`` times the same workload
 decoded by one call over all 1024 steps (the segmented kernel plus its
 boundary fix-up), for context. ``read_probe`` times a plain read of the same
 logit bytes, for context. Workloads whose logits are smaller than 512 MiB get
@@ -203,26 +204,30 @@ def main() -> int:
         rows_dev = rows_bufs[n_run[0] % n_buf]
         n_run[0] += 1
         capi.tb_init_states(dec.arena, B, K, mids, states, scores)
+        if events is not None:
+            events[0].record(stream)
         for i in range(n_launch):
             ta, tb = i * chunk, min(T, (i + 1) * chunk)
-            if events is not None:
-                events[i][0].record(stream)
             call(ta, tb, rows_dev)
-            if events is not None:
-                events[i][1].record(stream)
+        if events is not None:
+            events[1].record(stream)
 
     for _ in range(args.warmup):
         run_step()
     torch.cuda.synchronize()
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(n_launch)] for _ in range(args.steps)]
+    # one event pair per step around its calls: events between the calls of a
+    # step would add their own cost to the timed region (about a fifth of the
+    # streaming step), so the mean launch time is the bracketed calls over
+    # their number, gaps between launches included
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
         run_step(ev[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    launch_ms = [a.elapsed_time(b) for step in ev for (a, b) in step]
+    launch_ms = [a.elapsed_time(b) / n_launch for (a, b) in ev]
     avg_launch_s = float(np.mean(launch_ms)) / 1e3
     kept = tuple(o.clone() for o in outs)
 
