@@ -608,6 +608,144 @@ __device__ __forceinline__ Answer eval_general(const SGraph& G, const Tables<PER
   return a;
 }
 
+// The step from state x given the first children and child counts of its
+// suffix chain (x first, levels non-root states, kChainMax at most): up to
+// 128 children, two per lane (slot i in lane i, slot 64 + i in lane i's
+// second register), provided the children of every level but the shallowest
+// fit in the first 64 slots (the shadowing scan reads them by readlane).
+// Returns false, with no output, on any other shape.
+constexpr int kChainMax = 8;
+
+template <int PER>
+__device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PER>& tb,
+                                                const float* zrow, uint32_t* marks,
+                                                const RowShape<PER>& rs, int32_t x, float phi_x,
+                                                const int32_t (&fl)[kChainMax],
+                                                const int32_t (&nl)[kChainMax], int32_t levels,
+                                                const RowSum& r, const LaneTop* top, int32_t V,
+                                                Answer& a) {
+  constexpr int kLv = kChainMax;
+  const int lane = __lane_id();
+  int32_t st[kLv + 1];  // first slot of every level
+  st[0] = 0;
+#pragma unroll
+  for (int i = 0; i < kLv; ++i) st[i + 1] = st[i] + nl[i];
+  const int32_t total = st[kLv];
+  int32_t last = 0;  // first slot of the shallowest level
+#pragma unroll
+  for (int i = 1; i < kLv; ++i) last = (i < levels) ? st[i] : last;
+  if (total > 128 || last > 64) return false;
+
+  // a slot's child: its level, state record and best member
+  auto slot = [&](int32_t q, int32_t& lv, int32_t& y, int32_t& lab, float& py, float& kb,
+                  float& zb, int32_t& tk, bool& in, bool& bad) {
+    in = q < total;
+    // level and child index without indexing the level arrays (they stay in
+    // scalar registers): y = q + (fl[lv] - st[lv]), summed level by level
+    lv = 0;
+    int32_t yy = q + fl[0];
+#pragma unroll
+    for (int i = 1; i < kLv; ++i) {
+      const bool past = q >= st[i];
+      lv += past ? 1 : 0;
+      yy += past ? (fl[i] - st[i]) - (fl[i - 1] - st[i - 1]) : 0;
+    }
+    y = in ? yy : 0;
+    uint32_t c0 = 0u, c1 = 0u, c2 = 0x80000000u;
+    if (in && y < G.nhot) {
+      c0 = G.w0[y];
+      c1 = G.w1[y];
+      c2 = G.w2[y];
+    }
+    const int32_t mc = (int32_t)(c2 & 0xffu);
+    bad = in && ((c2 >> 31) != 0u || mc > 3);
+    lab = (int32_t)((c2 >> 16) & 0x7fffu);
+    const int32_t ms = in ? (int32_t)(c1 >> 16) : 0;
+    py = G.vpsi[c0 >> 24];
+    const int32_t t0 = tb.cls_tok[ms];
+    const int32_t t1 = tb.cls_tok[ms + (mc > 1 ? 1 : 0)];
+    const int32_t t2 = tb.cls_tok[ms + (mc > 2 ? 2 : (mc > 1 ? 1 : 0))];
+    const float z0 = zrow[t0], z1 = zrow[t1], z2 = zrow[t2];
+    kb = z0 + py;
+    zb = z0;
+    tk = t0;
+    const float k1 = z1 + py, k2 = z2 + py;
+    if (k1 > kb) { kb = k1; tk = t1; zb = z1; }  // members ascend: ties keep the lower
+    if (k2 > kb) { kb = k2; tk = t2; zb = z2; }
+  };
+  int32_t lvA, yA, labA, tkA, lvB, yB, labB, tkB;
+  float pyA, kA, zA, pyB, kB, zB;
+  bool inA, inB, badA, badB;
+  slot(lane, lvA, yA, labA, pyA, kA, zA, tkA, inA, badA);
+  slot(64 + lane, lvB, yB, labB, pyB, kB, zB, tkB, inB, badB);
+  if (__ballot(badA || badB) != 0ull) return false;
+  // a class that a deeper chain state (a lower level) also has is shadowed;
+  // the deeper levels' slots are all below 64 (lane = slot)
+  bool takeA = inA, takeB = inB;
+  for (int32_t j = 0; j < last; ++j) {
+    const int32_t cj = __builtin_amdgcn_readlane(labA, j);
+    const int32_t lvj = __builtin_amdgcn_readlane(lvA, j);
+    takeA = takeA && !(lvj < lvA && cj == labA);
+    takeB = takeB && !(lvj < lvB && cj == labB);
+  }
+  // this lane's better candidate, then the wave's
+  const float kAt = takeA ? kA : kNegInf, kBt = takeB ? kB : kNegInf;
+  const int32_t tAt = takeA ? tkA : INT_MAX, tBt = takeB ? tkB : INT_MAX;
+  const bool useB = better(kBt, tBt, kAt, tAt);
+  const float kL = useB ? kBt : kAt;
+  const int32_t tL = useB ? tBt : tAt;
+  float ok = kNegInf, o_psi = 0.f, o_z = 0.f;
+  int32_t ot = INT_MAX, o_ns = 0;
+  if (__ballot(takeA || takeB) != 0ull) {
+    const int32_t wl = wave_argmax_dpp(kL, tL, ok, ot);
+    o_ns = rl(useB ? yB : yA, wl);
+    o_psi = rlf(useB ? pyB : pyA, wl);
+    o_z = rlf(useB ? zB : zA, wl);
+  }
+  const bool over = __ballot((takeA && labA == r.r1_cls) || (takeB && labB == r.r1_cls)) != 0ull;
+  if (over) {
+    marks_clear<PER>(marks);
+    if (takeA) mark(marks, labA);
+    if (takeB) mark(marks, labB);
+    marks_fence();
+  }
+
+  // best root move whose class is not overridden
+  float rk = r.ymax;
+  int32_t rt = r.r1_tok, r_ns = r.r1_dst;
+  float r_psi = r.r1_psi, r_z = r.r1_z;
+  if (over) {
+    if (!(top && root_excluding<PER>(tb, zrow, marks, *top, rk, rt)))
+      root_scan<PER>(tb, zrow, marks, rs, rk, rt);
+    const int32_t rv = (rt < V) ? rt : 0;
+    r_ns = tb.rdst[rv];
+    r_psi = tb.rpsi[rv];
+    r_z = zrow[rv];
+  }
+  a.tok = V;
+  a.ns = x;
+  a.b = 0.f;
+  a.zv = r.zb;
+  float bk = r.zb + phi_x;  // blank keeps the state
+  int32_t bt = V;
+  if (better(ok, ot, bk, bt)) {
+    bk = ok;
+    bt = ot;
+    a.tok = ot;
+    a.ns = o_ns;
+    a.b = o_psi - phi_x;
+    a.zv = o_z;
+  }
+  if (better(rk, rt, bk, bt)) {
+    a.tok = rt;
+    a.ns = r_ns;
+    a.b = r_psi - phi_x;
+    a.zv = r_z;
+  }
+  return true;
+}
+
+
 // The step from state x from the packed state records in LDS. The children of
 // the states on x's suffix chain (x, link(x), ... up to four non-root states,
 // at most 64 children in all) are the override candidates, one per lane; a
@@ -642,7 +780,11 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
     }
   }
   const int32_t s1 = n0, s2 = s1 + n1, s3 = s2 + n2, total = s3 + n3;
-  if (total > 64) return false;
+  if (total > 64) {  // more children than lanes: two per lane
+    const int32_t fl[kChainMax] = {f0, f1, f2, f3, 0, 0, 0, 0};
+    const int32_t nl[kChainMax] = {n0, n1, n2, n3, 0, 0, 0, 0};
+    return eval_chain_wide<PER>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top, V, a);
+  }
 
   // best override candidate (none when the chain has no children)
   float ok = kNegInf, o_psi = 0.f, o_z = 0.f;
@@ -733,6 +875,37 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
   return true;
 }
 
+// eval_walk for chains of up to kChainMax non-root states (and the child
+// sets of eval_chain_wide). Returns false, with no output, on any other shape.
+template <int PER>
+__device__ __forceinline__ bool eval_walk2(const SGraph& G, const Tables<PER>& tb,
+                                           const float* zrow, uint32_t* marks,
+                                           const RowShape<PER>& rs, int32_t x, const RowSum& r,
+                                           const LaneTop* top, int32_t V, Answer& a) {
+  constexpr int kLv = kChainMax;
+  int32_t fc, nc, lnk;
+  float phi_x;
+  if (x == 0 || !G.srec(x, fc, nc, lnk, phi_x)) return false;
+  int32_t fl[kLv], nl[kLv];
+  fl[0] = fc;
+  nl[0] = nc;
+  int32_t levels = 1;
+#pragma unroll
+  for (int i = 1; i < kLv; ++i) {
+    fl[i] = 0;
+    nl[i] = 0;
+    if (lnk != 0) {
+      float phi_unused;
+      if (!G.srec(lnk, fc, nc, lnk, phi_unused)) return false;
+      fl[i] = fc;
+      nl[i] = nc;
+      ++levels;
+    }
+  }
+  if (lnk != 0) return false;
+  return eval_chain_wide<PER>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top, V, a);
+}
+
 // The boosted step from state x: from the LDS records when they apply, else
 // the general path.
 template <int PER>
@@ -742,6 +915,7 @@ __device__ __forceinline__ Answer eval_state(const SGraph& G, const Tables<PER>&
                                              const LaneTop* top, int32_t V) {
   Answer a;
   if (eval_walk<PER>(G, tb, zrow, marks, rs, x, r, top, V, a)) return a;
+  if (eval_walk2<PER>(G, tb, zrow, marks, rs, x, r, top, V, a)) return a;
   return eval_general<PER>(G, tb, zrow, marks, rs, x, r, top, V);
 }
 
@@ -855,6 +1029,76 @@ __device__ __forceinline__ void fill_tables(Tables<PER>& tb, const ArenaView& A,
       tb.cls_ptr[i] = (i < V1) ? (uint16_t)A.cls_ptr[i] : (uint16_t)0;
       tb.cls_tok[i] = (i < V) ? (uint16_t)A.cls_tok[i] : (uint16_t)0;
     }
+  }
+}
+
+// The LDS tables of fill_tables and fill_state_hot in two halves: the loads
+// into registers, then the stores. A kernel issues the loads before its
+// logit rows, so that the stores (loads complete in issue order) wait for the
+// tables only, not for the rows coming from HBM.
+template <int PER, int NT, int HOT>
+struct FillRegs {
+  static constexpr int KT = (64 * PER + NT - 1) / NT;
+  static constexpr int KH = (HOT + NT - 1) / NT;
+  float rpsi[KT];
+  int32_t rdst[KT], cls[KT], cptr[KT], ctok[KT];
+  uint32_t w0[KH], w1[KH], w2[KH];
+  float vt;
+};
+
+template <int PER, int NT, int HOT>
+__device__ __forceinline__ void fill_gather(FillRegs<PER, NT, HOT>& f, const ArenaView& A,
+                                            int32_t m, int mode, int32_t off, int32_t nhot) {
+  const int32_t V1 = A.V1, V = V1 - 1;
+  const float* gpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
+  const int32_t* gdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
+#pragma unroll
+  for (int k = 0; k < f.KT; ++k) {
+    const int32_t i = k * NT + (int32_t)threadIdx.x;
+    f.rpsi[k] = (i < V) ? (mode == 1 ? gpsi[i] : 0.f) : kNegInf;
+    f.rdst[k] = (i < V && mode == 1) ? gdst[i] : 0;
+    f.cls[k] = (i < V1) ? A.class_map[i] : -1;
+    f.cptr[k] = (i < V1) ? A.cls_ptr[i] : 0;
+    f.ctok[k] = (i < V) ? A.cls_tok[i] : 0;
+  }
+  const uint32_t* src = A.state_rec + 3 * (int64_t)off;
+#pragma unroll
+  for (int k = 0; k < f.KH; ++k) {
+    const int32_t i = k * NT + (int32_t)threadIdx.x;
+    const bool in = i < nhot;
+    f.w0[k] = in ? src[3 * i] : 0u;
+    f.w1[k] = in ? src[3 * i + 1] : 0u;
+    f.w2[k] = in ? src[3 * i + 2] : 0u;
+  }
+  f.vt = (nhot > 0 && threadIdx.x < 512) ? A.value_tab[512 * (int64_t)m + threadIdx.x] : 0.f;
+}
+
+template <int PER, int NT, int HOT>
+__device__ __forceinline__ void fill_scatter(const FillRegs<PER, NT, HOT>& f, Tables<PER>& tb,
+                                             StateHot<HOT>& h, int32_t nhot) {
+#pragma unroll
+  for (int k = 0; k < f.KT; ++k) {
+    const int32_t i = k * NT + (int32_t)threadIdx.x;
+    if (i < 64 * PER) {
+      tb.rpsi[i] = f.rpsi[k];
+      tb.rdst[i] = f.rdst[k];
+      tb.cls[i] = f.cls[k] < 0 ? (uint16_t)0xffff : (uint16_t)f.cls[k];
+      tb.cls_ptr[i] = (uint16_t)f.cptr[k];
+      tb.cls_tok[i] = (uint16_t)f.ctok[k];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < f.KH; ++k) {
+    const int32_t i = k * NT + (int32_t)threadIdx.x;
+    if (i < nhot) {
+      h.w0[i] = f.w0[k];
+      h.w1[i] = f.w1[k];
+      h.w2[i] = f.w2[k];
+    }
+  }
+  if (nhot > 0 && threadIdx.x < 512) {
+    if (threadIdx.x < 256) h.vpsi[threadIdx.x] = f.vt;
+    else h.vphi[threadIdx.x - 256] = f.vt;
   }
 }
 
@@ -1187,12 +1431,14 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   const int mode = resolve_stream(A, m, s0, off, n);
   const RowShape<PER> rs(V1);
   const bool own = w < T;  // this wave has a row
+  const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
+  // the tables' loads, then the row's, then the tables' stores
+  FillRegs<PER, NT, HOT> fr;
+  fill_gather<PER, NT, HOT>(fr, A, m, mode, off, nhot);
+  asm volatile("" ::: "memory");
   float raw[PER];
   if (own) load_row<Ld, PER>(raw, col + (int64_t)w * tstride, rs);
-
-  fill_tables<PER, NT>(S.tab, A, m, mode);
-  const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
-  fill_state_hot<HOT, NT>(S.hot, A, m, off, nhot);
+  fill_scatter<PER, NT, HOT>(fr, S.tab, S.hot, nhot);
   __syncthreads();
 
   RowSum r = {};
