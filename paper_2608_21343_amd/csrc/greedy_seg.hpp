@@ -679,34 +679,43 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
   slot(lane, lvA, yA, labA, pyA, kA, zA, tkA, inA, badA);
   slot(64 + lane, lvB, yB, labB, pyB, kB, zB, tkB, inB, badB);
   if (__ballot(badA || badB) != 0ull) return false;
-  // a class that a deeper chain state (a lower level) also has is shadowed;
-  // the deeper levels' slots are all below 64 (lane = slot)
-  bool takeA = inA, takeB = inB;
-  for (int32_t j = 0; j < last; ++j) {
-    const int32_t cj = __builtin_amdgcn_readlane(labA, j);
-    const int32_t lvj = __builtin_amdgcn_readlane(lvA, j);
-    takeA = takeA && !(lvj < lvA && cj == labA);
-    takeB = takeB && !(lvj < lvB && cj == labB);
-  }
-  // this lane's better candidate, then the wave's
-  const float kAt = takeA ? kA : kNegInf, kBt = takeB ? kB : kNegInf;
-  const int32_t tAt = takeA ? tkA : INT_MAX, tBt = takeB ? tkB : INT_MAX;
-  const bool useB = better(kBt, tBt, kAt, tAt);
-  const float kL = useB ? kBt : kAt;
-  const int32_t tL = useB ? tBt : tAt;
+  // A class that a deeper chain state (a lower level) also has is shadowed;
+  // the deeper levels' slots are all below 64 (lane = slot). The best of all
+  // children is the answer unless it is shadowed (a shadowing child has the
+  // same tokens; see eval_walk), which is checked on the winner alone.
+  auto best = [&](bool tA, bool tB, int32_t& wl, bool& useB, float& ok, int32_t& ot) {
+    const float kAt = tA ? kA : kNegInf, kBt = tB ? kB : kNegInf;
+    const int32_t tAt = tA ? tkA : INT_MAX, tBt = tB ? tkB : INT_MAX;
+    useB = better(kBt, tBt, kAt, tAt);
+    wl = wave_argmax_dpp(useB ? kBt : kAt, useB ? tBt : tAt, ok, ot);
+  };
   float ok = kNegInf, o_psi = 0.f, o_z = 0.f;
-  int32_t ot = INT_MAX, o_ns = 0;
-  if (__ballot(takeA || takeB) != 0ull) {
-    const int32_t wl = wave_argmax_dpp(kL, tL, ok, ot);
-    o_ns = rl(useB ? yB : yA, wl);
-    o_psi = rlf(useB ? pyB : pyA, wl);
-    o_z = rlf(useB ? zB : zA, wl);
+  int32_t ot = INT_MAX, wl;
+  bool useB;
+  best(inA, inB, wl, useB, ok, ot);
+  {
+    const bool wB = rl((int32_t)useB, wl) != 0;
+    const int32_t lw = rl(wB ? labB : labA, wl), vw = rl(wB ? lvB : lvA, wl);
+    if (__ballot((inA && labA == lw && lvA < vw) || (inB && labB == lw && lvB < vw)) != 0ull) {
+      bool takeA = inA, takeB = inB;
+      for (int32_t j = 0; j < last; ++j) {
+        const int32_t cj = __builtin_amdgcn_readlane(labA, j);
+        const int32_t lvj = __builtin_amdgcn_readlane(lvA, j);
+        takeA = takeA && !(lvj < lvA && cj == labA);
+        takeB = takeB && !(lvj < lvB && cj == labB);
+      }
+      best(takeA, takeB, wl, useB, ok, ot);
+    }
   }
-  const bool over = __ballot((takeA && labA == r.r1_cls) || (takeB && labB == r.r1_cls)) != 0ull;
+  const int32_t o_ns = rl(useB ? yB : yA, wl);
+  o_psi = rlf(useB ? pyB : pyA, wl);
+  o_z = rlf(useB ? zB : zA, wl);
+  // every chain child's class overrides its root move
+  const bool over = __ballot((inA && labA == r.r1_cls) || (inB && labB == r.r1_cls)) != 0ull;
   if (over) {
     marks_clear<PER>(marks);
-    if (takeA) mark(marks, labA);
-    if (takeB) mark(marks, labB);
+    if (inA) mark(marks, labA);
+    if (inB) mark(marks, labB);
     marks_fence();
   }
 
@@ -816,26 +825,34 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
     const float k1 = z1 + py, k2 = z2 + py;
     if (k1 > kb) { kb = k1; tk = t1; zb_ = z1; }  // members ascend: ties keep the lower
     if (k2 > kb) { kb = k2; tk = t2; zb_ = z2; }
-    bool take = in;
+    // A class that a deeper chain state (a lower level) also has is shadowed.
+    // The best of all children is the answer unless it is shadowed: a
+    // shadowing child has the same tokens, and among equal keys and tokens
+    // the lowest lane (the deepest level) wins the argmax. Only a shadowed
+    // winner needs the class-by-class resolution.
+    int32_t wl = wave_argmax_dpp(in ? kb : kNegInf, in ? tk : INT_MAX, ok, ot);
     if (levels > 1) {
-      // a class that a deeper chain state (a lower level) also has is shadowed
-      const int32_t last = levels == 2 ? s1 : (levels == 3 ? s2 : s3);
-      for (int32_t j = 0; j < last; ++j) {
-        const int32_t cj = __builtin_amdgcn_readlane(lab, j);
-        const int32_t lvj = (j >= s1) + (j >= s2) + (j >= s3);
-        take = take && !(lvj < lv && cj == lab);
+      const int32_t lw = rl(lab, wl), vw = rl(lv, wl);
+      if (__ballot(in && lab == lw && lv < vw) != 0ull) {
+        const int32_t last = levels == 2 ? s1 : (levels == 3 ? s2 : s3);
+        bool take = in;
+        for (int32_t j = 0; j < last; ++j) {
+          const int32_t cj = __builtin_amdgcn_readlane(lab, j);
+          const int32_t lvj = (j >= s1) + (j >= s2) + (j >= s3);
+          take = take && !(lvj < lv && cj == lab);
+        }
+        wl = wave_argmax_dpp(take ? kb : kNegInf, take ? tk : INT_MAX, ok, ot);
       }
     }
-    if (__ballot(take) != 0ull) {
-      const int32_t wl = wave_argmax_dpp(take ? kb : kNegInf, take ? tk : INT_MAX, ok, ot);
-      o_ns = rl(y, wl);
-      o_psi = rlf(py, wl);
-      o_z = rlf(zb_, wl);
-    }
-    over = __ballot(take && lab == r.r1_cls) != 0ull;
+    o_ns = rl(y, wl);
+    o_psi = rlf(py, wl);
+    o_z = rlf(zb_, wl);
+    // every chain child's class overrides its root move (a shadowed class is
+    // also a deeper child's)
+    over = __ballot(in && lab == r.r1_cls) != 0ull;
     if (over) {
       marks_clear<PER>(marks);
-      if (take) mark(marks, lab);
+      if (in) mark(marks, lab);
       marks_fence();
     }
   }
@@ -1492,13 +1509,20 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     gx = S.spec_x[lane];
   }
   int32_t s = (mode == 1) ? s0 : fixed;
+  // the next row's summary and lane tops are read while this row is checked
+  RowSum rn = S.rsum[0];
+  uint32_t tn = S.ltop[0][lane];
   for (int32_t t = 0; t < T; ++t) {
+    const RowSum rt = rn;
+    const uint32_t tp = tn;
+    if (t + 1 < T) {
+      rn = S.rsum[t + 1];
+      tn = S.ltop[t + 1][lane];
+    }
     int32_t ns;
     if (rl(gx, t) == s) {
       ns = rl(ans.y, t);
     } else {
-      const RowSum rt = S.rsum[t];
-      const uint32_t tp = S.ltop[t][lane];
       const LaneTop tt = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16), 0.f, 0.f};
       const Answer e = step_from<PER>(Gr, S.tab, S.zbuf[t], S.marks[0], rs, rt, s, mode, V, &tt);
       if (lane == t) ans = make_int4(e.tok, e.ns, __float_as_int(e.b), __float_as_int(e.zv));

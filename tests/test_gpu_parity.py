@@ -295,6 +295,63 @@ def test_segments_longer_than_the_kept_trajectory():
     assert np.max(ref[1][:, 0]) >= 100
 
 
+def _shadow_case(extra):
+    """A list where a suffix-chain child that a deeper child shadows has the
+    larger psi: from state (1,1,2) the class-1 child (1,1,2,1) has psi 3 and
+    the class-1 child (1,2,1) of its link (1,2) has psi 4 (commit reading:
+    (1,1,2) is a phrase, so (1,1,2,1) holds 1 pending token; (1,2,1) holds 2).
+    ``extra`` more children of (1,2) make the chain wider than one wave.
+    Logits walk 1 1 2 1 9 blank, each stream out of phase."""
+    V, B, T = 128, 3, 600
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    lst = [[1], [1, 1, 2], [1, 1, 2, 1, 9], [1, 2, 1, 9]] + [[1, 2, 20 + i] for i in range(extra)]
+    rng = np.random.default_rng(3 + extra)
+    rows = rng.normal(0.0, 0.1, size=(T, B, V + 1)).astype(np.float32)
+    seq = [1, 1, 2, 1, 9, V]
+    for b in range(B):
+        for t in range(T):
+            rows[t, b, seq[(t + b) % len(seq)]] += 3.0
+    return V, B, T, cm, lst, rows
+
+
+@pytest.mark.parametrize("extra", [0, 80])
+@pytest.mark.parametrize("chunk", [16, 64, 600])
+def test_shadowed_child_with_the_larger_psi(extra, chunk):
+    """The best child over the whole suffix chain is a shadowed one: the step
+    must take the deeper child of the same class (greedy, narrow and wide
+    chains, short and long calls)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V, B, T, cm, lst, rows = _shadow_case(extra)
+    g = oracle.build_graph(lst, cm, token_w=1.0, end_bonus=2.0)
+    s112 = g.strings.index((1, 1, 2))
+    deep, shallow = g.goto[s112][1], g.goto[g.link[s112]][1]
+    assert g.psi64[shallow] > g.psi64[deep]
+    mids = np.zeros(B, np.int32)
+    dec = BoostDecoder([lst], cm, token_w=1.0, end_bonus=2.0)
+    say(f"[shadow] extra={extra} chunk={chunk}")
+    gpu = gpu_greedy(dec, to_device_logits(rows), mids, chunk)
+    ref = oracle.greedy_decode({0: g}, mids, rows, np.zeros(B, np.int32))
+    compare_greedy(gpu, ref, range(B), ATOL)
+    assert np.sum(ref[1] == deep) >= 100  # the case really occurs
+
+
+@pytest.mark.parametrize("extra", [0, 80])
+def test_shadowed_child_with_the_larger_psi_beam(extra):
+    """The same list and logits through the beam step (K = 3)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V, B, T, cm, lst, rows = _shadow_case(extra)
+    K = 3
+    rk = np.ascontiguousarray(np.repeat(rows[:, :, None, :], K, axis=2))
+    g = oracle.build_graph(lst, cm, token_w=1.0, end_bonus=2.0)
+    mids = np.zeros(B, np.int32)
+    dec = BoostDecoder([lst], cm, token_w=1.0, end_bonus=2.0)
+    say(f"[shadow] beam extra={extra}")
+    gpu = gpu_beam(dec, to_device_logits(rk), mids, 16)
+    st0, S0 = oracle.init_carry(mids, K)
+    ref = oracle.beam_decode({0: g}, mids, rk, st0, S0)
+    compare_beam(gpu, ref, range(B), ATOL)
+
+
 def test_chunk_loop_graph_replay_matches_eager():
     """The streaming chunk loop captured in a HIP graph: every replay (with
     eager work and synchronisation in between) reproduces the eager outputs."""
