@@ -710,8 +710,12 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
   const int32_t o_ns = rl(useB ? yB : yA, wl);
   o_psi = rlf(useB ? pyB : pyA, wl);
   o_z = rlf(useB ? zB : zA, wl);
-  // every chain child's class overrides its root move
-  const bool over = __ballot((inA && labA == r.r1_cls) || (inB && labB == r.r1_cls)) != 0ull;
+  // every chain child's class overrides its root move; the remaining root
+  // moves have keys at most r.ymax, so when the best child or the blank is
+  // above it no root move can win
+  const bool hit = __ballot((inA && labA == r.r1_cls) || (inB && labB == r.r1_cls)) != 0ull;
+  const bool root_lost = hit && (ok > r.ymax || r.zb + phi_x > r.ymax);
+  const bool over = hit && !root_lost;
   if (over) {
     marks_clear<PER>(marks);
     if (inA) mark(marks, labA);
@@ -720,7 +724,7 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
   }
 
   // best root move whose class is not overridden
-  float rk = r.ymax;
+  float rk = root_lost ? kNegInf : r.ymax;
   int32_t rt = r.r1_tok, r_ns = r.r1_dst;
   float r_psi = r.r1_psi, r_z = r.r1_z;
   if (over) {
@@ -798,7 +802,7 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
   // best override candidate (none when the chain has no children)
   float ok = kNegInf, o_psi = 0.f, o_z = 0.f;
   int32_t ot = INT_MAX, o_ns = 0;
-  bool over = false;
+  bool over = false, root_lost = false;
   if (total > 0) {
     const bool in = lane < total;
     const int32_t lv = (lane >= s1) + (lane >= s2) + (lane >= s3);
@@ -850,6 +854,12 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
     // every chain child's class overrides its root move (a shadowed class is
     // also a deeper child's)
     over = __ballot(in && lab == r.r1_cls) != 0ull;
+    // the remaining root moves have keys at most r.ymax: when the best child
+    // or the blank is above it, no root move can win
+    if (over && (ok > r.ymax || r.zb + phi_x > r.ymax)) {
+      over = false;
+      root_lost = true;
+    }
     if (over) {
       marks_clear<PER>(marks);
       if (in) mark(marks, lab);
@@ -858,7 +868,7 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
   }
 
   // best root move whose class is not overridden
-  float rk = r.ymax;
+  float rk = root_lost ? kNegInf : r.ymax;
   int32_t rt = r.r1_tok, r_ns = r.r1_dst;
   float r_psi = r.r1_psi, r_z = r.r1_z;
   if (over) {
