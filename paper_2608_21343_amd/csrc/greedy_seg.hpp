@@ -99,6 +99,7 @@ struct alignas(16) FixedLds {
   int32_t spec_ns[2][W];   // short calls: state after row w's step from its guess (by round)
   int32_t spec_x[W];       // short calls: row w's final guess and its answer
   int4 spec_ans[W];
+  float lse[W];            // short calls: normaliser of row w
   int32_t fin_state[W];    // exact state after each segment
   int32_t fin_ready[W];
   int32_t abort_flag;
@@ -946,6 +947,19 @@ __device__ __forceinline__ Answer eval_state(const SGraph& G, const Tables<PER>&
   return eval_general<PER>(G, tb, zrow, marks, rs, x, r, top, V);
 }
 
+// log(sum(exp(z))) of a row from this lane's elements and their maximum:
+// max over the wave, then the sum of exp2 terms over the wave.
+template <int PER>
+__device__ __forceinline__ float lse_of(const float* cur, float zmax) {
+  zmax = wave_max_dpp(zmax);
+  const float mL = zmax * kLog2e;
+  float se = 0.f;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) se += __builtin_amdgcn_exp2f(__builtin_fmaf(cur[j], kLog2e, -mL));
+  se = wave_sum_dpp(se);
+  return zmax + __logf(se);
+}
+
 // State-independent part of a step on a row held in registers (raw[j] as
 // loaded): copies the row to zrow (LDS) and summarises it. rp holds this
 // lane's root-move psi (-inf for blank and masked lanes).
@@ -989,7 +1003,6 @@ __device__ __forceinline__ RowSum row_summary(float* zrow, const Tables<PER>& tb
     top->k1 = yb;
     top->k2 = y2;
   }
-  zmax = wave_max_dpp(zmax);
   wave_argmax_dpp(yb, idx, r.ymax, r.r1_tok);
   if (r.r1_tok >= V) r.r1_tok = 0;  // only with -inf / nan logits: keep indices in range
   const int32_t c16 = tb.cls[r.r1_tok];
@@ -997,16 +1010,31 @@ __device__ __forceinline__ RowSum row_summary(float* zrow, const Tables<PER>& tb
   r.r1_dst = tb.rdst[r.r1_tok];
   r.r1_psi = tb.rpsi[r.r1_tok];
   r.r1_z = zrow[r.r1_tok];
-  r.lse = 0.f;
-  if (need_lse) {  // warm-up rows only need the state
-    const float mL = zmax * kLog2e;
-    float se = 0.f;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) se += __builtin_amdgcn_exp2f(__builtin_fmaf(cur[j], kLog2e, -mL));
-    se = wave_sum_dpp(se);
-    r.lse = zmax + __logf(se);
-  }
+  r.lse = need_lse ? lse_of<PER>(cur, zmax) : 0.f;  // warm-up rows only need the state
   return r;
+}
+
+// The row's normaliser from this lane's elements in row_summary's layout
+// (from registers as loaded, or from the row in LDS).
+template <int PER>
+__device__ __forceinline__ float row_lse(const float* raw, const RowShape<PER>& rs) {
+  float cur[PER];
+  float zmax = kNegInf;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    cur[j] = (j < PER - 1 || rs.last_ok) ? raw[j] : kNegInf;
+    zmax = __builtin_fmaxf(zmax, cur[j]);
+  }
+  return lse_of<PER>(cur, zmax);
+}
+
+template <int PER>
+__device__ __forceinline__ float row_lse_lds(const float* zrow, const RowShape<PER>& rs) {
+  const int lane = __lane_id();
+  float raw[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) raw[j] = zrow[(j < PER - 1) ? 64 * j + lane : rs.last_idx];
+  return row_lse<PER>(raw, rs);
 }
 
 // The step from state s on a summarised row (zrow in LDS).
@@ -1075,7 +1103,7 @@ struct FillRegs {
 
 template <int PER, int NT, int HOT>
 __device__ __forceinline__ void fill_gather(FillRegs<PER, NT, HOT>& f, const ArenaView& A,
-                                            int32_t m, int mode, int32_t off, int32_t nhot) {
+                                            int32_t m, int mode) {
   const int32_t V1 = A.V1, V = V1 - 1;
   const float* gpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
   const int32_t* gdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
@@ -1088,6 +1116,13 @@ __device__ __forceinline__ void fill_gather(FillRegs<PER, NT, HOT>& f, const Are
     f.cptr[k] = (i < V1) ? A.cls_ptr[i] : 0;
     f.ctok[k] = (i < V) ? A.cls_tok[i] : 0;
   }
+}
+
+// The state records of the first nhot states of the model at off, and its
+// psi / phi value tables.
+template <int PER, int NT, int HOT>
+__device__ __forceinline__ void fill_gather_hot(FillRegs<PER, NT, HOT>& f, const ArenaView& A,
+                                                int32_t m, int32_t off, int32_t nhot) {
   const uint32_t* src = A.state_rec + 3 * (int64_t)off;
 #pragma unroll
   for (int k = 0; k < f.KH; ++k) {
@@ -1101,8 +1136,7 @@ __device__ __forceinline__ void fill_gather(FillRegs<PER, NT, HOT>& f, const Are
 }
 
 template <int PER, int NT, int HOT>
-__device__ __forceinline__ void fill_scatter(const FillRegs<PER, NT, HOT>& f, Tables<PER>& tb,
-                                             StateHot<HOT>& h, int32_t nhot) {
+__device__ __forceinline__ void fill_scatter(const FillRegs<PER, NT, HOT>& f, Tables<PER>& tb) {
 #pragma unroll
   for (int k = 0; k < f.KT; ++k) {
     const int32_t i = k * NT + (int32_t)threadIdx.x;
@@ -1114,6 +1148,11 @@ __device__ __forceinline__ void fill_scatter(const FillRegs<PER, NT, HOT>& f, Ta
       tb.cls_tok[i] = (uint16_t)f.ctok[k];
     }
   }
+}
+
+template <int PER, int NT, int HOT>
+__device__ __forceinline__ void fill_scatter_hot(const FillRegs<PER, NT, HOT>& f,
+                                                 StateHot<HOT>& h, int32_t nhot) {
 #pragma unroll
   for (int k = 0; k < f.KH; ++k) {
     const int32_t i = k * NT + (int32_t)threadIdx.x;
@@ -1459,13 +1498,16 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   const RowShape<PER> rs(V1);
   const bool own = w < T;  // this wave has a row
   const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
-  // the tables' loads, then the row's, then the tables' stores
+  // the tables' loads, then the row's (from HBM, the slowest), then the
+  // tables' stores while the row is still on its way
   FillRegs<PER, NT, HOT> fr;
-  fill_gather<PER, NT, HOT>(fr, A, m, mode, off, nhot);
+  fill_gather<PER, NT, HOT>(fr, A, m, mode);
+  fill_gather_hot<PER, NT, HOT>(fr, A, m, off, nhot);
   asm volatile("" ::: "memory");
   float raw[PER];
   if (own) load_row<Ld, PER>(raw, col + (int64_t)w * tstride, rs);
-  fill_scatter<PER, NT, HOT>(fr, S.tab, S.hot, nhot);
+  fill_scatter<PER, NT, HOT>(fr, S.tab);
+  fill_scatter_hot<PER, NT, HOT>(fr, S.hot, nhot);
   __syncthreads();
 
   RowSum r = {};
@@ -1473,7 +1515,8 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   if (own) {
     float rp[PER];
     root_psi_regs<PER>(rp, S.tab, rs);
-    r = row_summary<PER, true>(S.zbuf[w], S.tab, raw, rp, rs, V, true, &top);
+    // the normaliser is taken later, off the sequential part
+    r = row_summary<PER, true>(S.zbuf[w], S.tab, raw, rp, rs, V, false, &top);
     if (lane == 0) S.rsum[w] = r;
     S.ltop[w][lane] = (uint32_t)top.i1 | ((uint32_t)top.i2 << 16);
   }
@@ -1509,8 +1552,24 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     S.spec_ans[w] = make_int4(a.tok, a.ns, __float_as_int(a.b), __float_as_int(a.zv));
   }
   __syncthreads();
-  if (w != 0) return;
+  if (w != 0) {
+    // the normalisers while wave 0 walks: every other wave its own row (from
+    // registers), the last wave also row 0 (from LDS)
+    if (own) {
+      const float l = row_lse<PER>(raw, rs);
+      if (lane == 0) S.lse[w] = l;
+    }
+    if (w == Shape<PER>::W - 1 && T > 0) {
+      const float l = row_lse_lds<PER>(S.zbuf[0], rs);
+      if (lane == 0) S.lse[0] = l;
+    }
+    __syncthreads();
+    return;
+  }
 
+  // The walk is the sequential part: its instructions go first on this SIMD
+  // (the other waves' normalisers take the cycles it leaves idle).
+  __builtin_amdgcn_s_setprio(3);
   // lane t holds row t's answer; rows off the exact trajectory are redone
   int4 ans = make_int4(0, 0, 0, 0);
   int32_t gx = INT_MIN;
@@ -1540,11 +1599,12 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     }
     s = ns;
   }
+  __syncthreads();  // the normalisers
   if (lane < T) {
     const int64_t oi = (int64_t)lane * B + b;
     out_tok[oi] = ans.x;
     out_state[oi] = ans.y;
-    out_score[oi] = (__int_as_float(ans.w) - S.rsum[lane].lse) + __int_as_float(ans.z);
+    out_score[oi] = (__int_as_float(ans.w) - S.lse[lane]) + __int_as_float(ans.z);
   }
   if (lane == 0) states[b] = s;
 }
