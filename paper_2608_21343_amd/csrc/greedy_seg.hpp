@@ -1570,34 +1570,44 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   // The walk is the sequential part: its instructions go first on this SIMD
   // (the other waves' normalisers take the cycles it leaves idle).
   __builtin_amdgcn_s_setprio(3);
-  // lane t holds row t's answer; rows off the exact trajectory are redone
+  // Lane t holds row t's guess, answer and summary. A run of rows whose
+  // guesses follow each other's answers is exact as soon as its first guess
+  // is: link says that row t's answer is row t+1's guess, and the walk jumps
+  // over such runs. Any other row is evaluated again from the exact state.
   int4 ans = make_int4(0, 0, 0, 0);
   int32_t gx = INT_MIN;
+  RowSum rl_ = {};
   if (lane < T) {
     ans = S.spec_ans[lane];
     gx = S.spec_x[lane];
+    rl_ = S.rsum[lane];
   }
+  const int32_t gx_next = __shfl_down(gx, 1, 64);
+  const uint64_t stop = ~__ballot(lane + 1 < T && gx_next == ans.y);  // bit T-1 is set
   int32_t s = (mode == 1) ? s0 : fixed;
-  // the next row's summary and lane tops are read while this row is checked
-  RowSum rn = S.rsum[0];
-  uint32_t tn = S.ltop[0][lane];
-  for (int32_t t = 0; t < T; ++t) {
-    const RowSum rt = rn;
-    const uint32_t tp = tn;
-    if (t + 1 < T) {
-      rn = S.rsum[t + 1];
-      tn = S.ltop[t + 1][lane];
-    }
-    int32_t ns;
+  int32_t t = 0;
+  while (t < T) {
     if (rl(gx, t) == s) {
-      ns = rl(ans.y, t);
-    } else {
-      const LaneTop tt = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16), 0.f, 0.f};
-      const Answer e = step_from<PER>(Gr, S.tab, S.zbuf[t], S.marks[0], rs, rt, s, mode, V, &tt);
-      if (lane == t) ans = make_int4(e.tok, e.ns, __float_as_int(e.b), __float_as_int(e.zv));
-      ns = __builtin_amdgcn_readfirstlane(e.ns);
+      const int32_t u = t + (int32_t)__builtin_ctzll(stop >> t);
+      s = rl(ans.y, u);
+      t = u + 1;
+      continue;
     }
-    s = ns;
+    const uint32_t tp = S.ltop[t][lane];
+    RowSum rt;
+    rt.zb = rlf(rl_.zb, t);
+    rt.ymax = rlf(rl_.ymax, t);
+    rt.lse = 0.f;
+    rt.r1_psi = rlf(rl_.r1_psi, t);
+    rt.r1_z = rlf(rl_.r1_z, t);
+    rt.r1_tok = rl(rl_.r1_tok, t);
+    rt.r1_cls = rl(rl_.r1_cls, t);
+    rt.r1_dst = rl(rl_.r1_dst, t);
+    const LaneTop tt = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16), 0.f, 0.f};
+    const Answer e = step_from<PER>(Gr, S.tab, S.zbuf[t], S.marks[0], rs, rt, s, mode, V, &tt);
+    if (lane == t) ans = make_int4(e.tok, e.ns, __float_as_int(e.b), __float_as_int(e.zv));
+    s = __builtin_amdgcn_readfirstlane(e.ns);
+    ++t;
   }
   __syncthreads();  // the normalisers
   if (lane < T) {
