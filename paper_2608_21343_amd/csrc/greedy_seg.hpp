@@ -1458,9 +1458,8 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
 }
 
 // Short calls (T <= W steps, a streaming chunk). Wave w owns row w: it
-// summarises the row (normaliser, best root moves, row copy in LDS), then
-// evaluates the step of row w from a guessed start state x_w, all rows in
-// parallel:
+// summarises the row (best root moves, row copy in LDS), then evaluates the
+// step of row w from a guessed start state x_w, all rows in parallel:
 //
 //   x_0 = the carried state (exact);
 //   x_w (w >= 1) starts as the target of row w-1's best root move, the move
@@ -1476,6 +1475,7 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
 // matches. Every round costs about one evaluation and saves about one
 // walker evaluation in the stream with the longest match: three rounds
 // measured best on 128 streams of 16-row chunks (two and four were slower).
+// While wave 0 walks, the other waves take the rows' normalisers.
 constexpr int kSpecRounds = 3;
 
 template <class Ld, int PER>
