@@ -44,7 +44,7 @@
 namespace tbias {
 namespace seg {
 
-constexpr int kWarm = 2;    // warm-up rows of a guessed segment start
+constexpr int kWarm = 4;    // warm-up rows of a guessed segment start
 constexpr int kTraj = 64;   // trajectory states kept per segment
 constexpr int kMinSeg = 8;  // shortest segment worth a wave
 constexpr int kScalarKids = 8;  // arena children walked one at a time up to this many
