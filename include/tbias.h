@@ -23,7 +23,8 @@
  * - Graph states are model-local breadth-first ids (root = 0); -1 means "no
  *   model". A carried state or model id that is out of range for the arena is
  *   never dereferenced: that stream is decoded without biasing and its output
- *   states are written as TB_STATE_INVALID (-2).
+ *   states are written as TB_STATE_INVALID (-2), or TB_STATE_TIMEOUT (-3) when
+ *   the carried state was TB_STATE_TIMEOUT (see below).
  */
 #ifndef TBIAS_H
 #define TBIAS_H
@@ -45,7 +46,21 @@ enum {
 
 enum { TB_F32 = 0, TB_BF16 = 1 };                     /* logit element type */
 enum { TB_COMMIT = 0, TB_PURE_POTENTIAL = 1 };        /* potential reading   */
-enum { TB_STATE_NONE = -1, TB_STATE_INVALID = -2 };
+/*
+ * Special state values (graph states are otherwise >= 0):
+ *   TB_STATE_NONE     model -1: the stream is not biased.
+ *   TB_STATE_INVALID  the stream's model id or carried state was out of range
+ *                     for the arena: the stream is decoded without biasing.
+ *   TB_STATE_TIMEOUT  a bounded wait inside a greedy step kernel gave up (the
+ *                     waves of one workgroup hand states to each other; this
+ *                     should never happen and indicates a fault). The rows
+ *                     written as TB_STATE_TIMEOUT, and the stream's later
+ *                     rows, are unreliable. The state is sticky: a carried
+ *                     TB_STATE_TIMEOUT makes later calls decode that stream
+ *                     without biasing and write TB_STATE_TIMEOUT again, until
+ *                     tb_reset_stream or tb_init_states restarts it.
+ */
+enum { TB_STATE_NONE = -1, TB_STATE_INVALID = -2, TB_STATE_TIMEOUT = -3 };
 
 /* Host-side compiled graphs of all models (library owned). */
 typedef struct tb_graphs tb_graphs;
@@ -250,6 +265,24 @@ int tb_reset_stream(const tb_arena* a, int32_t B, int32_t b, int32_t new_model_i
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* tb_last_error(void);
+
+/*
+ * Test hooks (not for production use). They change process-wide settings
+ * that later step calls read; calls that overlap a change see either value.
+ *
+ * tb_debug_select_kernels — force a kernel family so that tests can compare
+ * every path: greedy 0 = automatic choice, 1 = the reference kernel (one
+ * workgroup per stream, any V); beam 0 = automatic, 1 = the reference kernel,
+ * 2 = automatic but never the helper-wave kernel. TB_EINVAL for other values.
+ *
+ * tb_debug_set_spin_limit — polls after which the greedy hand-off wait (the
+ * waves of a workgroup pass exact states in order) gives up and writes
+ * TB_STATE_TIMEOUT; 0 restores the default (2^26, never reached in normal
+ * operation). A limit of 1 lets a test force the timeout path from the host;
+ * the kernel still ends normally.
+ */
+int tb_debug_select_kernels(int32_t greedy, int32_t beam);
+int tb_debug_set_spin_limit(uint32_t polls);
 
 #ifdef __cplusplus
 }

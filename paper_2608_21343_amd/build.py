@@ -17,7 +17,7 @@ BUILD = PKG / "_build"
 LIB = PKG / "libtbias.so"
 ROCM = Path(os.environ.get("ROCM_PATH", "/opt/rocm"))
 
-HIP_SOURCES = ["capi.hip", "greedy.hip", "greedy_fast.hip", "greedy_seg.hip",
+HIP_SOURCES = ["capi.hip", "greedy.hip", "greedy_seg.hip",
                "greedy_seg_1_8.hip", "greedy_seg_9_16.hip", "greedy_seg_17_24.hip",
                "greedy_seg_25_32.hip", "greedy_wide.hip", "beam.hip", "beam_wide_f32.hip", "beam_wide_bf16.hip",
                "beam_pipe_f32.hip", "beam_pipe_bf16.hip", "beam_fast_1_8.hip", "beam_fast_9_16.hip",
@@ -32,9 +32,8 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]
-# per-file additions: the pipelined greedy kernel never sees NaN keys in its
-# contract, which lets max reductions skip NaN canonicalisation
-HIP_EXTRA = {"greedy_fast.hip": ["-fno-honor-nans"]}
+# per-file additions to HIPCC_FLAGS
+HIP_EXTRA: dict = {}
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall", "-pthread"]
 
 

@@ -20,8 +20,11 @@ LIB_PATH = _PKG / "libtbias.so"
 TB_OK, TB_EINVAL, TB_ENOMEM, TB_EHIP, TB_ERANGE = 0, -1, -2, -3, -4
 TB_F32, TB_BF16 = 0, 1
 TB_COMMIT, TB_PURE_POTENTIAL = 0, 1
-TB_STATE_NONE, TB_STATE_INVALID = -1, -2
+TB_STATE_NONE, TB_STATE_INVALID, TB_STATE_TIMEOUT = -1, -2, -3
 TB_MAX_BEAM = 16
+# tb_debug_select_kernels choices
+GREEDY_AUTO, GREEDY_REF = 0, 1
+BEAM_AUTO, BEAM_REF, BEAM_NO_PIPE = 0, 1, 2
 
 
 class tb_arena_layout(C.Structure):
@@ -74,6 +77,8 @@ def _load() -> C.CDLL:
         "tb_boost_step_beam": [C.POINTER(tb_arena), P, I32, I32, I32, I32, I64, P, P, P, P, P, P,
                                P, P, P],
         "tb_reset_stream": [C.POINTER(tb_arena), I32, I32, I32, I32, P, P, P, P],
+        "tb_debug_select_kernels": [I32, I32],
+        "tb_debug_set_spin_limit": [C.c_uint32],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -90,7 +95,8 @@ LIB = _load()
 
 EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb_graphs_upload",
             "tb_graphs_free", "tb_validate_image", "tb_init_states", "tb_boost_step_greedy",
-            "tb_boost_step_beam", "tb_reset_stream", "tb_last_error")
+            "tb_boost_step_beam", "tb_reset_stream", "tb_last_error",
+            "tb_debug_select_kernels", "tb_debug_set_spin_limit")
 
 
 def _check(code: int) -> None:
@@ -113,6 +119,16 @@ def _dptr(t, dtype=None, name="tensor") -> Optional[int]:
     if dtype is not None and t.dtype != dtype:
         raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
     return t.data_ptr()
+
+
+def _need(t, n: int, name: str, exact: bool = True) -> None:
+    """Reject a buffer whose element count does not fit the call (the kernels
+    trust these sizes)."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    k = t.numel()
+    if (k != n) if exact else (k < n):
+        raise ValueError(f"{name} holds {k} elements, needs {'' if exact else 'at least '}{n}")
 
 
 def _stream(stream) -> Optional[int]:
@@ -213,6 +229,7 @@ def tb_init_states(arena: Arena, B: int, K: int, model_ids, states, scores=None,
 
 
 def _logits_args(logits):
+    """(dtype code, row stride) of a logits tensor; shape and layout checks only."""
     import torch
     if logits.dtype == torch.float32:
         dt = TB_F32
@@ -220,11 +237,15 @@ def _logits_args(logits):
         dt = TB_BF16
     else:
         raise ValueError("logits must be float32 or bfloat16")
-    if not logits.is_cuda:
-        raise ValueError("logits must be a device tensor")
     if logits.stride(-1) != 1:
         raise ValueError("logits rows must be contiguous")
-    return dt, logits.data_ptr(), logits.stride(-2)
+    return dt, logits.stride(-2)
+
+
+def _logits_ptr(logits) -> int:
+    if not logits.is_cuda:
+        raise ValueError("logits must be a device tensor")
+    return logits.data_ptr()
 
 
 def tb_boost_step_greedy(arena: Arena, logits, model_ids, states, out_tok, out_state, out_score,
@@ -232,16 +253,31 @@ def tb_boost_step_greedy(arena: Arena, logits, model_ids, states, out_tok, out_s
                          row_stride: Optional[int] = None, stream=None) -> None:
     """logits: [T, B, V+1] (or [T, B, 1, V+1]) device tensor, rows contiguous."""
     import torch
-    dt, ptr, rs = _logits_args(logits)
+    dt, rs = _logits_args(logits)
     if logits.dim() == 4:
         if logits.shape[2] != 1:
             raise ValueError("greedy logits must have K = 1")
         rs = logits.stride(1)
+    if logits.dim() not in (3, 4):
+        raise ValueError("greedy logits must be [T, B, V+1] or [T, B, 1, V+1]")
+    if logits.shape[-1] != arena.layout.v_plus_blank:
+        raise ValueError(f"logits rows hold {logits.shape[-1]} values, the arena has "
+                         f"V+1 = {arena.layout.v_plus_blank}")
+    if T is not None and not 0 <= T <= logits.shape[0]:
+        raise ValueError(f"T = {T} outside [0, {logits.shape[0]}]")
+    if B is not None and B != logits.shape[1]:
+        raise ValueError(f"B = {B} differs from the logits' {logits.shape[1]} streams")
     T = logits.shape[0] if T is None else T
-    B = logits.shape[1] if B is None else B
-    if logits.dim() >= 3 and T > 1 and logits.stride(0) != B * rs:
+    B = logits.shape[1]
+    if T > 1 and logits.stride(0) != B * rs:
         raise ValueError("logits steps must be laid out as (t*B + b) * row_stride")
-    rs = rs if row_stride is None else row_stride
+    if row_stride is not None and row_stride != rs:
+        raise ValueError(f"row_stride {row_stride} differs from the logits' {rs}")
+    _need(model_ids, B, "model_ids")
+    _need(states, B, "states")
+    for name, o in (("out_tok", out_tok), ("out_state", out_state), ("out_score", out_score)):
+        _need(o, T * B, name, exact=False)
+    ptr = _logits_ptr(logits)
     _check(LIB.tb_boost_step_greedy(C.byref(arena.arena), C.c_void_p(ptr), dt, T, B, rs,
                                     _dptr(model_ids, torch.int32, "model_ids"),
                                     _dptr(states, torch.int32, "states"),
@@ -255,12 +291,22 @@ def tb_boost_step_beam(arena: Arena, logits, model_ids, states, scores, out_tok,
                        out_state, out_step, out_cum, stream=None) -> None:
     """logits: [T, B, K, V+1] device tensor with (t, b, k) rows at ((t*B+b)*K+k)*row_stride."""
     import torch
-    dt, ptr, rs = _logits_args(logits)
+    dt, rs = _logits_args(logits)
     if logits.dim() != 4:
         raise ValueError("beam logits must be [T, B, K, V+1]")
-    T, B, K, _ = logits.shape
+    T, B, K, Vp1 = logits.shape
+    if Vp1 != arena.layout.v_plus_blank:
+        raise ValueError(f"logits rows hold {Vp1} values, the arena has "
+                         f"V+1 = {arena.layout.v_plus_blank}")
     if logits.stride(1) != K * rs or (T > 1 and logits.stride(0) != B * K * rs):
         raise ValueError("beam logits must be laid out as ((t*B + b)*K + k) * row_stride")
+    _need(model_ids, B, "model_ids")
+    _need(states, B * K, "states")
+    _need(scores, B * K, "scores")
+    for name, o in (("out_tok", out_tok), ("out_parent", out_parent), ("out_state", out_state),
+                    ("out_step", out_step), ("out_cum", out_cum)):
+        _need(o, T * B * K, name, exact=False)
+    ptr = _logits_ptr(logits)
     _check(LIB.tb_boost_step_beam(C.byref(arena.arena), C.c_void_p(ptr), dt, T, B, K, rs,
                                   _dptr(model_ids, torch.int32, "model_ids"),
                                   _dptr(states, torch.int32, "states"),
@@ -283,6 +329,31 @@ def tb_reset_stream(arena: Arena, b: int, new_model_id: int, K: int, model_ids, 
                                _dptr(model_ids, torch.int32, "model_ids"),
                                _dptr(states, torch.int32, "states"),
                                _dptr(scores, torch.float32, "scores"), _stream(stream)))
+
+
+def tb_debug_select_kernels(greedy: int = GREEDY_AUTO, beam: int = BEAM_AUTO) -> None:
+    """Test hook: force a kernel family (see tbias.h)."""
+    _check(LIB.tb_debug_select_kernels(greedy, beam))
+
+
+def tb_debug_set_spin_limit(polls: int = 0) -> None:
+    """Test hook: poll limit of the greedy hand-off wait (0 = default)."""
+    _check(LIB.tb_debug_set_spin_limit(polls))
+
+
+class kernels:
+    """Context manager for tests: ``with capi.kernels(greedy=GREEDY_REF): ...``."""
+
+    def __init__(self, greedy: int = GREEDY_AUTO, beam: int = BEAM_AUTO):
+        self.choice = (greedy, beam)
+
+    def __enter__(self):
+        tb_debug_select_kernels(*self.choice)
+        return self
+
+    def __exit__(self, *exc):
+        tb_debug_select_kernels(GREEDY_AUTO, BEAM_AUTO)
+        return False
 
 
 def image_arrays(image: np.ndarray, layout: tb_arena_layout) -> dict:

@@ -10,9 +10,6 @@
 // graph states (Sec. II-C: scores and states carried across calls).
 #include <climits>
 
-#include <cstdlib>
-#include <cstring>
-
 #include "beam_fast.hpp"
 #include "beam_pipe.hpp"
 #include "beam_wide.hpp"
@@ -97,12 +94,12 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
   __shared__ float sh_phi[MAXK];
   __shared__ int32_t sel_idx[MAXK];
   __shared__ float sel_val[MAXK];
-  __shared__ int32_t sh_bad;
+  __shared__ int32_t sh_bad, sh_tmo;
 
   const int tid = threadIdx.x;
   const int32_t b = blockIdx.x;
   const int32_t m = model_ids[b];
-  if (tid == 0) sh_bad = 0;
+  if (tid == 0) { sh_bad = 0; sh_tmo = 0; }
   __syncthreads();
   int32_t off = 0, n = 0;
   int mode = (m == -1) ? 0 : 1;
@@ -113,6 +110,7 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
     sh_state[tid] = s;
     sh_S[tid] = scores[(int64_t)b * K + tid];
     if (mode == 1 && (s < 0 || s >= n)) sh_bad = 1;
+    if (s == TB_STATE_TIMEOUT) sh_tmo = 1;
   }
   for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
   __syncthreads();
@@ -224,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
           bst = A.psi[off + ns] - sh_phi[k];
         }
       } else {
-        ns = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+        ns = unbiased_state(mode, sh_tmo != 0);
       }
       const typename Ld::T* row = logits + (((int64_t)t * B + b) * K + k) * stride;
       const float z = Ld::get(row, v);
@@ -278,20 +276,20 @@ void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int3
 
 }  // namespace
 
-// The kernel with helper waves serves K <= 8 where a two-slot ring of rows
-// fits in LDS (V+1 <= 1088 for float32 and K > 4, up to 8256 for bfloat16 and
-// K <= 4); then the one-wave-per-hypothesis kernel (K <= 8, V+1 <= 2048,
-// override sets that fit its lists) and the wide-row kernel (K <= 8, V+1 in
-// (2048, 256 * 41]); the reference kernel serves the rest.
-// TBIAS_BEAM_KERNEL=ref selects the reference kernel and =nopipe skips the
-// helper-wave kernel (used to test every path).
+// Kernel choice: the helper-wave kernel serves V+1 > 2048 with K <= 4 (rows
+// up to 4224 float32 or 8320 bfloat16 tokens, where its two-slot LDS ring
+// fits); the one-wave-per-hypothesis kernel serves V+1 <= 2048 with K <= 8
+// (override sets that fit its lists); the wide-row kernel serves K <= 8 and
+// V+1 in (2048, 256 * 41]; the reference kernel serves the rest. Tests can
+// force the reference kernel, or skip the helper-wave kernel, through
+// tb_debug_select_kernels.
 hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, int32_t T, int32_t B,
                        int32_t K, int64_t row_stride, const int32_t* model_ids, int32_t* states,
                        float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
                        float* out_step, float* out_cum, hipStream_t st) {
-  const char* e = std::getenv("TBIAS_BEAM_KERNEL");
-  const bool ref = e && std::strcmp(e, "ref") == 0;
-  const bool nopipe = e && std::strcmp(e, "nopipe") == 0;
+  const int32_t choice = debug_beam_kernel();
+  const bool ref = choice == kBeamRef;
+  const bool nopipe = choice == kBeamNoPipe;
   if (!ref && !nopipe && K <= 8) {
     bpipe::PipeLaunch f = dtype == TB_F32 ? bpipe::pipe_launcher_f32(A.V1, K)
                                           : bpipe::pipe_launcher_bf16(A.V1, K);

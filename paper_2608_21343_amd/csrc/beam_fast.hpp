@@ -63,6 +63,7 @@ struct alignas(16) BeamFixed {
   int32_t red_f[MAXK];
   int32_t red_dst[MAXK];
   int32_t bad;
+  int32_t tmo;  // a slot carried TB_STATE_TIMEOUT
 };
 
 template <int PER, int MAXK>
@@ -122,13 +123,14 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     off = A.model_off[m];
     n = A.model_n[m];
   }
-  if (threadIdx.x == 0) S.bad = 0;
+  if (threadIdx.x == 0) { S.bad = 0; S.tmo = 0; }
   __syncthreads();
   if (threadIdx.x < K) {
     const int32_t s = states[(int64_t)b * K + threadIdx.x];
     S.hyp_s[0][threadIdx.x] = s;
     S.hyp_S[0][threadIdx.x] = scores[(int64_t)b * K + threadIdx.x];
     if (mode == 1 && (s < 0 || s >= n)) S.bad = 1;
+    if (s == TB_STATE_TIMEOUT) S.tmo = 1;
   }
   const RowShape<PER> rs(V1);
   float cur[PER], nxt[PER];
@@ -461,7 +463,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           bst = ((d >= 0) ? G.psi_of(ns) : S.tab.rpsi[v]) - phi_k;
         }
       } else {
-        ns = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+        ns = unbiased_state(mode, S.tmo != 0);
       }
       const float z = S.zbuf[k][v];
       const float val = S.sel_val[w];

@@ -89,6 +89,7 @@ struct alignas(16) PipeLds {
   int32_t hyp_s[kSlots];
   float hyp_S[kSlots];
   int32_t bad;
+  int32_t tmo;  // a slot carried TB_STATE_TIMEOUT
 };
 
 template <class RT>
@@ -258,17 +259,18 @@ __global__ __launch_bounds__(kThreads) void beam_pipe_kernel(
     off = A.model_off[m];
     n = A.model_n[m];
   }
-  if (threadIdx.x == 0) sh.bad = 0;
+  if (threadIdx.x == 0) { sh.bad = 0; sh.tmo = 0; }
   __syncthreads();
   if ((int32_t)threadIdx.x < K) {
     const int32_t s = states[(int64_t)b * K + threadIdx.x];
     sh.hyp_s[threadIdx.x] = s;
     sh.hyp_S[threadIdx.x] = scores[(int64_t)b * K + threadIdx.x];
     if (mode == 1 && (s < 0 || s >= n)) sh.bad = 1;
+    if (s == TB_STATE_TIMEOUT) sh.tmo = 1;
   }
   __syncthreads();
   if (mode == 1 && sh.bad) mode = -1;  // uniform: an invalid carried state decodes unbiased
-  const int32_t fixed = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+  const int32_t fixed = unbiased_state(mode, sh.tmo != 0);
   const float* rpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
   const int32_t* rdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
   auto row_of = [&](int32_t t, int32_t kk) {

@@ -38,6 +38,7 @@ struct alignas(16) BeamShared {
   double reds[kWaves];
   int32_t nlist;
   int32_t bad;
+  int32_t tmo;  // a slot carried TB_STATE_TIMEOUT
   int32_t hyp_s[MAXK];
   float hyp_S[MAXK];
   float hyp_lse[MAXK];
@@ -78,21 +79,22 @@ __global__ __launch_bounds__(kThreads) void beam_wide_kernel(
     off = A.model_off[m];
     n = A.model_n[m];
   }
-  if (tid == 0) sh.bad = 0;
+  if (tid == 0) { sh.bad = 0; sh.tmo = 0; }
   __syncthreads();
   if (tid < K) {
     const int32_t s = states[(int64_t)b * K + tid];
     sh.hyp_s[tid] = s;
     sh.hyp_S[tid] = scores[(int64_t)b * K + tid];
     if (mode == 1 && (s < 0 || s >= n)) sh.bad = 1;
+    if (s == TB_STATE_TIMEOUT) sh.tmo = 1;
   }
   __syncthreads();
   if (mode == 1 && sh.bad) mode = -1;  // uniform: an invalid carried state decodes unbiased
-  const int32_t fixed = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+  const int32_t fixed = unbiased_state(mode, sh.tmo != 0);
   Own<TPV> o;
   float zn[TPV], zbn = kNegInf;
   own_tables<TPV>(o, A, m, mode, fixed);
-  Ctx C = make_ctx(A, off, mode, &sh.nlist, dyn);
+  Ctx C = make_ctx(A, off, mode, fixed, &sh.nlist, dyn);
   auto row_of = [&](int32_t t, int32_t k) {
     return logits + (((int64_t)t * B + b) * K + k) * stride;
   };

@@ -1,4 +1,5 @@
 // C ABI shim: synchronous argument checks, then asynchronous launches.
+#include <atomic>
 #include <cstring>
 #include <string>
 
@@ -44,7 +45,30 @@ int check_logits(const void* logits, int32_t dtype, int64_t row_stride, int32_t 
   return TB_OK;
 }
 
+std::atomic<int32_t> g_greedy_kernel{kGreedyAuto};
+std::atomic<int32_t> g_beam_kernel{kBeamAuto};
+std::atomic<uint32_t> g_spin_limit{0u};
+
 }  // namespace
+
+namespace tbias {
+int32_t debug_greedy_kernel() { return g_greedy_kernel.load(std::memory_order_relaxed); }
+int32_t debug_beam_kernel() { return g_beam_kernel.load(std::memory_order_relaxed); }
+uint32_t debug_spin_limit() { return g_spin_limit.load(std::memory_order_relaxed); }
+}  // namespace tbias
+
+extern "C" int tb_debug_select_kernels(int32_t greedy, int32_t beam) {
+  if (greedy < kGreedyAuto || greedy > kGreedyRef) return fail(TB_EINVAL, "unknown greedy kernel");
+  if (beam < kBeamAuto || beam > kBeamNoPipe) return fail(TB_EINVAL, "unknown beam kernel");
+  g_greedy_kernel.store(greedy, std::memory_order_relaxed);
+  g_beam_kernel.store(beam, std::memory_order_relaxed);
+  return TB_OK;
+}
+
+extern "C" int tb_debug_set_spin_limit(uint32_t polls) {
+  g_spin_limit.store(polls, std::memory_order_relaxed);
+  return TB_OK;
+}
 
 extern "C" int tb_graphs_upload(const tb_graphs* g, void* dev_base, int64_t bytes,
                                 void* hip_stream, tb_arena* out) {

@@ -203,6 +203,15 @@ __device__ __forceinline__ double exp_nonpos(double x) {
   return tiny ? 0.0 : __builtin_ldexp(p, (int)k);
 }
 
+// The state written for a stream decoded without biasing (mode != 1 below):
+// -1 for model -1; a carried TB_STATE_TIMEOUT stays TB_STATE_TIMEOUT (the
+// stream's earlier outputs are unreliable until it is reset); any other
+// out-of-range model id or carried state gives TB_STATE_INVALID.
+__device__ __forceinline__ int32_t unbiased_state(int mode, bool carried_timeout) {
+  if (mode == 0) return TB_STATE_NONE;
+  return carried_timeout ? TB_STATE_TIMEOUT : TB_STATE_INVALID;
+}
+
 // Resolve a (model id, carried state) pair.
 //   returns 1 and sets off/n when the stream is biased with a valid state,
 //   0 for model -1, -1 for an out-of-range model id or carried state.

@@ -11,8 +11,6 @@
 // marks the entries written in the current step (cleared once every 65535
 // steps) next to the overriding target state.
 #include <climits>
-#include <cstdlib>
-#include <cstring>
 
 #include "device.hpp"
 #include "launch.hpp"
@@ -81,6 +79,7 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
   int32_t s = states[b];
   int32_t off = 0, n = 0;
   const int mode = resolve_stream(A, m, s, off, n);  // 1 biased, 0 none, -1 invalid
+  const int32_t fixed = unbiased_state(mode, s == TB_STATE_TIMEOUT);
   for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
   __syncthreads();
   uint32_t tag = 0;
@@ -150,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
           bst = A.psi[off + ns] - phi_s;
         }
       } else {
-        ns = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+        ns = fixed;
       }
       const float z = Ld::get(row, v);
       const int64_t o = (int64_t)t * B + b;
@@ -167,28 +166,15 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
 
 }  // namespace
 
-namespace {
-// TBIAS_GREEDY_KERNEL selects a kernel for testing: "ref" (one workgroup per
-// stream, any V), "pipe" (pipelined), anything else the segmented kernels
-// (waves as segments for V+1 <= 2048, workgroups as segments above).
-int greedy_kernel_choice() {
-  const char* e = std::getenv("TBIAS_GREEDY_KERNEL");
-  if (e && std::strcmp(e, "ref") == 0) return 0;
-  if (e && std::strcmp(e, "pipe") == 0) return 1;
-  return 2;
-}
-}  // namespace
-
 hipError_t launch_greedy(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
                          int32_t B, int64_t row_stride, const int32_t* model_ids, int32_t* states,
                          int32_t* out_tok, int32_t* out_state, float* out_score, hipStream_t st) {
-  const int choice = greedy_kernel_choice();
-  if (choice != 0) {
-    hipError_t e = (choice == 1)
-                       ? launch_greedy_fast(A, logits, dtype, T, B, row_stride, model_ids, states,
-                                            out_tok, out_state, out_score, st)
-                       : launch_greedy_seg(A, logits, dtype, T, B, row_stride, model_ids, states,
-                                           out_tok, out_state, out_score, st);
+  // the segmented kernels (waves as segments for V+1 <= 2048, workgroups as
+  // segments above); the reference kernel for anything larger, or when a
+  // test selects it
+  if (debug_greedy_kernel() != kGreedyRef) {
+    hipError_t e = launch_greedy_seg(A, logits, dtype, T, B, row_stride, model_ids, states,
+                                     out_tok, out_state, out_score, st);
     if (e != hipErrorNotSupported) return e;
     (void)hipGetLastError();  // clear the sticky "not supported" before the fallback
     e = launch_greedy_wide(A, logits, dtype, T, B, row_stride, model_ids, states, out_tok,

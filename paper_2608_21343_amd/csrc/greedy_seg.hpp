@@ -40,6 +40,7 @@
 #include <climits>
 
 #include "device.hpp"
+#include "launch.hpp"
 
 namespace tbias {
 namespace seg {
@@ -48,8 +49,11 @@ constexpr int kWarm = 4;    // warm-up rows of a guessed segment start
 constexpr int kTraj = 64;   // trajectory states kept per segment
 constexpr int kMinSeg = 8;  // shortest segment worth a wave
 constexpr int kScalarKids = 8;  // arena children walked one at a time up to this many
+// Polls of the hand-off wait before it gives up (rows then get
+// TB_STATE_TIMEOUT). The waves of a workgroup are resident together and a
+// wave never waits for a later one, so the wait always ends well before this.
 constexpr uint32_t kSpinLimit = 1u << 26;
-constexpr int32_t kStateTimeout = -3;
+constexpr int32_t kStateTimeout = TB_STATE_TIMEOUT;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -1227,7 +1231,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
     int32_t G, int32_t L, const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
     int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
-    float* __restrict__ out_score) {
+    float* __restrict__ out_score, uint32_t spin_limit) {
   constexpr int W = Shape<PER>::W;
   constexpr int NT = Shape<PER>::NT;
   constexpr int HOT = SegLds<PER>::HOT;
@@ -1271,8 +1275,8 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   float rp[PER];
   root_psi_regs<PER>(rp, S.tab, rs);
 
-  const int32_t unbiased_state = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
-  const int32_t start = (mode == 1) ? (segi == 0 ? s0 : 0) : unbiased_state;
+  const int32_t start = (mode == 1) ? (segi == 0 ? s0 : 0)
+                                    : unbiased_state(mode, s0 == TB_STATE_TIMEOUT);
 
   // ---- main pass over the segment (with warm-up rows)
   int32_t s = start;
@@ -1323,7 +1327,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   if (w > 0) {
     uint32_t spins = 0;
     while (lds_ld(&S.fin_ready[w - 1]) == 0) {
-      if (lds_ld(&S.abort_flag) || ++spins > kSpinLimit) {
+      if (lds_ld(&S.abort_flag) || ++spins > spin_limit) {
         lds_st(&S.abort_flag, 1);
         break;
       }
@@ -1438,8 +1442,12 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
         load_row<Ld, PER>(rb, col + (int64_t)(tb0 + 1 < T ? tb0 + 1 : tb0) * tstride, rs);
       }
       int32_t x = __builtin_amdgcn_readfirstlane(out_state[(int64_t)(tb0 - 1) * B + b]);
-      if (x < 0 || x >= n) {  // invalid carried state (-2) or a timed-out main kernel (-3)
+      if (x < 0 || x >= n) {
+        // a timed-out main kernel (-3): no exact state reaches this boundary,
+        // so none of the following rows can be repaired; they are marked
         timed_out = x == kStateTimeout;
+        if (timed_out)
+          for (int32_t t = tb0 + lane; t < T; t += 64) out_state[(int64_t)t * B + b] = kStateTimeout;
         break;
       }
       // the rows up to the meeting point are recomputed; find where it was
@@ -1526,7 +1534,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   __syncthreads();
 
   const SGraph Gr(A, off, nhot, S.hot, S.tab);
-  const int32_t fixed = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+  const int32_t fixed = unbiased_state(mode, s0 == TB_STATE_TIMEOUT);
   int32_t x;  // guessed start state of row w
   if (mode != 1) {
     x = fixed;  // unbiased rows: the step does not depend on the state
@@ -1659,9 +1667,10 @@ hipError_t launch_seg(const ArenaView& A, const void* logits, int32_t T, int32_t
   }
   int32_t G, L;
   seg_geometry<PER>(T, B, G, L);
+  const uint32_t spin = debug_spin_limit();
   hipLaunchKernelGGL((greedy_seg_kernel<Ld, PER>), dim3(B * G), dim3(Shape<PER>::NT), 0, st, A,
                      static_cast<const TT*>(logits), T, B, stride, G, L, model_ids, states,
-                     out_tok, out_state, out_score);
+                     out_tok, out_state, out_score, spin ? spin : kSpinLimit);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || G == 1) return e;
   hipLaunchKernelGGL((greedy_fix_kernel<Ld, PER>), dim3(B), dim3(kFixThreads), 0, st, A,

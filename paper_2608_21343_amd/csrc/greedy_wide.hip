@@ -136,8 +136,9 @@ __global__ __launch_bounds__(kThreads) void greedy_wide_kernel(
   Own<TPV> o;
   float zn[TPV], zbn = kNegInf;
   if (t0 < t1) load_row<Ld, TPV>(o.z, o.zb, col + (int64_t)tw * tstride, V1);
-  own_tables<TPV>(o, A, m, mode, (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID);
-  Ctx C = make_ctx(A, off, mode, &sh.nlist, dyn);
+  const int32_t fixed = unbiased_state(mode, s0 == TB_STATE_TIMEOUT);
+  own_tables<TPV>(o, A, m, mode, fixed);
+  Ctx C = make_ctx(A, off, mode, fixed, &sh.nlist, dyn);
   __syncthreads();
 
   int32_t s = (mode == 1) ? (g == 0 ? s0 : 0) : C.fixed;
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void greedy_wide_fix_kernel(
     Own<TPV> o;
     float zn[TPV], zbn = kNegInf;
     own_tables<TPV>(o, A, m, 1, 0);
-    Ctx C = make_ctx(A, off, 1, &sh.nlist, dyn);
+    Ctx C = make_ctx(A, off, 1, 0, &sh.nlist, dyn);
     __syncthreads();
     for (int32_t gg = 1; gg < G; ++gg) {
       const int32_t tb0 = gg * L;

@@ -22,12 +22,6 @@ hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, in
                        float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
                        float* out_step, float* out_cum, hipStream_t st);
 
-// Pipelined greedy kernel; hipErrorNotSupported when V+1 is too large for it.
-hipError_t launch_greedy_fast(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
-                              int32_t B, int64_t row_stride, const int32_t* model_ids,
-                              int32_t* states, int32_t* out_tok, int32_t* out_state,
-                              float* out_score, hipStream_t st);
-
 // Segmented greedy kernel (plus its boundary fix-up); hipErrorNotSupported
 // when V+1 is too large for it.
 hipError_t launch_greedy_seg(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
@@ -44,5 +38,14 @@ hipError_t launch_greedy_wide(const ArenaView& A, const void* logits, int32_t dt
 
 // Largest V+1 the step kernels accept (LDS tables are sized by it).
 constexpr int32_t kMaxV1 = 10241;
+
+// Test hooks (tb_debug_select_kernels, tb_debug_set_spin_limit): kernel
+// choices forced by tests, and the poll limit of the greedy hand-off wait
+// (0 = the kernel's default). Plain process-wide values, read per call.
+enum { kGreedyAuto = 0, kGreedyRef = 1 };
+enum { kBeamAuto = 0, kBeamRef = 1, kBeamNoPipe = 2 };
+int32_t debug_greedy_kernel();
+int32_t debug_beam_kernel();
+uint32_t debug_spin_limit();
 
 }  // namespace tbias

@@ -49,14 +49,14 @@ inline size_t lds_bytes(const ArenaView& A) {
   return 4 * (size_t)(A.V1 - 1) + 8 * (size_t)cap;
 }
 
-__device__ __forceinline__ Ctx make_ctx(const ArenaView& A, int32_t off, int mode,
+__device__ __forceinline__ Ctx make_ctx(const ArenaView& A, int32_t off, int mode, int32_t fixed,
                                         int32_t* nlist, unsigned char* dyn) {
   const int32_t V = A.V1 - 1;
   Ctx C;
   C.A = &A;
   C.off = off;
   C.mode = mode;
-  C.fixed = (mode == 0) ? TB_STATE_NONE : TB_STATE_INVALID;
+  C.fixed = fixed;
   C.cap = A.max_override > 0 ? A.max_override : 1;
   C.omark = reinterpret_cast<uint32_t*>(dyn);
   C.olist_y = reinterpret_cast<int32_t*>(dyn + 4 * (size_t)V);

@@ -1,0 +1,169 @@
+// Host-side driver of the graph compiler and image validator, built with
+// AddressSanitizer and UndefinedBehaviorSanitizer by tests/test_sanitize_cpu.py
+// (no GPU code is involved: compiler.cpp and errors.cpp only).
+//
+// It compiles random phrase lists (empty lists, duplicates, nested and long
+// phrases, case classes, several reading flags and thread counts), checks
+// that every compiled image validates, corrupts images byte by byte and
+// checks that validation rejects or accepts them without any memory error,
+// and drives every documented argument error of tb_compile_graphs.
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <random>
+#include <vector>
+
+#include "../../include/tbias.h"
+
+namespace {
+
+int g_fail = 0;
+
+void expect(bool ok, const char* what) {
+  if (!ok) {
+    std::fprintf(stderr, "FAIL: %s (%s)\n", what, tb_last_error());
+    ++g_fail;
+  }
+}
+
+struct Lists {
+  std::vector<int64_t> mp{0}, tp{0};
+  std::vector<int32_t> tok;
+  void add_model(const std::vector<std::vector<int32_t>>& phrases) {
+    for (const auto& p : phrases) {
+      tok.insert(tok.end(), p.begin(), p.end());
+      tp.push_back((int64_t)tok.size());
+    }
+    mp.push_back((int64_t)tp.size() - 1);
+  }
+  int32_t n_models() const { return (int32_t)mp.size() - 1; }
+};
+
+std::vector<int32_t> class_map(int32_t V, int32_t n_case) {
+  std::vector<int32_t> cm(V + 1);
+  for (int32_t v = 0; v < V; ++v) cm[v] = (v < 3 * n_case) ? v % n_case : v;
+  cm[V] = -1;
+  return cm;
+}
+
+tb_graphs* compile(const Lists& L, const std::vector<int32_t>& cm, int32_t sem, int32_t threads,
+                   int* rc) {
+  std::vector<float> w(L.n_models(), 1.0f), be(L.n_models(), 2.0f), sc(L.n_models(), 1.5f);
+  tb_graphs* g = nullptr;
+  *rc = tb_compile_graphs(L.n_models(), L.mp.data(), L.tp.data(),
+                          L.tok.empty() ? nullptr : L.tok.data(), w.data(), be.data(),
+                          (threads & 1) ? sc.data() : nullptr, cm.data(), (int32_t)cm.size(), sem,
+                          threads, &g);
+  return g;
+}
+
+void random_models(std::mt19937& rng) {
+  std::uniform_int_distribution<int> nm(1, 6), np(0, 40), plen(1, 14);
+  const int32_t V = 40 + (int32_t)(rng() % 300);
+  const int32_t n_case = 1 + (int32_t)(rng() % (V / 3));
+  std::uniform_int_distribution<int32_t> tokd(0, V - 1), small(0, 5);
+  const auto cm = class_map(V, n_case);
+  Lists L;
+  const int M = nm(rng);
+  for (int m = 0; m < M; ++m) {
+    std::vector<std::vector<int32_t>> ph;
+    const int n = (m == 0) ? 0 : np(rng);  // model 0: an empty list
+    for (int i = 0; i < n; ++i) {
+      std::vector<int32_t> p(plen(rng));
+      const bool narrow = (rng() & 3) == 0;   // few symbols: deep shared prefixes
+      for (auto& t : p) t = narrow ? small(rng) : tokd(rng);
+      ph.push_back(p);
+      if ((rng() & 7) == 0) ph.push_back(p);  // duplicates
+      if ((rng() & 7) == 0 && p.size() > 1)   // nested prefixes
+        ph.push_back(std::vector<int32_t>(p.begin(), p.begin() + p.size() / 2));
+    }
+    L.add_model(ph);
+  }
+  for (int32_t sem = 0; sem < 2; ++sem) {
+    int rc = 0;
+    tb_graphs* g = compile(L, cm, sem, 1 + (int32_t)(rng() % 4), &rc);
+    expect(rc == TB_OK && g, "compile random models");
+    if (!g) continue;
+    tb_arena_layout lay;
+    expect(tb_graphs_layout(g, &lay) == TB_OK, "layout");
+    std::vector<unsigned char> img(lay.total_bytes);
+    expect(tb_graphs_host_image(g, img.data(), lay.total_bytes) == TB_OK, "host image");
+    expect(tb_graphs_host_image(g, img.data(), lay.total_bytes - 1) != TB_OK, "short buffer");
+    expect(tb_validate_image(img.data(), &lay) == TB_OK, "validate compiled image");
+    // corrupt single words: validation must never read out of bounds
+    std::uniform_int_distribution<int64_t> pos(0, lay.total_bytes / 4 - 1);
+    for (int k = 0; k < 64; ++k) {
+      std::vector<unsigned char> bad = img;
+      const int64_t i = pos(rng);
+      const uint32_t vals[] = {0xffffffffu, 0x7fffffffu, 0x80000000u, 0u, (uint32_t)rng()};
+      std::memcpy(bad.data() + 4 * i, &vals[rng() % 5], 4);
+      const int r = tb_validate_image(bad.data(), &lay);
+      expect(r == TB_OK || r == TB_ERANGE, "validate corrupted image returns a status");
+    }
+    tb_graphs_free(g);
+  }
+}
+
+void argument_errors() {
+  const int32_t V = 50;
+  const auto cm = class_map(V, 10);
+  Lists L;
+  L.add_model({{1, 2, 3}, {4}});
+  int rc = 0;
+  tb_graphs* g = compile(L, cm, 0, 1, &rc);
+  expect(rc == TB_OK, "valid compile");
+  tb_graphs_free(g);
+
+  std::vector<float> one(1, 1.0f);
+  tb_graphs* out = nullptr;
+  auto call = [&](int32_t n, const int64_t* mp, const int64_t* tp, const int32_t* tk,
+                  const int32_t* c, int32_t v1, int32_t sem, tb_graphs** o) {
+    return tb_compile_graphs(n, mp, tp, tk, one.data(), one.data(), nullptr, c, v1, sem, 1, o);
+  };
+  expect(call(1, L.mp.data(), L.tp.data(), L.tok.data(), cm.data(), V + 1, 0, nullptr) ==
+             TB_EINVAL, "NULL out");
+  expect(call(0, L.mp.data(), L.tp.data(), L.tok.data(), cm.data(), V + 1, 0, &out) ==
+             TB_EINVAL, "no models");
+  expect(call(1, nullptr, L.tp.data(), L.tok.data(), cm.data(), V + 1, 0, &out) == TB_EINVAL,
+         "NULL model_phrase_ptr");
+  expect(call(1, L.mp.data(), L.tp.data(), L.tok.data(), cm.data(), 1, 0, &out) == TB_EINVAL,
+         "v_plus_blank < 2");
+  expect(call(1, L.mp.data(), L.tp.data(), L.tok.data(), cm.data(), V + 1, 7, &out) ==
+             TB_EINVAL, "unknown reading");
+  std::vector<int64_t> dec_tp = {0, 3, 2};  // a decreasing CSR
+  expect(call(1, L.mp.data(), dec_tp.data(), L.tok.data(), cm.data(), V + 1, 0, &out) ==
+             TB_EINVAL, "non-monotone phrase_tok_ptr");
+  std::vector<int32_t> tk = {1, 2, 3, V};  // token == V (the blank)
+  std::vector<int64_t> tp = {0, 3, 4}, mp = {0, 2};
+  expect(call(1, mp.data(), tp.data(), tk.data(), cm.data(), V + 1, 0, &out) == TB_ERANGE,
+         "blank in a phrase");
+  tk[3] = -1;
+  expect(call(1, mp.data(), tp.data(), tk.data(), cm.data(), V + 1, 0, &out) == TB_ERANGE,
+         "negative token");
+  std::vector<int64_t> tp_empty = {0, 3, 3};
+  tk[3] = 4;
+  expect(call(1, mp.data(), tp_empty.data(), tk.data(), cm.data(), V + 1, 0, &out) ==
+             TB_ERANGE, "empty phrase");
+  auto cm2 = cm;
+  cm2[4] = -1;  // a non-blank token without a class cannot be in a phrase
+  expect(call(1, mp.data(), tp.data(), tk.data(), cm2.data(), V + 1, 0, &out) == TB_ERANGE,
+         "classless token");
+  cm2 = cm;
+  cm2[7] = V + 3;  // class id outside [0, V)
+  expect(call(1, mp.data(), tp.data(), tk.data(), cm2.data(), V + 1, 0, &out) == TB_ERANGE,
+         "class out of range");
+}
+
+}  // namespace
+
+int main() {
+  std::mt19937 rng(12345);
+  for (int i = 0; i < 60; ++i) random_models(rng);
+  argument_errors();
+  if (g_fail) {
+    std::fprintf(stderr, "%d failures\n", g_fail);
+    return 1;
+  }
+  std::printf("sanitized compiler driver: ok\n");
+  return 0;
+}

@@ -302,3 +302,83 @@ def test_state_records_unpack_to_the_oracle_graph(name, streams):
                 assert w2 & 0xff == len(mem)
                 ms = w1 >> 16
                 assert list(A["cls_tok"][ms:ms + len(mem)]) == mem
+
+
+def _fake_arena(cfg):
+    cm = W.class_map(cfg)
+    mp, tp, tk = W.phrase_csr(W.phrases(cfg, [0]))
+    g = capi.tb_compile_graphs(mp, tp, tk, 1.0, 2.0, cm)
+    ar = capi.tb_arena()
+    ar.base = 0x10000       # never dereferenced: the binding rejects before any call
+    ar.layout = g.layout
+    return capi.Arena(None, ar)
+
+
+def test_binding_rejects_mismatched_sizes_before_any_call():
+    """The kernels trust buffer sizes; the binding checks them first (host
+    tensors are used here: every check runs before the device-pointer check)."""
+    import torch
+    cfg = W.config_by_name("tiny")
+    arena = _fake_arena(cfg)
+    T, B, V1 = 5, 3, cfg.Vp1
+    i32 = lambda *s: torch.zeros(s, dtype=torch.int32)
+    f32 = lambda *s: torch.zeros(s, dtype=torch.float32)
+
+    def greedy(logits=None, mids=None, st=None, tok=None, sst=None, sc=None, **kw):
+        capi.tb_boost_step_greedy(arena, f32(T, B, V1) if logits is None else logits,
+                                  i32(B) if mids is None else mids, i32(B) if st is None else st,
+                                  i32(T, B) if tok is None else tok,
+                                  i32(T, B) if sst is None else sst,
+                                  f32(T, B) if sc is None else sc, **kw)
+
+    cases = [
+        (dict(logits=f32(T, B, V1 + 1)), r"V\+1"),
+        (dict(logits=f32(T, B, 2, V1)), "K = 1"),
+        (dict(mids=i32(B + 1)), "model_ids"),
+        (dict(st=i32(B - 1)), "states"),
+        (dict(tok=i32(T - 1, B)), "out_tok"),
+        (dict(sst=i32(T, B - 1)), "out_state"),
+        (dict(sc=f32(2)), "out_score"),
+        (dict(T=T + 1), "outside"),
+        (dict(B=B + 1), "differs"),
+        (dict(row_stride=V1 + 3), "row_stride"),
+    ]
+    for kw, msg in cases:
+        with pytest.raises(ValueError, match=msg):
+            greedy(**kw)
+    with pytest.raises(ValueError, match="device tensor"):   # every size check passed
+        greedy()
+
+    K = 4
+
+    def beam(logits=None, st=None, S=None, outs=None):
+        o = outs if outs is not None else [i32(T, B, K), i32(T, B, K), i32(T, B, K),
+                                           f32(T, B, K), f32(T, B, K)]
+        capi.tb_boost_step_beam(arena, f32(T, B, K, V1) if logits is None else logits, i32(B),
+                                i32(B * K) if st is None else st, f32(B * K) if S is None else S,
+                                *o)
+
+    bcases = [
+        (dict(logits=f32(T, B, K, V1 - 1)), r"V\+1"),
+        (dict(logits=f32(T, B, V1)), r"\[T, B, K, V\+1\]"),
+        (dict(st=i32(B)), "states"),
+        (dict(S=f32(B * K + 1)), "scores"),
+        (dict(outs=[i32(T, B, K), i32(T, B, K - 1), i32(T, B, K), f32(T, B, K), f32(T, B, K)]),
+         "out_parent"),
+        (dict(outs=[i32(T, B, K), i32(T, B, K), i32(T, B, K), f32(T, B, K), f32(1)]), "out_cum"),
+    ]
+    for kw, msg in bcases:
+        with pytest.raises(ValueError, match=msg):
+            beam(**kw)
+    with pytest.raises(ValueError, match="device tensor"):
+        beam()
+
+
+def test_debug_hooks_validate_their_arguments():
+    assert capi.LIB.tb_debug_select_kernels(2, 0) == capi.TB_EINVAL
+    assert capi.LIB.tb_debug_select_kernels(0, 3) == capi.TB_EINVAL
+    assert capi.LIB.tb_debug_select_kernels(-1, 0) == capi.TB_EINVAL
+    with capi.kernels(greedy=capi.GREEDY_REF, beam=capi.BEAM_NO_PIPE):
+        pass
+    assert capi.LIB.tb_debug_select_kernels(0, 0) == capi.TB_OK
+    assert capi.LIB.tb_debug_set_spin_limit(0) == capi.TB_OK

@@ -2,29 +2,33 @@
 
 Every workload runs at its full size on the device, in the launch pattern the
 benchmark uses (streaming chunks of 16 for the streaming workload, one call
-per workload otherwise). The oracle recomputes a sample of streams one by one
-(all streams where it is cheap). Bar: selected tokens, graph states and beam
-parents bit-exact; accumulated beam scores bit-exact; per-step fused scores
-within 1e-5 absolute.
+per workload otherwise), and the oracle recomputes every stream (in at most 16
+worker processes). Bar: selected tokens, graph states and beam parents
+bit-exact; accumulated beam scores bit-exact; per-step fused scores within
+1e-5 absolute.
 """
+
+import os
 
 import numpy as np
 import pytest
 
 import oracle
 import workloads as W
+from paper_2608_21343_amd import capi
 from tests.gpu_cases import (compare_beam, compare_greedy, device_rows, gpu_beam,
-                             gpu_greedy, oracle_graphs, say)
+                             gpu_greedy, oracle_all_streams, oracle_graphs, say, spill_path)
 
 pytestmark = pytest.mark.gpu
 
 ATOL = 1e-5
 
 
-def _sample(B):
-    if B <= 32:
-        return list(range(B))
-    return sorted({0, 1, B // 5, B // 3, B // 2, (2 * B) // 3, B - 2, B - 1})
+@pytest.fixture
+def restore_kernels():
+    """Tests that force a kernel family leave the automatic choice behind them."""
+    yield
+    capi.tb_debug_select_kernels(capi.GREEDY_AUTO, capi.BEAM_AUTO)
 
 
 def _decoder(cfg, lists):
@@ -32,46 +36,41 @@ def _decoder(cfg, lists):
     return BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
 
 
-@pytest.mark.parametrize("name", ["tiny", "batched", "streaming", "stress_greedy"])
-def test_greedy_full_size(name):
+def _full_size(name, run):
+    """Full workload on the device in its launch pattern, the oracle on every stream."""
     cfg = W.config_by_name(name)
-    streams = _sample(cfg.B)
-    say(f"[parity] greedy {name}: generating B={cfg.B} T={cfg.T} V+1={cfg.Vp1} {cfg.dtype}")
+    say(f"[parity] {name}: generating B={cfg.B} K={cfg.K} T={cfg.T} V+1={cfg.Vp1} {cfg.dtype}")
     lists = W.phrases(cfg)
     dec = _decoder(cfg, lists)
     mids = W.model_ids(cfg)
-    dev, keep = device_rows(cfg, streams)
-    say(f"[parity] greedy {name}: running HIP path, chunk={cfg.chunk}")
-    gpu = gpu_greedy(dec, dev[:, :, 0, :], mids, cfg.chunk)
-    del dev
-    graphs = oracle_graphs(cfg, lists, streams, mids)
-    say(f"[parity] greedy {name}: oracle on streams {streams}")
-    sub = mids[streams]
-    ref = oracle.greedy_decode(graphs, sub, keep, np.zeros(len(streams), np.int32))
-    err = compare_greedy(gpu, ref, streams, ATOL, ref_streams=range(len(streams)))
-    assert np.array_equal(gpu[3][streams], ref[3])
-    say(f"[parity] greedy {name}: ok, max score error {err:.2e}")
+    path = spill_path(name)
+    try:
+        dev, _ = device_rows(cfg, [], spill=path)
+        say(f"[parity] {name}: running HIP path, chunk={cfg.chunk}")
+        gpu = run(dec, dev, mids, cfg.chunk)
+        del dev
+        say(f"[parity] {name}: oracle on all {cfg.B} streams")
+        ref = oracle_all_streams(cfg, path)
+    finally:
+        if os.path.exists(path):
+            os.remove(path)
+    return cfg, gpu, ref
+
+
+@pytest.mark.parametrize("name", ["tiny", "batched", "streaming", "stress_greedy"])
+def test_greedy_full_size(name):
+    cfg, gpu, ref = _full_size(name, lambda dec, dev, mids, ch: gpu_greedy(dec, dev[:, :, 0, :],
+                                                                          mids, ch))
+    err = compare_greedy(gpu, ref, range(cfg.B), ATOL)
+    assert np.array_equal(gpu[3], ref[3]), "carried states differ"
+    say(f"[parity] greedy {name}: ok on all {cfg.B} streams, max score error {err:.2e}")
 
 
 @pytest.mark.parametrize("name", ["beam", "stress_beam"])
 def test_beam_full_size(name):
-    cfg = W.config_by_name(name)
-    streams = _sample(cfg.B)[:4] if cfg.V > 2000 else _sample(cfg.B)[:6]
-    say(f"[parity] beam {name}: generating B={cfg.B} K={cfg.K} T={cfg.T} V+1={cfg.Vp1}")
-    lists = W.phrases(cfg)
-    dec = _decoder(cfg, lists)
-    mids = W.model_ids(cfg)
-    dev, keep = device_rows(cfg, streams)
-    say(f"[parity] beam {name}: running HIP path")
-    gpu = gpu_beam(dec, dev, mids, cfg.chunk)
-    del dev
-    graphs = oracle_graphs(cfg, lists, streams, mids)
-    say(f"[parity] beam {name}: oracle on streams {streams}")
-    sub = mids[streams]
-    st0, S0 = oracle.init_carry(sub, cfg.K)
-    ref = oracle.beam_decode(graphs, sub, keep, st0, S0)
-    err = compare_beam(gpu, ref, streams, ATOL, ref_streams=range(len(streams)))
-    say(f"[parity] beam {name}: ok, max step score error {err:.2e}")
+    cfg, gpu, ref = _full_size(name, gpu_beam)
+    err = compare_beam(gpu, ref, range(cfg.B), ATOL)
+    say(f"[parity] beam {name}: ok on all {cfg.B} streams, max step score error {err:.2e}")
 
 
 def _small_case(seed=0, B=6, V=200, n_case=20, T=64, K=1, dtype="f32"):
@@ -205,12 +204,11 @@ def test_stream_permutation_permutes_outputs():
         assert np.array_equal(a[:, perm], b)
 
 
-@pytest.mark.parametrize("kernel", ["seg", "pipe"])
 @pytest.mark.parametrize("name,T,chunk", [("tiny", 50, 50), ("batched", 500, 500),
                                           ("streaming", 1024, 1024), ("streaming", 200, 37),
                                           ("streaming", 96, 16), ("batched", 40, 7)])
-def test_greedy_kernels_agree_with_reference_kernel(kernel, name, T, chunk, monkeypatch):
-    """The segmented and pipelined kernels give the reference kernel's outputs:
+def test_greedy_kernels_agree_with_reference_kernel(name, T, chunk):
+    """The segmented and short-call kernels give the reference kernel's outputs:
     tokens, states and carries identical, scores within rounding of the
     normaliser. Whole-length calls make the segmented kernel split streams
     over several workgroups and run its boundary fix-up; calls of at most 16
@@ -225,11 +223,10 @@ def test_greedy_kernels_agree_with_reference_kernel(kernel, name, T, chunk, monk
         mids[1] = -1
     dev = to_device_logits(rows[:, :, 0, :])
     del rows
-    say(f"[agree] {kernel} vs ref: {name} T={T} chunk={chunk}")
-    monkeypatch.setenv("TBIAS_GREEDY_KERNEL", kernel)
+    say(f"[agree] seg vs ref: {name} T={T} chunk={chunk}")
     out = gpu_greedy(dec, dev, mids, chunk)
-    monkeypatch.setenv("TBIAS_GREEDY_KERNEL", "ref")
-    ref = gpu_greedy(dec, dev, mids, chunk)
+    with capi.kernels(greedy=capi.GREEDY_REF):
+        ref = gpu_greedy(dec, dev, mids, chunk)
     bad = np.nonzero(out[0] != ref[0])
     assert bad[0].size == 0, f"token mismatch at (t, b) {list(zip(*bad))[:5]}"
     assert np.array_equal(out[1], ref[1]) and np.array_equal(out[3], ref[3])
@@ -397,17 +394,16 @@ def test_chunk_loop_graph_replay_matches_eager():
             assert torch.equal(a, b), f"replay {rep} differs from the eager run"
 
 
-BEAM_KERNEL_ENV = {"default": None, "wide": "nopipe", "ref": "ref"}
+BEAM_KERNEL = {"default": capi.BEAM_AUTO, "wide": capi.BEAM_NO_PIPE, "ref": capi.BEAM_REF}
 
 
 @pytest.mark.parametrize("kernel", ["default", "ref"])
 @pytest.mark.parametrize("K,dtype", [(2, "f32"), (3, "bf16"), (8, "f32")])
-def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, monkeypatch):
+def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, restore_kernels):
     """Every beam kernel against the oracle: ragged V+1 = 301, model -1, an
     empty list and an out-of-range id (decoded unbiased, states -2)."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if BEAM_KERNEL_ENV[kernel]:
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
     cfg, lists, rows = _small_case(6, B=6, V=300, K=K, T=40, dtype=dtype)
     lists = list(lists[:4]) + [[]]
     dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
@@ -428,12 +424,11 @@ def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, monkeypatc
 
 
 @pytest.mark.parametrize("kernel", ["default", "ref"])
-def test_beam_inside_long_phrases(kernel, monkeypatch):
+def test_beam_inside_long_phrases(kernel, restore_kernels):
     """Beam hypotheses deep inside 40-token phrases (chains of several suffix
     states, override sets of dozens of classes)."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if BEAM_KERNEL_ENV[kernel]:
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
     V, B, T, K = 64, 4, 200, 4
     cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
     phrase = list(range(1, 41))
@@ -455,7 +450,7 @@ def test_beam_inside_long_phrases(kernel, monkeypatch):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_wide_vocabulary_mixed_streams_and_chunks(dtype, monkeypatch):
+def test_wide_vocabulary_mixed_streams_and_chunks(dtype, restore_kernels):
     """Wide rows (V+1 = 3001, not a multiple of 256): the workgroup-segmented
     kernel against the oracle with model -1, an empty list and an
     out-of-range id, for whole calls (several segments per stream and the
@@ -486,8 +481,8 @@ def test_wide_vocabulary_mixed_streams_and_chunks(dtype, monkeypatch):
         z = oracle.widen(rows[:, 4, 0, :])
         assert np.array_equal(gpu[0][:, 4], np.argmax(z, axis=1))
         outs[chunk] = gpu
-    monkeypatch.setenv("TBIAS_GREEDY_KERNEL", "ref")
-    r = gpu_greedy(dec, dev, mids, 96)
+    with capi.kernels(greedy=capi.GREEDY_REF):
+        r = gpu_greedy(dec, dev, mids, 96)
     assert np.array_equal(outs[96][0], r[0]) and np.array_equal(outs[96][1], r[1])
     assert np.array_equal(outs[96][3], r[3])
 
@@ -515,13 +510,12 @@ def test_wide_vocabulary_segments_inside_long_phrases():
 
 @pytest.mark.parametrize("kernel", ["default", "wide"])
 @pytest.mark.parametrize("K,dtype", [(3, "f32"), (4, "bf16"), (8, "bf16")])
-def test_wide_vocabulary_beam_mixed_streams(kernel, K, dtype, monkeypatch):
+def test_wide_vocabulary_beam_mixed_streams(kernel, K, dtype, restore_kernels):
     """Beam kernels on wide rows (V+1 = 3001) against the oracle: model -1, an
     empty list and an out-of-range id (decoded unbiased, states -2), chunked
     calls equal one call, and the reference kernel agrees."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if BEAM_KERNEL_ENV[kernel]:
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
     cfg = W.Config(108, "small", B=6, K=K, V=3000, T=40, chunk=40, dtype=dtype, n_phrases=200,
                    len_lo=1, len_hi=6, token_dist="zipf", zipf_s=1.1, logit_std=1.5,
                    blank_offset=0.0, n_case=300)
@@ -546,20 +540,19 @@ def test_wide_vocabulary_beam_mixed_streams(kernel, K, dtype, monkeypatch):
         out = gpu_beam(dec, dev, mids, ch)
         for a, b in zip(gpu, out):
             assert np.array_equal(a, b), f"chunk {ch} differs"
-    monkeypatch.setenv("TBIAS_BEAM_KERNEL", "ref")
-    r = gpu_beam(dec, dev, mids, 40)
+    with capi.kernels(beam=capi.BEAM_REF):
+        r = gpu_beam(dec, dev, mids, 40)
     for i in range(5):
         assert np.array_equal(gpu[i], r[i]) if i != 3 else np.max(np.abs(gpu[3] - r[3])) <= 1e-6
 
 
 @pytest.mark.parametrize("kernel", ["default", "ref"])
 @pytest.mark.parametrize("K", [1, 4, 7])
-def test_beam_tiny_vocabulary(kernel, K, monkeypatch):
+def test_beam_tiny_vocabulary(kernel, K, restore_kernels):
     """V+1 = 8 with K up to 7: fewer root moves than a row list holds, most
     candidates of a step in the K best, ties between equal logits."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if BEAM_KERNEL_ENV[kernel]:
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
     V, B, T = 7, 3, 30
     cm = np.array([0, 0, 2, 3, 3, 5, 6, -1], np.int32)
     lists = [[[0, 2], [3, 5, 6], [2]], [[6, 6, 6]], []]
@@ -578,13 +571,12 @@ def test_beam_tiny_vocabulary(kernel, K, monkeypatch):
 
 @pytest.mark.parametrize("kernel", ["default", "wide"])
 @pytest.mark.parametrize("K,dtype", [(4, "bf16"), (2, "f32")])
-def test_wide_vocabulary_beam_inside_long_phrases(kernel, K, dtype, monkeypatch):
+def test_wide_vocabulary_beam_inside_long_phrases(kernel, K, dtype, restore_kernels):
     """Wide rows (V+1 = 2601) with hypotheses deep inside 40-token phrases
     whose tokens have the largest logits: most of a row's listed root moves
     are overridden, so the helper-wave kernel rescans rows too."""
     from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    if BEAM_KERNEL_ENV[kernel]:
-        monkeypatch.setenv("TBIAS_BEAM_KERNEL", BEAM_KERNEL_ENV[kernel])
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
     V, B, T = 2600, 4, 120
     cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
     phrase = list(range(1, 41))
