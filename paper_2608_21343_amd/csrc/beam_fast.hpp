@@ -1,26 +1,46 @@
-// Boosted beam step for V+1 <= 64*PER: one workgroup per stream, one wave per
+// Boosted beam step for V+1 <= 64*PER: a row-preparation kernel over every
+// row of the call, then one workgroup per stream with one wave per
 // hypothesis (templates; instantiated per chunk count in beam_fast_*.hip).
 //
-// Per step, wave k takes hypothesis k and its own logit row [t, b, k] (the
-// row of a slot does not depend on the selection, so the next step's row is
-// prefetched while this one is scored):
+// Part of a beam step does not depend on the hypotheses: a slot reads its own
+// row [t, b, k] whatever the selection was, so the row's normaliser and its
+// best root moves can be taken for every row of the call at once, on every
+// CU, before the sequential part starts. beam_prep_kernel does that, one wave
+// per row:
 //
-//  * the row's normaliser: max in float32, sum of exponentials and log in
-//    float64, rounded once to float32 (beam scores are carried and compared,
-//    so they follow the exact reading);
+//  * the normaliser: max in float32, sum of exponentials and log in float64,
+//    rounded once to float32 (beam scores are carried and compared, so they
+//    follow the exact reading);
+//  * the kList best root moves y = z + psi(root move) of the row in (y
+//    descending, token ascending) order, over every token of the row (the
+//    root-move psi of the stream's model; zero for unbiased streams).
+//
+// It stores them in the call's own output rows of that (t, b, k): out_step
+// holds the normaliser and out_tok, out_parent, out_state and out_cum two
+// 16-bit token ids each. The step kernel reads a row's entries one step ahead
+// (wave k reads only row k, and writes row k's outputs afterwards), so the
+// call needs no workspace.
+//
+// Per step, wave k takes hypothesis k:
+//
 //  * c_k = (S_k - lse_k) - phi(s_k), and the candidates c_k + key over the row:
 //    root moves z + psi(root move) from registers (tokens whose class is
 //    overridden in s_k excluded through a class-mark table), the override
 //    members of the classes of the children along s_k's suffix chain (deepest
 //    state first) listed in LDS, and the blank c_k + z[V] + phi(s_k);
 //  * the K best of all K*(V+1) candidates (larger first, ties to the lower
-//    flat index k*(V+1)+v): every wave's K-th largest lane maximum bounds the
-//    K-th best from below; the largest bound theta is taken, every candidate
-//    >= theta is compacted into LDS and one wave selects the K best exactly.
-//    When too many candidates tie at theta, K rounds of a workgroup argmax
-//    select them instead;
+//    flat index k*(V+1)+v): the listed root moves of every slot whose class
+//    is not overridden are real candidates, so the K-th largest of them,
+//    theta, bounds the K-th best from below; every candidate >= theta is
+//    compacted into LDS and ranked exactly. When fewer than K listed moves
+//    remain, or too many candidates reach theta, K rounds of a workgroup
+//    argmax select the K best instead;
 //  * slot j takes the j-th best: its parent, token, advanced state (blank
 //    keeps it), step score (z - lse) + boost and cumulative score.
+//
+// Graph records: every state of the model (up to the LDS budget) as a packed
+// 12-byte record with the model's psi and phi value tables in LDS, so the
+// sequential part of a step reads no arena memory.
 #pragma once
 
 #include <climits>
@@ -31,13 +51,16 @@
 namespace tbias {
 namespace beamk {
 
-using seg::HotRecords;
 using seg::kNegInf;
 using seg::RowShape;
+using seg::StateHot;
 using seg::Tables;
 
 constexpr int kOverCap = 256;  // override members listed per hypothesis
 constexpr int kCandCap = 128;  // candidates compacted for the final selection (multiple of 8)
+constexpr int kList = 8;       // best root moves listed per row by beam_prep_kernel
+constexpr int kPrepThreads = 256;
+constexpr uint32_t kNoTok = 0xffffu;
 
 template <int PER, int MAXK>
 struct alignas(16) BeamFixed {
@@ -54,7 +77,7 @@ struct alignas(16) BeamFixed {
   float hyp_S[2][MAXK];
   float hyp_lse[MAXK];
   float hyp_phi[MAXK];
-  float theta_w[MAXK * MAXK];  // every wave's K largest lane maxima
+  float listed[MAXK * kList];  // candidates of every slot's listed root moves
   int32_t cnt_w[MAXK];
   float sel_val[MAXK];
   int32_t sel_f[MAXK];
@@ -69,15 +92,15 @@ struct alignas(16) BeamFixed {
 template <int PER, int MAXK>
 constexpr int beam_hot() {
   const int budget = 160 * 1024 - 1024;
-  const int room = (budget - (int)sizeof(BeamFixed<PER, MAXK>)) / seg::kHotRecordBytes;
+  const int room = (budget - (int)sizeof(BeamFixed<PER, MAXK>) - 2048) / seg::kStateHotBytes;
   const int h = (room / 64) * 64;
-  return h > 4096 ? 4096 : (h < 0 ? 0 : h);
+  return h > 8192 ? 8192 : (h < 0 ? 0 : h);
 }
 
 template <int PER, int MAXK>
 struct alignas(16) BeamLds : BeamFixed<PER, MAXK> {
   static constexpr int HOT = beam_hot<PER, MAXK>() > 64 ? beam_hot<PER, MAXK>() : 64;
-  HotRecords<HOT> hot;
+  StateHot<HOT> hot;
 };
 
 // Exclusive prefix sum over the lanes of a wave (lane i gets the sum of lanes
@@ -100,6 +123,156 @@ __device__ __forceinline__ bool cbetter(float a, int32_t fa, float b, int32_t fb
   return a > b || (a == b && fa < fb);
 }
 
+// Float order as unsigned integers (larger float, larger key; -0 below +0).
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float from_order_key(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// The n-th largest lane value of the wave, counting equal values separately
+// (n >= 1): bitwise search for the largest key t with at least n lanes >= t.
+__device__ __forceinline__ float wave_nth_largest(float x, int32_t n) {
+  const uint32_t k = order_key(x);
+  uint32_t t = 0u;
+#pragma unroll
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    if ((int32_t)__builtin_popcountll(__ballot(k >= c)) >= n) t = c;
+  }
+  return from_order_key(t);
+}
+
+// The state-independent part of every beam row of a call (see above): one
+// wave per row (t, b, k), rows in (t*B + b)*K + k order.
+template <class Ld, int PER>
+__global__ __launch_bounds__(kPrepThreads) void beam_prep_kernel(
+    ArenaView A, const typename Ld::T* __restrict__ logits, int64_t n_rows, int32_t B,
+    int32_t K, int64_t stride, const int32_t* __restrict__ model_ids,
+    const int32_t* __restrict__ states, int32_t* __restrict__ out_tok,
+    int32_t* __restrict__ out_parent, int32_t* __restrict__ out_state,
+    float* __restrict__ out_step, float* __restrict__ out_cum) {
+  const int lane = __lane_id();
+  const int64_t r = (int64_t)blockIdx.x * (kPrepThreads / 64) + (threadIdx.x >> 6);
+  if (r >= n_rows) return;  // uniform per wave; no barrier follows
+  const int32_t V1 = A.V1, V = V1 - 1;
+  const int32_t b = (int32_t)((r / K) % B);
+  // the step kernel's decision: biased when the model id and every carried
+  // state of the stream are in range
+  const int32_t m = model_ids[b];
+  bool biased = m >= 0 && m < A.n_models;
+  if (biased) {
+    const int32_t n = A.model_n[m];
+    const int32_t s = (lane < K) ? states[(int64_t)b * K + lane] : 0;
+    biased = __ballot(s < 0 || s >= n) == 0ull;
+  }
+  const RowShape<PER> rs(V1);
+  float z[PER];
+  seg::load_row<Ld, PER>(z, logits + r * stride, rs);
+  const float* gpsi = A.root_psi + (int64_t)(biased ? m : 0) * V1;
+
+  // normaliser (as the one-wave-per-row kernels always took it)
+  float zmax = kNegInf;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const float zj = (j < PER - 1 || rs.last_ok) ? z[j] : kNegInf;
+    zmax = __builtin_fmaxf(zmax, zj);
+  }
+  zmax = wave_max_dpp(zmax);
+  double se = 0.0;
+  const double zmd = (double)zmax;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const bool ok = (j < PER - 1) || rs.last_ok;
+    se += ok ? exp_nonpos((double)z[j] - zmd) : 0.0;
+  }
+  se = wave_sum_d(se);
+  const float lse = (float)(zmd + log(se));
+
+  // root-move keys, then the kList best in (key, token) order
+  float y[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int32_t v = (j < PER - 1) ? 64 * j + lane : rs.last_idx;
+    const bool ok = ((j < PER - 1) || rs.last_ok) && v < V;
+    y[j] = ok ? z[j] + (biased ? gpsi[v] : 0.f) : kNegInf;
+  }
+  // theta: the kList-th largest lane maximum; kList lanes hold a move >= theta,
+  // so every listed move is >= theta. The moves >= theta (few) are gathered
+  // in LDS and ranked in (key, token) order.
+  __shared__ float g_key[kPrepThreads / 64][64];
+  __shared__ int32_t g_tok[kPrepThreads / 64][64];
+  const int wv = threadIdx.x >> 6;
+  float lm = kNegInf;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) lm = __builtin_fmaxf(lm, y[j]);
+  const float theta = wave_nth_largest(lm, kList);
+  int32_t cnt = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) cnt += (theta > kNegInf && y[j] >= theta) ? 1 : 0;
+  int32_t total;
+  int32_t pos = wave_excl_scan(cnt, total);
+  uint32_t words[kList / 2] = {0u, 0u, 0u, 0u};
+  if (theta > kNegInf && total <= 64) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      if (y[j] >= theta) {
+        g_key[wv][pos] = y[j];
+        g_tok[wv][pos] = (j == PER - 1) ? rs.last_idx : 64 * j + lane;
+        ++pos;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+    const float ki = (lane < total) ? g_key[wv][lane] : kNegInf;
+    const int32_t ti = (lane < total) ? g_tok[wv][lane] : INT_MAX;
+    int32_t rank = 0;
+    for (int32_t q = 0; q < total; ++q) {
+      const float kq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ki), q));
+      const int32_t tq = __builtin_amdgcn_readlane(ti, q);
+      rank += (kq > ki || (kq == ki && tq < ti)) ? 1 : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < kList; ++i) {
+      const uint64_t who = __ballot(lane < total && rank == i);
+      const uint32_t tok =
+          who ? (uint32_t)__builtin_amdgcn_readlane(ti, (int32_t)__builtin_ctzll(who)) : kNoTok;
+      words[i >> 1] |= tok << (16 * (i & 1));
+    }
+  } else {
+    // fewer than kList finite moves, or very many equal keys: kList rounds
+    // of a wave argmax
+    uint32_t taken = 0u;
+#pragma unroll
+    for (int i = 0; i < kList; ++i) {
+      float bk = kNegInf;
+      int32_t bj = -1;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        const bool gt = !((taken >> j) & 1u) && y[j] > bk;
+        bk = gt ? y[j] : bk;
+        bj = gt ? j : bj;
+      }
+      const int32_t idx = (bj < 0) ? INT_MAX : ((bj == PER - 1) ? rs.last_idx : 64 * bj + lane);
+      float wk;
+      int32_t wt;
+      wave_argmax_dpp(bj < 0 ? kNegInf : bk, idx, wk, wt);
+      const bool none = !(wk > kNegInf);
+      if (!none && idx == wt) taken |= 1u << bj;
+      const uint32_t tok = none ? kNoTok : (uint32_t)wt;
+      words[i >> 1] |= tok << (16 * (i & 1));
+    }
+  }
+  if (lane == 0) {
+    out_step[r] = lse;
+    out_tok[r] = (int32_t)words[0];
+    out_parent[r] = (int32_t)words[1];
+    out_state[r] = (int32_t)words[2];
+    out_cum[r] = __uint_as_float(words[3]);
+  }
+}
+
 template <class Ld, int PER, int MAXK>
 __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int32_t K,
@@ -115,6 +288,8 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   const int32_t b = blockIdx.x;
   const int64_t tstride = (int64_t)B * K * stride;  // row (t, b, w) = base + t * tstride
   const typename Ld::T* base = logits + ((int64_t)b * K + w) * stride;
+  const int64_t ostride = (int64_t)B * K;  // output / row-summary entry (t, b, w) = o0 + t * ostride
+  const int64_t o0 = (int64_t)b * K + w;
 
   const int32_t m = model_ids[b];
   int mode = (m == -1) ? 0 : ((m < -1 || m >= A.n_models) ? -1 : 1);
@@ -134,9 +309,23 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   }
   const RowShape<PER> rs(V1);
   float cur[PER], nxt[PER];
-  if (T > 0) seg::load_row<Ld, PER>(cur, base, rs);
+  // row summary of this slot's row: normaliser and four words of listed tokens
+  float lse_cur = 0.f, lse_nxt = 0.f;
+  uint32_t lw_cur[kList / 2], lw_nxt[kList / 2];
+  auto load_summary = [&](int32_t t, float& l, uint32_t* lw) {
+    const int64_t o = o0 + (int64_t)t * ostride;
+    l = out_step[o];
+    lw[0] = (uint32_t)out_tok[o];
+    lw[1] = (uint32_t)out_parent[o];
+    lw[2] = (uint32_t)out_state[o];
+    lw[3] = __float_as_uint(out_cum[o]);
+  };
+  if (T > 0) {
+    seg::load_row<Ld, PER>(cur, base, rs);
+    load_summary(0, lse_cur, lw_cur);
+  }
 
-  // tables: root row, class map and members; hot records; marks
+  // tables: root row, class map and members; packed state records; marks
   {
     const int32_t mm = (mode == 1) ? m : 0;
     const float* gpsi = A.root_psi + (int64_t)mm * V1;
@@ -150,15 +339,18 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       S.tab.cls_tok[i] = (i < V) ? (uint16_t)A.cls_tok[i] : (uint16_t)0;
     }
     const int32_t nhot0 = (mode == 1) ? (n < HOT ? n : HOT) : 0;
+    const uint32_t* src = A.state_rec + 3 * (int64_t)off;
     for (int32_t i = threadIdx.x; i < nhot0; i += nt) {
-      int4 r;
-      r.x = A.first_child[off + i];
-      r.y = (int32_t)((uint32_t)A.link[off + i] | ((uint32_t)A.n_child[off + i] << 16));
-      r.z = __float_as_int(A.phi[off + i]);
-      r.w = __float_as_int(A.psi[off + i]);
-      S.hot.rec[i] = r;
-      const int64_t q = 2 * ((int64_t)off + i);
-      S.hot.mem[i] = make_uint2(A.arc_mem[q], A.arc_mem[q + 1]);
+      S.hot.w0[i] = src[3 * i];
+      S.hot.w1[i] = src[3 * i + 1];
+      S.hot.w2[i] = src[3 * i + 2];
+    }
+    if (nhot0 > 0) {
+      const float* vt = A.value_tab + 512 * (int64_t)m;
+      for (int32_t i = threadIdx.x; i < 512; i += nt) {
+        if (i < 256) S.hot.vpsi[i] = vt[i];
+        else S.hot.vphi[i - 256] = vt[i];
+      }
     }
     for (int32_t i = threadIdx.x; i < MAXK * 16 * PER; i += nt)
       reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
@@ -166,7 +358,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   __syncthreads();
   if (mode == 1 && S.bad) mode = -1;  // uniform: every thread read the same flag
   const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
-  const seg::Graph G(A, off, nhot, S.hot);
+  const seg::SGraph G(A, off, nhot, S.hot, S.tab);
   float* zrow = S.zbuf[w];
   uint8_t* stamps = S.stamps[w];
   uint32_t tag = 0;
@@ -182,35 +374,25 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
 
   for (int32_t t = 0; t < T; ++t) {
     const int par = t & 1;
-    {  // prefetch this slot's next row (the last row is read again at the end)
+    {  // prefetch this slot's next row and its summary (the last ones are read again)
       const int32_t tn = (t + 1 < T) ? t + 1 : t;
       seg::load_row<Ld, PER>(nxt, base + (int64_t)tn * tstride, rs);
+      load_summary(tn, lse_nxt, lw_nxt);
     }
     const int32_t s_k = __builtin_amdgcn_readfirstlane(S.hyp_s[par][w]);
     const float S_k = S.hyp_S[par][w];
 
-    // ---- row: copy to LDS, normaliser in float64
+    // ---- row to LDS; the normaliser comes from the row summary
 #pragma unroll
     for (int j = 0; j < PER - 1; ++j) zrow[64 * j + lane] = cur[j];
     zrow[rs.last_idx] = cur[PER - 1];
     const float zb = seg::rlf(cur[PER - 1], PER > 1 ? 63 : V);
-    float zmax = kNegInf;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const float zj = (j < PER - 1 || rs.last_ok) ? cur[j] : kNegInf;
-      zmax = __builtin_fmaxf(zmax, zj);
+    const float lse = lse_cur;  // every lane loaded the same entry
+    float phi_s = 0.f;
+    if (mode == 1) {
+      int32_t fc_u, nc_u, lk_u;
+      G.rec(s_k, fc_u, nc_u, lk_u, phi_s);
     }
-    zmax = wave_max_dpp(zmax);
-    double se = 0.0;
-    const double zmd = (double)zmax;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const bool ok = (j < PER - 1) || rs.last_ok;
-      se += ok ? exp_nonpos((double)cur[j] - zmd) : 0.0;
-    }
-    se = wave_sum_d(se);
-    const float lse = (float)(zmd + log(se));
-    const float phi_s = (mode == 1) ? G.phi_of(s_k) : 0.f;
     const float c = (S_k - lse) - phi_s;
     if (lane == 0) {
       S.hyp_lse[w] = lse;
@@ -279,6 +461,21 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
         xm |= (clsr[j] != 0xffffu && stamps[clsr[j]] == tg) ? (1u << j) : 0u;
     }
 
+    // ---- the listed root moves of this row that are not overridden: real
+    // candidates, hence lower bounds of the K-th best
+    {
+      float lv = kNegInf;
+      if (lane < kList) {
+        const uint32_t tok = (lw_cur[lane >> 1] >> (16 * (lane & 1))) & 0xffffu;
+        if (tok != kNoTok && (int32_t)tok < V) {
+          const uint32_t cl = S.tab.cls[tok];
+          const bool over = n_ov > 0 && cl != 0xffffu && stamps[cl] == tg;
+          if (!over) lv = c + (zrow[tok] + S.tab.rpsi[tok]);
+        }
+        S.listed[w * kList + lane] = lv;
+      }
+    }
+
     // ---- candidates of this lane: dense root moves (unless overridden), the
     // lane's override entries and (lane 0) the blank
     const float cb = c + (zb + phi_s);
@@ -291,45 +488,10 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     auto dense_f = [&](int j) -> int32_t {
       return fbase + ((j < PER - 1) ? 64 * j + lane : rs.last_idx);
     };
-    float head = (lane == 0) ? cb : kNegInf;
-#pragma unroll
-    for (int j = 0; j < PER; ++j) head = __builtin_fmaxf(head, dense_val(j));
-    for (int32_t i = lane; i < n_ov; i += 64) head = __builtin_fmaxf(head, S.ov_val[w][i]);
-
-    // theta = the K-th largest of all lane maxima (a lower bound of the K-th
-    // best candidate): every wave lists its K largest lane maxima (values,
-    // with multiplicity), and the K-th largest of those lists is taken
-    {
-      float h = head;
-      int32_t got = 0;
-      for (int r = 0; r < MAXK && got < K; ++r) {
-        const float mx = wave_max_dpp(h);
-        const int32_t cnt = __builtin_popcountll(__ballot(h == mx));
-        // record min(cnt, K - got) copies of mx (-inf fills a short list)
-        if (lane >= got && lane < got + cnt && lane < K) S.theta_w[w * MAXK + lane] = mx;
-        got += cnt;
-        h = (h == mx) ? kNegInf : h;
-        if (!(mx > kNegInf)) {
-          if (lane >= got && lane < K) S.theta_w[w * MAXK + lane] = kNegInf;
-          got = K;
-        }
-      }
-    }
     __syncthreads();
-    float theta;
-    {
-      float h = (lane < K * K) ? S.theta_w[(lane / K) * MAXK + (lane % K)] : kNegInf;
-      theta = kNegInf;
-      int32_t rem = K;
-      for (int r = 0; r < MAXK; ++r) {
-        const float mx = wave_max_dpp(h);
-        if (!(mx > kNegInf)) break;
-        const int32_t cnt = __builtin_popcountll(__ballot(h == mx));
-        if (cnt >= rem) { theta = mx; break; }
-        rem -= cnt;
-        h = (h == mx) ? kNegInf : h;
-      }
-    }
+    // theta: the K-th largest listed candidate over all slots
+    const float theta =
+        wave_nth_largest((lane < K * kList) ? S.listed[lane] : kNegInf, K);
 
     // count and compact every candidate >= theta
     int32_t mine = 0;
@@ -468,7 +630,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       const float z = S.zbuf[k][v];
       const float val = S.sel_val[w];
       if (lane == 0) {
-        const int64_t o = ((int64_t)t * B + b) * K + w;
+        const int64_t o = o0 + (int64_t)t * ostride;
         out_tok[o] = v;
         out_parent[o] = k;
         out_state[o] = ns;
@@ -481,6 +643,9 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < PER; ++j) cur[j] = nxt[j];
+    lse_cur = lse_nxt;
+#pragma unroll
+    for (int i = 0; i < kList / 2; ++i) lw_cur[i] = lw_nxt[i];
   }
   if (lane == 0 && T > 0) {
     states[(int64_t)b * K + w] = S.hyp_s[T & 1][w];
@@ -495,9 +660,17 @@ hipError_t launch_beam_fast_t(const ArenaView& A, const void* logits, int32_t T,
                               int32_t* out_parent, int32_t* out_state, float* out_step,
                               float* out_cum, hipStream_t st) {
   static_assert(sizeof(BeamLds<PER, MAXK>) <= 160 * 1024, "LDS budget");
+  typedef typename Ld::T TT;
+  const int64_t n_rows = (int64_t)T * B * K;
+  const int64_t blocks = (n_rows + kPrepThreads / 64 - 1) / (kPrepThreads / 64);
+  hipLaunchKernelGGL((beam_prep_kernel<Ld, PER>), dim3((uint32_t)blocks), dim3(kPrepThreads), 0,
+                     st, A, static_cast<const TT*>(logits), n_rows, B, K, stride, model_ids,
+                     states, out_tok, out_parent, out_state, out_step, out_cum);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((beam_fast_kernel<Ld, PER, MAXK>), dim3(B), dim3(64 * K), 0, st, A,
-                     static_cast<const typename Ld::T*>(logits), T, B, K, stride, model_ids,
-                     states, scores, out_tok, out_parent, out_state, out_step, out_cum);
+                     static_cast<const TT*>(logits), T, B, K, stride, model_ids, states, scores,
+                     out_tok, out_parent, out_state, out_step, out_cum);
   return hipGetLastError();
 }
 

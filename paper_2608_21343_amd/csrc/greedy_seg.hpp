@@ -263,6 +263,15 @@ struct SGraph {
     phi = vphi[(c >> 8) & 0xffu];
     return true;
   }
+  // psi of state x (uniform): from its LDS record when usable, else the arena
+  __device__ __forceinline__ float psi_of(int32_t x) const {
+    uint32_t a = 0u, c = 0x80000000u;
+    if (x < nhot) {
+      a = w0[x];
+      c = w2[x];
+    }
+    return (c >> 31) ? A->psi[off + x] : vpsi[a >> 24];
+  }
   // the same, from the arena when x has no usable LDS record
   __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
                                       float& phi) const {
