@@ -20,7 +20,12 @@ decoded by one call over all 1024 steps (the segmented kernel plus its
 boundary fix-up), for context. ``read_probe`` times a plain read of the same
 logit bytes, for context. Workloads whose logits are smaller than 512 MiB get
 replicated buffers, one per bench step in turn, so that the last-level cache
-does not hold a step's input. ``cpu_baseline`` times the CPU oracle over a
+does not hold a step's input. ``launch_floor_us`` is the mean time of an
+empty kernel of the short-call kernel's shape launched the same number of
+times through the same path: the part of a launch that is not the kernel's
+work. For streaming, ``per_stream_vs_global`` times the same calls with every
+stream on one model id (a single global tree) beside the per-stream lists.
+``cpu_baseline`` times the CPU oracle over a
 process pool on a bounded sample of the same workload (decode only), with a
 single-process figure beside it.
 
@@ -46,6 +51,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+LAUNCH_FLOOR_LDS = 160 * 1024 - 1024
 ROTATE_BYTES = 512 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_chunk_streaming_traffic.json")
 
@@ -56,6 +62,7 @@ KERNELS = {
     "stress_greedy": "wide-row greedy kernel, one workgroup per time segment, + boundary fix-up "
                      "(one call of 256 steps)",
     "stress_beam": "wide-row beam kernel, one workgroup per stream (one call of 256 steps)",
+    "lifecycle": "greedy short-call kernel on a registry arena (one launch per 16-step chunk)",
 }
 
 # CPU oracle sample per workload: (streams, steps); None = all
@@ -123,6 +130,117 @@ def cpu_baseline(cfg):
     }
 
 
+def lifecycle(args) -> int:
+    """Model lifecycle next to the streaming step: the 128 streaming models in
+    a registry arena (room for 8 more), then the cost of adding one compiled
+    model (its records copied in, ids and offsets recorded) and of removing one
+    from the middle (the later half of the arena moved left by the compaction
+    kernel, the model table rebased), each as the mean of several, beside the
+    streaming workload decoded through the registry arena."""
+    import torch
+    import workloads as W
+    from paper_2608_21343_amd import capi
+    from paper_2608_21343_amd.decoder import BoostDecoder
+
+    cfg = W.config_by_name("streaming")
+    T, B, V1, chunk = cfg.T, cfg.B, cfg.Vp1, cfg.chunk
+    cm = W.class_map(cfg)
+    lists = W.phrases(cfg)
+    spare = W.phrases(W.config_by_name("streaming", B=B + 8), range(B, B + 8))
+    t0 = time.perf_counter()
+    g_all = capi.tb_compile_graphs(*W.phrase_csr(lists), cfg.token_w, cfg.end_bonus, cm)
+    compile_s = time.perf_counter() - t0
+    spare_g = [capi.tb_compile_graphs(*W.phrase_csr([l]), cfg.token_w, cfg.end_bonus, cm)
+               for l in spare]
+    cap = g_all.layout.n_states + sum(g.layout.n_states for g in spare_g)
+    reg = capi.Registry(B + 8, cap, cm)
+    ids = reg.register(g_all)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        a.record(stream)
+        fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b), (time.perf_counter() - t) * 1e3
+
+    add_ms, add_wall, rm_ms, rm_wall, moved = [], [], [], [], []
+    ws = torch.empty(max(reg.workspace_bytes(i) for i in ids), dtype=torch.uint8, device="cuda")
+    for g in spare_g:
+        new = []
+        d, w = timed(lambda: new.extend(reg.register(g)))
+        add_ms.append(d)
+        add_wall.append(w)
+        victim = ids[len(ids) // 2]
+        moved.append(reg.workspace_bytes(victim))
+        d, w = timed(lambda: reg.unregister(victim, workspace=ws))
+        rm_ms.append(d)
+        rm_wall.append(w)
+        ids = [i for i in ids if i != victim] + new
+    # the streaming workload through the registry arena (every stream on a live model)
+    dec = BoostDecoder.for_arena(reg.arena)
+    dt = torch.float32
+    logits = torch.empty((T, B, V1), dtype=dt, device="cuda")
+    for ta, tb, rows in W.logit_chunks(cfg, 16):
+        logits[ta:tb].copy_(torch.from_numpy(rows[:, :, 0, :]).cuda())
+    mids_np = np.asarray(sorted(ids)[:B], np.int32)
+    mids, states, _ = dec.start(mids_np)
+    outs = (torch.empty((T, B), dtype=torch.int32, device="cuda"),
+            torch.empty((T, B), dtype=torch.int32, device="cuda"),
+            torch.empty((T, B), dtype=torch.float32, device="cuda"))
+    n_launch = T // chunk
+
+    def run():
+        capi.tb_init_states(dec.arena, B, 1, mids, states)
+        for i in range(n_launch):
+            ta, tb = i * chunk, (i + 1) * chunk
+            capi.tb_boost_step_greedy(dec.arena, logits[ta:tb], mids, states,
+                                      *(o[ta:tb] for o in outs))
+
+    for _ in range(args.warmup):
+        run()
+    step_ms = [timed(run)[0] for _ in range(args.steps)]
+    step_s = float(np.mean(step_ms)) / 1e3
+    alg_bytes = chunk * B * (V1 * 4 + 12) + B * 12
+    result = {
+        "metric": "boosted decode token-scores/s (B x K x (V+1) per step) with achieved HBM GB/s",
+        "value": T * B * V1 / step_s,
+        "unit": "token-scores/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": step_s * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "lifecycle: streaming greedy decode (64 calls of 16 steps) on a "
+                               "registry arena after 8 model additions and removals",
+                   "B": B, "K": 1, "V": cfg.V, "T": T, "chunk": chunk,
+                   "models": B, "spare_ids": 8, "arena_bytes": reg.arena.layout.total_bytes},
+        "roofline": {"bound": "hbm", "achieved": alg_bytes / (step_s / n_launch) / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": alg_bytes / (step_s / n_launch) / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": KERNELS["lifecycle"], "alg_bytes_per_launch": alg_bytes,
+                     "avg_launch_us": step_s / n_launch * 1e6},
+        "lifecycle": {
+            "register_one_model_ms": float(np.mean(add_ms)),
+            "register_one_model_wall_ms": float(np.mean(add_wall)),
+            "unregister_one_model_ms": float(np.mean(rm_ms)),
+            "unregister_one_model_wall_ms": float(np.mean(rm_wall)),
+            "compaction_bytes_moved": int(np.mean(moved)),
+            # the records are read and written twice (out to the workspace and back)
+            "compaction_traffic_GBps": float(np.mean(moved)) * 4 / (float(np.mean(rm_ms)) / 1e3) / 1e9,
+            "compile_128_models_s": compile_s,
+            "step_ms": step_s * 1e3,
+            "what": "one compiled model added (host records copied in, table updated, "
+                    "synchronised) and one model removed from the middle of 128 (the later "
+                    "records moved left through a workspace, table rebased on the device), "
+                    "device time between events and host wall time, mean of 8 each",
+        },
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -156,6 +274,8 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
+    if args.workload == "lifecycle":
+        return lifecycle(args)
     cfg = W.config_by_name(args.workload)
     T, B, K, V1, chunk = cfg.T, cfg.B, cfg.K, cfg.Vp1, cfg.chunk
     item = 4 if cfg.dtype == "f32" else 2
@@ -287,6 +407,54 @@ def main() -> int:
     result["read_probe"] = {"GBps": logits.numel() * item / probe_s / 1e9,
                             "bytes": logits.numel() * item,
                             "what": "torch.amax over the workload's logits, median of 3"}
+
+    # the launch floor: an empty kernel of the short-call kernel's shape (one
+    # workgroup of 16 waves per stream, its LDS), launched as often as the
+    # step's calls through the same path, one event pair around them
+    floor_ms = []
+    for rep in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(n_launch):
+            capi.tb_debug_launch_empty(B, 1024, LAUNCH_FLOOR_LDS)
+        b.record(stream)
+        torch.cuda.synchronize()
+        if rep > 0:
+            floor_ms.append(a.elapsed_time(b) / n_launch)
+    result["launch_floor_us"] = float(np.median(floor_ms)) * 1e3
+    result["launch_floor_shape"] = f"{B} workgroups x 1024 threads, {LAUNCH_FLOOR_LDS} B LDS"
+
+    if cfg.name == "streaming":
+        # every stream on one model id (a single global tree) against the
+        # per-stream lists above: the same calls, states carried, timed the
+        # same way (the paper reports no observable speed difference)
+        gdec = BoostDecoder([lists[0]], W.class_map(cfg), token_w=cfg.token_w,
+                            end_bonus=cfg.end_bonus)
+        gm, gst, gsc = gdec.start(np.zeros(B, np.int32), K)
+        g_ms = []
+        for rep in range(args.steps + 1):
+            rows_dev = rows_bufs[rep % n_buf]
+            capi.tb_init_states(gdec.arena, B, K, gm, gst, gsc)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(n_launch):
+                ta, tb = i * chunk, min(T, (i + 1) * chunk)
+                capi.tb_boost_step_greedy(gdec.arena, rows_dev[ta:tb], gm, gst,
+                                          *(o[ta:tb] for o in outs))
+            b.record(stream)
+            torch.cuda.synchronize()
+            if rep > 0:
+                g_ms.append(a.elapsed_time(b))
+        per_ms = float(np.mean([a.elapsed_time(b) for (a, b) in ev]))
+        glob_ms = float(np.mean(g_ms))
+        result["per_stream_vs_global"] = {
+            "per_stream_ms": per_ms, "global_ms": glob_ms,
+            "per_stream_token_scores_per_s": token_scores / (per_ms / 1e3),
+            "global_token_scores_per_s": token_scores / (glob_ms / 1e3),
+            "ratio": per_ms / glob_ms,
+            "what": f"the step's {n_launch} calls: {B} streams with their own lists (model b) "
+                    f"against all {B} streams on one model id (stream 0's list)"}
+        del gdec
 
     if cfg.name == "streaming":
         # context: the same workload as one call over all T steps

@@ -263,6 +263,62 @@ int tb_boost_step_beam(const tb_arena* a, const void* logits, int32_t dtype, int
 int tb_reset_stream(const tb_arena* a, int32_t B, int32_t b, int32_t new_model_id, int32_t K,
                     int32_t* model_ids, int32_t* states, float* scores, void* hip_stream);
 
+/*
+ * Model lifecycle (Sec. II-B: per-stream lists are added and removed as
+ * streams start and finish; adding appends a model's tensors and records its
+ * offsets, removing marks its id inactive and shifts the later ranges left;
+ * stream-facing model ids are kept apart from the physical offsets).
+ *
+ * A registry is an arena with free capacity: tb_compile_graphs' image layout
+ * sized for max_models model slots (the stable ids 0..max_models-1) and
+ * max_states states, in caller-owned device memory. tb_registry_arena gives
+ * the tb_arena that step calls take; a free or removed id decodes like an
+ * out-of-range one (no biasing, states TB_STATE_INVALID), so streams on a
+ * removed model should be reset. Lifecycle calls and step calls on one
+ * registry must be ordered on one stream (the step calls read the model
+ * table and the moved ranges). The registry handle is host memory owned by
+ * the library (tb_registry_free).
+ *
+ * tb_registry_layout — layout (and total_bytes) of a registry's device
+ *   arena; max_models >= 1, max_states in [max_models, 2^31), v_plus_blank
+ *   in [2, 32768]. TB_EINVAL otherwise.
+ * tb_registry_create — start an empty registry (every id free) in dev_base
+ *   (device, 256-byte aligned, >= total_bytes, else TB_EINVAL / TB_ENOMEM)
+ *   with the class map of every model it will hold (host int32[v_plus_blank],
+ *   as tb_compile_graphs; TB_ERANGE when invalid). Returns once the tables
+ *   are on the device.
+ * tb_registry_model — device range of id: first state and state count (0:
+ *   free). TB_ERANGE for an id outside [0, max_models).
+ * tb_register_models — add every model of g (compiled by tb_compile_graphs
+ *   with the same class map and v_plus_blank, else TB_EINVAL) at the end of
+ *   the used states, under the lowest free ids, written to ids (host
+ *   int32[number of models of g]). TB_ENOMEM when ids or states run out
+ *   (nothing is changed then). Returns once the copies are done (g may be
+ *   freed afterwards).
+ * tb_unregister_workspace_bytes — device scratch tb_unregister_model needs
+ *   for id (44 bytes per state after the model); -1 for a free id.
+ * tb_unregister_model — remove id: its states are filled by the later ones,
+ *   moved left by a compaction kernel through workspace (device, 4-byte
+ *   aligned, >= tb_unregister_workspace_bytes, else TB_ENOMEM before any
+ *   launch), and the model table is rebased on the device. Asynchronous on
+ *   hip_stream; the workspace is free again once the stream has passed the
+ *   call. TB_EINVAL for a free id.
+ */
+typedef struct tb_registry tb_registry;
+int tb_registry_layout(int32_t max_models, int64_t max_states, int32_t v_plus_blank,
+                       tb_arena_layout* out);
+int tb_registry_create(int32_t max_models, int64_t max_states, const int32_t* class_map,
+                       int32_t v_plus_blank, void* dev_base, int64_t bytes, void* hip_stream,
+                       tb_registry** out);
+int tb_registry_arena(const tb_registry* r, tb_arena* out);
+int tb_registry_model(const tb_registry* r, int32_t id, int64_t* first_state, int32_t* n_states);
+int64_t tb_registry_used_states(const tb_registry* r); /* states in use; -1 for NULL */
+int tb_register_models(tb_registry* r, const tb_graphs* g, int32_t* ids, void* hip_stream);
+int64_t tb_unregister_workspace_bytes(const tb_registry* r, int32_t id);
+int tb_unregister_model(tb_registry* r, int32_t id, void* workspace, int64_t workspace_bytes,
+                        void* hip_stream);
+void tb_registry_free(tb_registry* r);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* tb_last_error(void);
 
@@ -283,6 +339,14 @@ const char* tb_last_error(void);
  */
 int tb_debug_select_kernels(int32_t greedy, int32_t beam);
 int tb_debug_set_spin_limit(uint32_t polls);
+
+/*
+ * tb_debug_launch_empty — enqueue a kernel that does nothing, with grid
+ * workgroups of block threads (<= 1024) and lds_bytes of dynamic LDS (<= 160
+ * KiB), on hip_stream: what a step kernel's launch of that shape costs by
+ * itself (the benchmark's launch floor). TB_EINVAL for other shapes.
+ */
+int tb_debug_launch_empty(int32_t grid, int32_t block, int32_t lds_bytes, void* hip_stream);
 
 #ifdef __cplusplus
 }

@@ -79,6 +79,13 @@ def _load() -> C.CDLL:
         "tb_reset_stream": [C.POINTER(tb_arena), I32, I32, I32, I32, P, P, P, P],
         "tb_debug_select_kernels": [I32, I32],
         "tb_debug_set_spin_limit": [C.c_uint32],
+        "tb_debug_launch_empty": [I32, I32, I32, P],
+        "tb_registry_layout": [I32, I64, I32, C.POINTER(tb_arena_layout)],
+        "tb_registry_create": [I32, I64, P, I32, P, I64, P, C.POINTER(C.c_void_p)],
+        "tb_registry_arena": [P, C.POINTER(tb_arena)],
+        "tb_registry_model": [P, I32, C.POINTER(C.c_int64), C.POINTER(C.c_int32)],
+        "tb_register_models": [P, P, P, P],
+        "tb_unregister_model": [P, I32, P, I64, P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -86,6 +93,12 @@ def _load() -> C.CDLL:
         f.restype = C.c_int
     lib.tb_graphs_free.argtypes = [P]
     lib.tb_graphs_free.restype = None
+    lib.tb_registry_free.argtypes = [P]
+    lib.tb_registry_free.restype = None
+    for name in ("tb_registry_used_states", "tb_unregister_workspace_bytes"):
+        getattr(lib, name).restype = C.c_int64
+    lib.tb_registry_used_states.argtypes = [P]
+    lib.tb_unregister_workspace_bytes.argtypes = [P, I32]
     lib.tb_last_error.argtypes = []
     lib.tb_last_error.restype = C.c_char_p
     return lib
@@ -96,7 +109,10 @@ LIB = _load()
 EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb_graphs_upload",
             "tb_graphs_free", "tb_validate_image", "tb_init_states", "tb_boost_step_greedy",
             "tb_boost_step_beam", "tb_reset_stream", "tb_last_error",
-            "tb_debug_select_kernels", "tb_debug_set_spin_limit")
+            "tb_debug_select_kernels", "tb_debug_set_spin_limit", "tb_debug_launch_empty",
+            "tb_registry_layout", "tb_registry_create", "tb_registry_arena", "tb_registry_model",
+            "tb_registry_used_states", "tb_register_models", "tb_unregister_workspace_bytes",
+            "tb_unregister_model", "tb_registry_free")
 
 
 def _check(code: int) -> None:
@@ -331,6 +347,78 @@ def tb_reset_stream(arena: Arena, b: int, new_model_id: int, K: int, model_ids, 
                                _dptr(scores, torch.float32, "scores"), _stream(stream)))
 
 
+class Registry:
+    """Model lifecycle on a device arena with free capacity (tb_registry_*).
+
+    The device buffer is a torch tensor owned by this object. ``arena`` is the
+    current tb_arena for step calls (the same object is updated in place
+    after every lifecycle call, so Arena wrappers built from it stay valid)."""
+
+    def __init__(self, max_models: int, max_states: int, class_map, device="cuda", stream=None):
+        import torch
+        cm = np.ascontiguousarray(class_map, dtype=np.int32)
+        lay = tb_arena_layout()
+        _check(LIB.tb_registry_layout(max_models, max_states, len(cm), C.byref(lay)))
+        self.buf = torch.empty(lay.total_bytes + 256, dtype=torch.uint8, device=device)
+        base = self.buf.data_ptr()
+        self._base = base + (-base) % 256
+        h = C.c_void_p()
+        _check(LIB.tb_registry_create(max_models, max_states, _np_ptr(cm), len(cm),
+                                      C.c_void_p(self._base), lay.total_bytes, _stream(stream),
+                                      C.byref(h)))
+        self._h = h
+        self.max_models = max_models
+        self.device = device
+        self.arena = Arena(self.buf, tb_arena())
+        self._refresh()
+
+    def _refresh(self):
+        _check(LIB.tb_registry_arena(self._h, C.byref(self.arena.arena)))
+
+    def model(self, model_id: int):
+        """(first state, state count) of an id; count 0 for a free id."""
+        f, n = C.c_int64(), C.c_int32()
+        _check(LIB.tb_registry_model(self._h, model_id, C.byref(f), C.byref(n)))
+        return f.value, n.value
+
+    @property
+    def used_states(self) -> int:
+        return int(LIB.tb_registry_used_states(self._h))
+
+    def register(self, graphs: Graphs, stream=None) -> list:
+        ids = np.zeros(graphs.layout.n_models, dtype=np.int32)
+        _check(LIB.tb_register_models(self._h, graphs._h, _np_ptr(ids), _stream(stream)))
+        self._refresh()
+        return [int(i) for i in ids]
+
+    def workspace_bytes(self, model_id: int) -> int:
+        return int(LIB.tb_unregister_workspace_bytes(self._h, model_id))
+
+    def unregister(self, model_id: int, workspace=None, stream=None) -> None:
+        """Remove a model; ``workspace`` is a device tensor of at least
+        workspace_bytes(model_id) bytes (allocated here when None)."""
+        import torch
+        need = self.workspace_bytes(model_id)
+        if workspace is None and need > 0:
+            workspace = torch.empty(need, dtype=torch.uint8, device=self.device)
+        ptr = None if workspace is None else workspace.data_ptr()
+        nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        _check(LIB.tb_unregister_model(self._h, model_id, ptr, nbytes, _stream(stream)))
+        self._refresh()
+        self._last_workspace = workspace  # alive until the stream has used it
+
+    def free(self) -> None:
+        if getattr(self, "_h", None):
+            LIB.tb_registry_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
 def tb_debug_select_kernels(greedy: int = GREEDY_AUTO, beam: int = BEAM_AUTO) -> None:
     """Test hook: force a kernel family (see tbias.h)."""
     _check(LIB.tb_debug_select_kernels(greedy, beam))
@@ -339,6 +427,11 @@ def tb_debug_select_kernels(greedy: int = GREEDY_AUTO, beam: int = BEAM_AUTO) ->
 def tb_debug_set_spin_limit(polls: int = 0) -> None:
     """Test hook: poll limit of the greedy hand-off wait (0 = default)."""
     _check(LIB.tb_debug_set_spin_limit(polls))
+
+
+def tb_debug_launch_empty(grid: int, block: int, lds_bytes: int = 0, stream=None) -> None:
+    """Measurement hook: enqueue a kernel that does nothing (see tbias.h)."""
+    _check(LIB.tb_debug_launch_empty(grid, block, lds_bytes, _stream(stream)))
 
 
 class kernels:

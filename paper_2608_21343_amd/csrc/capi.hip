@@ -70,6 +70,15 @@ extern "C" int tb_debug_set_spin_limit(uint32_t polls) {
   return TB_OK;
 }
 
+extern "C" int tb_debug_launch_empty(int32_t grid, int32_t block, int32_t lds_bytes,
+                                     void* hip_stream) {
+  if (grid < 1 || block < 1 || block > 1024 || lds_bytes < 0 || lds_bytes > 160 * 1024)
+    return fail(TB_EINVAL, "launch shape out of range");
+  hipError_t e = launch_empty(grid, block, lds_bytes, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "empty kernel launch");
+  return TB_OK;
+}
+
 extern "C" int tb_graphs_upload(const tb_graphs* g, void* dev_base, int64_t bytes,
                                 void* hip_stream, tb_arena* out) {
   if (!g || !dev_base || !out) return fail(TB_EINVAL, "NULL argument");

@@ -239,6 +239,45 @@ int compile_model(const int32_t* toks, const int64_t* tok_ptr, int64_t n_phrases
   return TB_OK;
 }
 
+void plan_layout(int32_t n_models, int64_t n_states, int32_t v_plus_blank, tb_arena_layout* L) {
+  const int64_t M = n_models, N = n_states, R = (int64_t)n_models * v_plus_blank;
+  const int32_t V = v_plus_blank - 1;
+  L->n_models = n_models;
+  L->v_plus_blank = v_plus_blank;
+  L->n_states = n_states;
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) { int64_t o = off; off = align256(off + bytes); return o; };
+  L->off_model_off = take(4 * M);
+  L->off_model_n = take(4 * M);
+  L->off_first_child = take(4 * N);
+  L->off_n_child = take(4 * N);
+  L->off_link = take(4 * N);
+  L->off_label = take(4 * N);
+  L->off_phi = take(4 * N);
+  L->off_psi = take(4 * N);
+  L->off_root_psi = take(4 * R);
+  L->off_root_dst = take(4 * R);
+  L->off_class_map = take(4 * (int64_t)v_plus_blank);
+  L->off_cls_ptr = take(4 * (int64_t)v_plus_blank);
+  L->off_cls_tok = take(4 * (int64_t)V);
+  L->off_arc_mem = take(8 * N);
+  L->off_value_tab = take(4 * 512 * M);
+  L->off_state_rec = take(12 * N);
+  L->total_bytes = off;
+}
+
+void class_tables(const int32_t* class_map, int32_t V, int32_t* cp, int32_t* ct) {
+  // members ascending because tokens are scanned in order
+  std::vector<int32_t> cnt(V + 1, 0);
+  for (int32_t v = 0; v < V; ++v)
+    if (class_map[v] >= 0) cnt[class_map[v] + 1]++;
+  cp[0] = 0;
+  for (int32_t c = 0; c < V; ++c) cp[c + 1] = cp[c] + cnt[c + 1];
+  std::vector<int32_t> fillp(cp, cp + V);
+  for (int32_t v = 0; v < V; ++v)
+    if (class_map[v] >= 0) ct[fillp[class_map[v]]++] = v;
+}
+
 }  // namespace tbias
 
 using namespace tbias;
@@ -311,8 +350,6 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   if (!g) return fail(TB_ENOMEM, "host allocation failed");
   tb_arena_layout& L = g->layout;
   std::memset(&L, 0, sizeof(L));
-  L.n_models = n_models;
-  L.v_plus_blank = v_plus_blank;
   int64_t N = 0;
   for (auto& mg : graphs) {
     N += mg.n;
@@ -320,27 +357,8 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
     L.max_depth = std::max(L.max_depth, mg.max_depth);
   }
   if (N > INT32_MAX) { delete g; return fail(TB_ERANGE, "more than 2^31 states in total"); }
-  L.n_states = N;
-  const int64_t M = n_models, R = (int64_t)n_models * v_plus_blank;
-  int64_t off = 0;
-  auto take = [&](int64_t bytes) { int64_t o = off; off = align256(off + bytes); return o; };
-  L.off_model_off = take(4 * M);
-  L.off_model_n = take(4 * M);
-  L.off_first_child = take(4 * N);
-  L.off_n_child = take(4 * N);
-  L.off_link = take(4 * N);
-  L.off_label = take(4 * N);
-  L.off_phi = take(4 * N);
-  L.off_psi = take(4 * N);
-  L.off_root_psi = take(4 * R);
-  L.off_root_dst = take(4 * R);
-  L.off_class_map = take(4 * (int64_t)v_plus_blank);
-  L.off_cls_ptr = take(4 * (int64_t)v_plus_blank);
-  L.off_cls_tok = take(4 * (int64_t)V);
-  L.off_arc_mem = take(8 * N);
-  L.off_value_tab = take(4 * 512 * M);
-  L.off_state_rec = take(12 * N);
-  L.total_bytes = off;
+  plan_layout(n_models, N, v_plus_blank, &L);
+  const int64_t off = L.total_bytes;
   try {
     g->image.assign((size_t)off, 0);
   } catch (const std::bad_alloc&) {
@@ -368,17 +386,10 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
     s0 += mg.n;
   }
   std::memcpy(I32(L.off_class_map), class_map, 4 * (size_t)v_plus_blank);
-  // class members CSR (members ascending because tokens are scanned in order)
+  // class members CSR
   int32_t* cp = I32(L.off_cls_ptr);
   int32_t* ct = I32(L.off_cls_tok);
-  std::vector<int32_t> cnt(V + 1, 0);
-  for (int32_t v = 0; v < V; ++v)
-    if (class_map[v] >= 0) cnt[class_map[v] + 1]++;
-  cp[0] = 0;
-  for (int32_t c = 0; c < V; ++c) cp[c + 1] = cp[c] + cnt[c + 1];
-  std::vector<int32_t> fillp(cp, cp + V);
-  for (int32_t v = 0; v < V; ++v)
-    if (class_map[v] >= 0) ct[fillp[class_map[v]]++] = v;
+  class_tables(class_map, V, cp, ct);
   // largest override set: over all states, the member tokens of the classes
   // of the children along the state's suffix chain (root excluded), each
   // class counted once

@@ -37,4 +37,12 @@ int compile_model(const int32_t* toks, const int64_t* tok_ptr, int64_t n_phrases
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
+// Offsets (256-byte aligned) and total size of an arena image holding
+// n_models model slots and n_states states; the maxima fields are left alone.
+void plan_layout(int32_t n_models, int64_t n_states, int32_t v_plus_blank, tb_arena_layout* L);
+
+// Class member CSR of a class map: members of class c are
+// cls_tok[cls_ptr[c] .. cls_ptr[c+1]-1], ascending (cls_ptr has V+1 entries).
+void class_tables(const int32_t* class_map, int32_t V, int32_t* cls_ptr, int32_t* cls_tok);
+
 }  // namespace tbias

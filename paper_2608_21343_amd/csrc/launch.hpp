@@ -9,6 +9,7 @@ namespace tbias {
 
 hipError_t launch_init_states(const ArenaView& A, int32_t B, int32_t K, const int32_t* model_ids,
                               int32_t* states, float* scores, hipStream_t st);
+hipError_t launch_empty(int32_t grid, int32_t block, int32_t lds_bytes, hipStream_t st);
 hipError_t launch_reset_stream(int32_t b, int32_t m, int32_t K, int32_t* model_ids,
                                int32_t* states, float* scores, hipStream_t st);
 

@@ -24,6 +24,23 @@ __global__ void reset_stream_kernel(int32_t b, int32_t m, int32_t K, int32_t* mo
   if (scores) scores[(int64_t)b * K + k] = (k == 0) ? 0.f : -__builtin_huge_valf();
 }
 
+// A kernel that does nothing, for measuring what a launch of a given shape
+// costs by itself (tb_debug_launch_empty).
+__global__ void empty_kernel(int32_t* sink) {
+  extern __shared__ int32_t pad[];
+  if (sink && threadIdx.x == 0 && blockIdx.x == 0xffffffffu) sink[0] = pad[0];
+}
+
+hipError_t launch_empty(int32_t grid, int32_t block, int32_t lds_bytes, hipStream_t st) {
+  if (lds_bytes > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&empty_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(empty_kernel, dim3(grid), dim3(block), (size_t)lds_bytes, st, nullptr);
+  return hipGetLastError();
+}
+
 hipError_t launch_init_states(const ArenaView& A, int32_t B, int32_t K, const int32_t* model_ids,
                               int32_t* states, float* scores, hipStream_t st) {
   int64_t n = (int64_t)B * K;

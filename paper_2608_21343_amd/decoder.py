@@ -37,6 +37,16 @@ class BoostDecoder:
         self.device = device
         self.V1 = int(len(class_map))
 
+    @classmethod
+    def for_arena(cls, arena, device="cuda") -> "BoostDecoder":
+        """A decoder over an existing device arena (for example a registry's)."""
+        self = cls.__new__(cls)
+        self.graphs = None
+        self.arena = arena
+        self.device = device
+        self.V1 = int(arena.layout.v_plus_blank)
+        return self
+
     def start(self, model_ids: Sequence[int], K: int = 1):
         """Device carry for len(model_ids) streams: (model_ids, states, scores)."""
         B = len(model_ids)

@@ -382,3 +382,41 @@ def test_debug_hooks_validate_their_arguments():
         pass
     assert capi.LIB.tb_debug_select_kernels(0, 0) == capi.TB_OK
     assert capi.LIB.tb_debug_set_spin_limit(0) == capi.TB_OK
+
+
+def test_registry_layout_and_argument_checks():
+    """Registry calls validate before touching the device."""
+    L = capi.LIB
+    lay = capi.tb_arena_layout()
+    assert L.tb_registry_layout(4, 1000, 257, C.byref(lay)) == capi.TB_OK
+    assert lay.n_models == 4 and lay.n_states == 1000 and lay.v_plus_blank == 257
+    offs = sorted(getattr(lay, f) for f, _ in capi.tb_arena_layout._fields_ if f.startswith("off_"))
+    assert all(o % 256 == 0 for o in offs) and offs[-1] < lay.total_bytes
+    # per-state arrays hold the capacity
+    assert lay.off_n_child - lay.off_first_child >= 4 * 1000
+    assert L.tb_registry_layout(0, 1000, 257, C.byref(lay)) == capi.TB_EINVAL
+    assert L.tb_registry_layout(4, 3, 257, C.byref(lay)) == capi.TB_EINVAL
+    assert L.tb_registry_layout(4, 1 << 31, 257, C.byref(lay)) == capi.TB_EINVAL
+    assert L.tb_registry_layout(4, 1000, 1, C.byref(lay)) == capi.TB_EINVAL
+    assert L.tb_registry_layout(4, 1000, 257, None) == capi.TB_EINVAL
+    cm = np.arange(257, dtype=np.int32)
+    cm[256] = -1
+    h = C.c_void_p()
+    ok = L.tb_registry_layout(4, 1000, 257, C.byref(lay))
+    assert ok == capi.TB_OK
+    fake = C.c_void_p(0x100000)   # never dereferenced: every case below fails first
+    assert L.tb_registry_create(4, 1000, None, 257, fake, lay.total_bytes, None,
+                                C.byref(h)) == capi.TB_EINVAL
+    assert L.tb_registry_create(4, 1000, cm.ctypes.data, 257, C.c_void_p(0x100010),
+                                lay.total_bytes, None, C.byref(h)) == capi.TB_EINVAL
+    assert L.tb_registry_create(4, 1000, cm.ctypes.data, 257, fake, lay.total_bytes - 1, None,
+                                C.byref(h)) == capi.TB_ENOMEM
+    bad = cm.copy()
+    bad[256] = 3
+    assert L.tb_registry_create(4, 1000, bad.ctypes.data, 257, fake, lay.total_bytes, None,
+                                C.byref(h)) == capi.TB_ERANGE
+    assert h.value is None
+    assert L.tb_registry_used_states(None) == -1
+    assert L.tb_unregister_workspace_bytes(None, 0) == -1
+    assert L.tb_registry_arena(None, None) == capi.TB_EINVAL
+    assert L.tb_unregister_model(None, 0, None, 0, None) == capi.TB_EINVAL
