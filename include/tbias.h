@@ -319,6 +319,19 @@ int tb_unregister_model(tb_registry* r, int32_t id, void* workspace, int64_t wor
                         void* hip_stream);
 void tb_registry_free(tb_registry* r);
 
+/*
+ * tb_unregister_model_noalloc — tb_unregister_model for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the compaction goes through a scratch
+ * array the library holds in device memory, 32 MiB on every device it runs
+ * on, kept until the process ends. Removing a model whose later states take
+ * more than 32 MiB of records (44 bytes per state) is rejected with TB_ENOMEM
+ * before any launch. Every call on one device shares that device's scratch:
+ * calls that overlap on one device (different streams, or threads) race;
+ * order them. Otherwise as tb_unregister_model (allocates nothing).
+ */
+int tb_unregister_model_noalloc(tb_registry* r, int32_t id, void* hip_stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* tb_last_error(void);
 

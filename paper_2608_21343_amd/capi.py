@@ -86,6 +86,7 @@ def _load() -> C.CDLL:
         "tb_registry_model": [P, I32, C.POINTER(C.c_int64), C.POINTER(C.c_int32)],
         "tb_register_models": [P, P, P, P],
         "tb_unregister_model": [P, I32, P, I64, P],
+        "tb_unregister_model_noalloc": [P, I32, P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -112,7 +113,7 @@ EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb
             "tb_debug_select_kernels", "tb_debug_set_spin_limit", "tb_debug_launch_empty",
             "tb_registry_layout", "tb_registry_create", "tb_registry_arena", "tb_registry_model",
             "tb_registry_used_states", "tb_register_models", "tb_unregister_workspace_bytes",
-            "tb_unregister_model", "tb_registry_free")
+            "tb_unregister_model", "tb_registry_free", "tb_unregister_model_noalloc")
 
 
 def _check(code: int) -> None:
@@ -406,6 +407,11 @@ class Registry:
         _check(LIB.tb_unregister_model(self._h, model_id, ptr, nbytes, _stream(stream)))
         self._refresh()
         self._last_workspace = workspace  # alive until the stream has used it
+
+    def unregister_noalloc(self, model_id: int, stream=None) -> None:
+        """Remove a model through the library's own scratch (no allocation)."""
+        _check(LIB.tb_unregister_model_noalloc(self._h, model_id, _stream(stream)))
+        self._refresh()
 
     def free(self) -> None:
         if getattr(self, "_h", None):

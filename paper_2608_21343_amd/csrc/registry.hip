@@ -10,6 +10,7 @@
 // indexed by the stable id and never move.
 #include <algorithm>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -109,6 +110,16 @@ hipError_t launch_copy(const Segs& S, hipStream_t st) {
 unsigned char* dev_bytes(const tb_registry* r) {
   return static_cast<unsigned char*>(const_cast<void*>(r->arena.base));
 }
+
+// Scratch of tb_unregister_model_noalloc: one copy on every device the
+// library runs on, held until the process ends, shared by every call on that
+// device. Host code never uses the array's name as an address: the device
+// address comes from hipGetSymbolAddress, once per device.
+constexpr int64_t kNoAllocScratchBytes = int64_t(32) << 20;
+static __device__ __align__(256) uint32_t scratch[kNoAllocScratchBytes / 4];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
 
 }  // namespace
 
@@ -326,6 +337,34 @@ extern "C" int tb_unregister_model(tb_registry* r, int32_t id, void* workspace,
   if (workspace && reinterpret_cast<uintptr_t>(workspace) % 4)
     return fail(TB_EINVAL, "workspace not 4-byte aligned");
   return registry_remove(r, id, static_cast<uint32_t*>(workspace), workspace_bytes,
+                         static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int tb_unregister_model_noalloc(tb_registry* r, int32_t id, void* hip_stream) {
+  if (!r) return fail(TB_EINVAL, "registry is NULL");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(TB_EINVAL, "device index beyond the scratch table");
+  void* ptr = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {  // first call on this device (it is current)
+      e = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+      if (e != hipSuccess) {
+        g_scratch_ptr[dev] = nullptr;
+        return hip_fail(e, "hipGetSymbolAddress of the scratch array");
+      }
+    }
+    ptr = g_scratch_ptr[dev];
+  }
+  const int64_t need = tb_unregister_workspace_bytes(r, id);
+  if (need > kNoAllocScratchBytes)
+    return fail(TB_ENOMEM, "removing model " + std::to_string(id) + " moves " +
+                               std::to_string(need) + " bytes of records, beyond the " +
+                               std::to_string(kNoAllocScratchBytes) +
+                               "-byte scratch of tb_unregister_model_noalloc");
+  return registry_remove(r, id, static_cast<uint32_t*>(ptr), kNoAllocScratchBytes,
                          static_cast<hipStream_t>(hip_stream));
 }
 
