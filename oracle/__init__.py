@@ -17,6 +17,9 @@ What it computes (TurboBias 2.0, Sec. II):
 * ``decode.greedy_decode`` / ``decode.beam_decode``: per-stream boosted
   greedy and beam steps over joint-logit rows (Sec. II-B: each stream carries a
   model id, -1 meaning no biasing; Sec. II-C: state carried across chunks).
+* ``decode.beam_decode_stream``: the streaming beam of Sec. II-C with
+  hypothesis recombination (equal label sequences merged by log-add-exp) and a
+  flattened tree of the kept label records.
 
 Floating point: potentials are computed in float64 and rounded once to
 float32. Keys, beam candidates and accumulated beam scores are float32 with a
@@ -35,8 +38,11 @@ chunk invariance).
 from .graph import Graph, build_graph  # noqa: F401
 from .decode import (  # noqa: F401
     beam_decode,
+    beam_decode_stream,
     greedy_decode,
     init_carry,
+    init_stream_carry,
     lse32,
+    tree_sequence,
     widen,
 )
