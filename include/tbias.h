@@ -254,6 +254,68 @@ int tb_boost_step_beam(const tb_arena* a, const void* logits, int32_t dtype, int
                        int32_t* out_state, float* out_step, float* out_cum, void* hip_stream);
 
 /*
+ * Streaming beam search with hypothesis recombination and a flattened
+ * hypothesis tree (Sec. II-C: finalized hypotheses are stored in a flattened
+ * tree with their accumulated scores and carried across chunks, where they are
+ * continued, merged and pruned).
+ *
+ * A hypothesis is its label sequence (the non-blank tokens it emitted). Each
+ * slot carries a tb_hyp: a 64-bit polynomial hash of the sequence (empty: 0;
+ * appending label v: h * TB_HASH_MUL + v + 1, modulo 2^64), the hash without
+ * the last label, the last label and the tree record of that label. The tree
+ * of stream b is tree[(b * tree_cap + r) * 2 + {0, 1}] = (label, parent
+ * record) for r < tree_len[b]; a record that does not fit tree_cap is not
+ * stored and the slot's node is -2. A node is -1 for the empty sequence.
+ */
+#define TB_HASH_MUL 0x9E3779B97F4A7C15ull
+typedef struct {
+  uint64_t hash;        /* hash of the label sequence */
+  uint64_t prefix_hash; /* hash of the sequence without its last label (0 if empty) */
+  int32_t last;         /* last label, -1 if empty */
+  int32_t node;         /* tree record of the last label, -1 if empty, -2 if it did not fit */
+} tb_hyp;
+
+/*
+ * tb_init_beam_stream — tb_init_states for the streaming beam, plus empty
+ * hypotheses: hyps device tb_hyp[B*K] (8-byte aligned) out, tree_len device
+ * int32[B] out (0).
+ */
+int tb_init_beam_stream(const tb_arena* a, int32_t B, int32_t K, const int32_t* model_ids,
+                        int32_t* states, float* scores, tb_hyp* hyps, int32_t* tree_len,
+                        void* hip_stream);
+
+/*
+ * tb_boost_step_beam_stream — tb_boost_step_beam (same arguments and per-step
+ * outputs) with the hypothesis carry and tree. With recombine != 0, two
+ * candidates of a step with equal label sequences (necessarily slot i extended
+ * by the blank and the slot holding i's sequence without its last label,
+ * extended by that label; both live) are merged before the K best are taken:
+ * the better one in (score, flat index) order keeps its position with score
+ * log(exp(a) + exp(b)) (float64, rounded once to float32), the other is
+ * dropped. Every kept non-blank extension appends a record (label, parent
+ * slot's node) to its stream's tree, in slot order.
+ *
+ *   hyps      device tb_hyp[B*K] in/out (8-byte aligned), from tb_init_beam_stream
+ *   tree      device int32[B * tree_cap * 2] in/out; may be NULL when tree_cap is 0
+ *             (no record is stored, nodes are -2)
+ *   tree_len  device int32[B] in/out: records stored per stream (a value
+ *             outside [0, tree_cap] is read as its nearest bound)
+ *   recombine 0: no merging (then the outputs equal tb_boost_step_beam's)
+ *
+ * Label sequences are compared by their hashes (a collision of two different
+ * sequences among one stream's live slots would merge them). Supports
+ * K <= V+1 <= 2048 except V+1 in 1857..1984, K <= 8 and arenas whose largest
+ * override set has at most 256 tokens: TB_EINVAL otherwise. Concurrent calls
+ * on the same carry race.
+ */
+int tb_boost_step_beam_stream(const tb_arena* a, const void* logits, int32_t dtype, int32_t T,
+                              int32_t B, int32_t K, int64_t row_stride, const int32_t* model_ids,
+                              int32_t* states, float* scores, tb_hyp* hyps, int32_t* tree,
+                              int32_t tree_cap, int32_t* tree_len, int32_t recombine,
+                              int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
+                              float* out_step, float* out_cum, void* hip_stream);
+
+/*
  * tb_reset_stream — give stream b (0 <= b < B) a new model id (Sec. II-B:
  * lists are added and removed as streams start and finish) and restart its
  * carry: model id new_model_id in [-1, n_models), states 0 (or -1), scores

@@ -21,7 +21,8 @@ HIP_SOURCES = ["capi.hip", "greedy.hip", "greedy_seg.hip",
                "greedy_seg_1_8.hip", "greedy_seg_9_16.hip", "greedy_seg_17_24.hip",
                "greedy_seg_25_32.hip", "greedy_wide.hip", "beam.hip", "beam_wide_f32.hip", "beam_wide_bf16.hip",
                "beam_pipe_f32.hip", "beam_pipe_bf16.hip", "beam_fast_1_8.hip", "beam_fast_9_16.hip",
-               "beam_fast_17_24.hip", "beam_fast_25_32.hip", "state.hip", "registry.hip"]
+               "beam_fast_17_24.hip", "beam_fast_25_32.hip", "beam_stream_1_8.hip",
+               "beam_stream_9_16.hip", "beam_stream_17_24.hip", "beam_stream_25_32.hip", "state.hip", "registry.hip"]
 CXX_SOURCES = ["compiler.cpp", "errors.cpp"]
 
 HIPCC_FLAGS = [

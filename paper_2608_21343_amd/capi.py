@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import ctypes as C
 from pathlib import Path
-from typing import Optional, Sequence
+from typing import Optional, Sequence, Tuple
 
 import numpy as np
 
@@ -77,6 +77,9 @@ def _load() -> C.CDLL:
         "tb_boost_step_beam": [C.POINTER(tb_arena), P, I32, I32, I32, I32, I64, P, P, P, P, P, P,
                                P, P, P],
         "tb_reset_stream": [C.POINTER(tb_arena), I32, I32, I32, I32, P, P, P, P],
+        "tb_init_beam_stream": [C.POINTER(tb_arena), I32, I32, P, P, P, P, P, P],
+        "tb_boost_step_beam_stream": [C.POINTER(tb_arena), P, I32, I32, I32, I32, I64, P, P, P,
+                                      P, P, I32, P, I32, P, P, P, P, P, P],
         "tb_debug_select_kernels": [I32, I32],
         "tb_debug_set_spin_limit": [C.c_uint32],
         "tb_debug_launch_empty": [I32, I32, I32, P],
@@ -113,7 +116,8 @@ EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb
             "tb_debug_select_kernels", "tb_debug_set_spin_limit", "tb_debug_launch_empty",
             "tb_registry_layout", "tb_registry_create", "tb_registry_arena", "tb_registry_model",
             "tb_registry_used_states", "tb_register_models", "tb_unregister_workspace_bytes",
-            "tb_unregister_model", "tb_registry_free", "tb_unregister_model_noalloc")
+            "tb_unregister_model", "tb_registry_free", "tb_unregister_model_noalloc",
+            "tb_init_beam_stream", "tb_boost_step_beam_stream")
 
 
 def _check(code: int) -> None:
@@ -334,6 +338,87 @@ def tb_boost_step_beam(arena: Arena, logits, model_ids, states, scores, out_tok,
                                   _dptr(out_step, torch.float32, "out_step"),
                                   _dptr(out_cum, torch.float32, "out_cum"),
                                   _stream(stream)))
+
+
+# tb_hyp: 24 bytes, held as three int64 words (hash, prefix hash, last | node << 32)
+HYP_WORDS = 3
+TB_HASH_MUL = 0x9E3779B97F4A7C15
+
+
+def hyp_fields(hyps) -> Tuple[np.ndarray, np.ndarray, np.ndarray, np.ndarray]:
+    """(hash, prefix_hash, last, node) of a host copy of tb_hyp records
+    (an int64 array of shape [..., 3])."""
+    h = np.ascontiguousarray(np.asarray(hyps, dtype=np.int64))
+    words = h.view(np.uint64)
+    ln = h[..., 2:3].copy().view(np.int32)
+    return words[..., 0], words[..., 1], ln[..., 0], ln[..., 1]
+
+
+def sequence_hash(seq) -> int:
+    """The tb_hyp hash of a label sequence (empty: 0; appending v: h*MUL + v + 1 mod 2^64)."""
+    h = 0
+    for v in seq:
+        h = (h * TB_HASH_MUL + int(v) + 1) & 0xFFFFFFFFFFFFFFFF
+    return h
+
+
+def tb_init_beam_stream(arena: Arena, B: int, K: int, model_ids, states, scores, hyps, tree_len,
+                        stream=None) -> None:
+    """hyps: device int64 [B*K, 3] (tb_hyp records); tree_len: device int32 [B]."""
+    import torch
+    _need(model_ids, B, "model_ids")
+    _need(states, B * K, "states")
+    _need(scores, B * K, "scores")
+    _need(hyps, B * K * HYP_WORDS, "hyps")
+    _need(tree_len, B, "tree_len")
+    _check(LIB.tb_init_beam_stream(C.byref(arena.arena), B, K,
+                                   _dptr(model_ids, torch.int32, "model_ids"),
+                                   _dptr(states, torch.int32, "states"),
+                                   _dptr(scores, torch.float32, "scores"),
+                                   _dptr(hyps, torch.int64, "hyps"),
+                                   _dptr(tree_len, torch.int32, "tree_len"), _stream(stream)))
+
+
+def tb_boost_step_beam_stream(arena: Arena, logits, model_ids, states, scores, hyps, tree,
+                              tree_len, out_tok, out_parent, out_state, out_step, out_cum,
+                              recombine: bool = True, stream=None) -> None:
+    """tb_boost_step_beam with the hypothesis carry: hyps device int64 [B*K, 3],
+    tree device int32 [B, tree_cap, 2] (or None with tree_cap 0), tree_len
+    device int32 [B]."""
+    import torch
+    dt, rs = _logits_args(logits)
+    if logits.dim() != 4:
+        raise ValueError("beam logits must be [T, B, K, V+1]")
+    T, B, K, Vp1 = logits.shape
+    if Vp1 != arena.layout.v_plus_blank:
+        raise ValueError(f"logits rows hold {Vp1} values, the arena has "
+                         f"V+1 = {arena.layout.v_plus_blank}")
+    if logits.stride(1) != K * rs or (T > 1 and logits.stride(0) != B * K * rs):
+        raise ValueError("beam logits must be laid out as ((t*B + b)*K + k) * row_stride")
+    _need(model_ids, B, "model_ids")
+    _need(states, B * K, "states")
+    _need(scores, B * K, "scores")
+    _need(hyps, B * K * HYP_WORDS, "hyps")
+    _need(tree_len, B, "tree_len")
+    if tree is None:
+        cap = 0
+    else:
+        if tree.dim() != 3 or tree.shape[0] != B or tree.shape[2] != 2:
+            raise ValueError("tree must be [B, tree_cap, 2]")
+        cap = tree.shape[1]
+    for name, o in (("out_tok", out_tok), ("out_parent", out_parent), ("out_state", out_state),
+                    ("out_step", out_step), ("out_cum", out_cum)):
+        _need(o, T * B * K, name, exact=False)
+    ptr = _logits_ptr(logits)
+    _check(LIB.tb_boost_step_beam_stream(
+        C.byref(arena.arena), C.c_void_p(ptr), dt, T, B, K, rs,
+        _dptr(model_ids, torch.int32, "model_ids"), _dptr(states, torch.int32, "states"),
+        _dptr(scores, torch.float32, "scores"), _dptr(hyps, torch.int64, "hyps"),
+        _dptr(tree, torch.int32, "tree"), cap, _dptr(tree_len, torch.int32, "tree_len"),
+        1 if recombine else 0, _dptr(out_tok, torch.int32, "out_tok"),
+        _dptr(out_parent, torch.int32, "out_parent"), _dptr(out_state, torch.int32, "out_state"),
+        _dptr(out_step, torch.float32, "out_step"), _dptr(out_cum, torch.float32, "out_cum"),
+        _stream(stream)))
 
 
 def tb_reset_stream(arena: Arena, b: int, new_model_id: int, K: int, model_ids, states,

@@ -327,4 +327,37 @@ hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, in
   return hipGetLastError();
 }
 
+// The streaming beam runs the one-wave-per-hypothesis kernel with the
+// recombination and tree stages (K <= 8, V+1 <= 2048 except the chunk counts
+// 30 and 31 that are not instantiated, override sets within its lists).
+bool beam_stream_supported(int32_t v_plus_blank, int32_t max_override, int32_t K) {
+  if (K < 1 || K > 8 || v_plus_blank < 2 || v_plus_blank > 64 * 32 || K > v_plus_blank)
+    return false;
+  const int per = (v_plus_blank + 63) / 64;
+  return per != 30 && per != 31 && max_override <= beamk::kOverCap;
+}
+
+hipError_t launch_beam_stream(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                              int32_t B, int32_t K, int64_t row_stride, const int32_t* model_ids,
+                              int32_t* states, float* scores, tb_hyp* hyps, int32_t* tree,
+                              int32_t tree_cap, int32_t* tree_len, int32_t recombine,
+                              int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
+                              float* out_step, float* out_cum, hipStream_t st) {
+  if (!beam_stream_supported(A.V1, A.max_override, K)) return hipErrorNotSupported;
+  const int per = (A.V1 + 63) / 64;
+  beamk::BeamStreamLaunch f = per <= 8    ? beamk::beam_stream_launcher_1_8(per, dtype)
+                              : per <= 16 ? beamk::beam_stream_launcher_9_16(per, dtype)
+                              : per <= 24 ? beamk::beam_stream_launcher_17_24(per, dtype)
+                                          : beamk::beam_stream_launcher_25_32(per, dtype);
+  if (!f) return hipErrorNotSupported;
+  beamk::StreamArgs sa;
+  sa.hyps = hyps;
+  sa.tree = tree;
+  sa.cap = tree_cap;
+  sa.tree_len = tree_len;
+  sa.recombine = recombine;
+  return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
+           out_state, out_step, out_cum, st, sa);
+}
+
 }  // namespace tbias

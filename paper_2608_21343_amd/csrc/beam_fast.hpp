@@ -62,7 +62,8 @@ constexpr int kList = 8;       // best root moves listed per row by beam_prep_ke
 constexpr int kPrepThreads = 256;
 constexpr uint32_t kNoTok = 0xffffu;
 
-template <int PER, int MAXK>
+// SK: MAXK for the streaming beam, 1 (fields unused) otherwise.
+template <int PER, int MAXK, int SK>
 struct alignas(16) BeamFixed {
   Tables<PER> tab;
   float zbuf[MAXK][64 * PER];  // row of every hypothesis
@@ -87,19 +88,44 @@ struct alignas(16) BeamFixed {
   int32_t red_dst[MAXK];
   int32_t bad;
   int32_t tmo;  // a slot carried TB_STATE_TIMEOUT
+  // streaming beam (tb_boost_step_beam_stream): hypothesis carry, double
+  // buffered; every slot's normaliser for the step ahead; the listed tokens;
+  // the merges a slot applies to its candidates (entry [j][i] from slot i)
+  uint64_t hyp_h[2][SK], hyp_hp[2][SK];
+  int32_t hyp_lv[2][SK], hyp_node[2][SK];
+  float lse_ahead[2][SK];
+  int32_t listed_tok[SK * kList];
+  int32_t mod_tok[SK][SK];
+  float mod_val[SK][SK];
+  int32_t mod_dst[SK][SK];
 };
 
-template <int PER, int MAXK>
+// Carry of the streaming beam (tb_boost_step_beam_stream); unused otherwise.
+struct StreamArgs {
+  tb_hyp* hyps;        // [B*K]
+  int32_t* tree;       // [B*cap*2] (label, parent record)
+  int32_t cap;
+  int32_t* tree_len;   // [B]
+  int32_t recombine;
+};
+
+// log(exp(a) + exp(b)) of two finite float32 values, in float64, rounded once.
+__device__ __forceinline__ float logaddexp32(float a, float b) {
+  const double hi = (double)(a > b ? a : b), lo = (double)(a > b ? b : a);
+  return (float)(hi + log1p(exp(lo - hi)));
+}
+
+template <int PER, int MAXK, int SK>
 constexpr int beam_hot() {
   const int budget = 160 * 1024 - 1024;
-  const int room = (budget - (int)sizeof(BeamFixed<PER, MAXK>) - 2048) / seg::kStateHotBytes;
+  const int room = (budget - (int)sizeof(BeamFixed<PER, MAXK, SK>) - 2048) / seg::kStateHotBytes;
   const int h = (room / 64) * 64;
   return h > 8192 ? 8192 : (h < 0 ? 0 : h);
 }
 
-template <int PER, int MAXK>
-struct alignas(16) BeamLds : BeamFixed<PER, MAXK> {
-  static constexpr int HOT = beam_hot<PER, MAXK>() > 64 ? beam_hot<PER, MAXK>() : 64;
+template <int PER, int MAXK, int SK = 1>
+struct alignas(16) BeamLds : BeamFixed<PER, MAXK, SK> {
+  static constexpr int HOT = beam_hot<PER, MAXK, SK>() > 64 ? beam_hot<PER, MAXK, SK>() : 64;
   StateHot<HOT> hot;
 };
 
@@ -273,14 +299,16 @@ __global__ __launch_bounds__(kPrepThreads) void beam_prep_kernel(
   }
 }
 
-template <class Ld, int PER, int MAXK>
+template <class Ld, int PER, int MAXK, bool STREAM>
 __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int32_t K,
     int64_t stride, const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
     float* __restrict__ scores, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_parent,
-    int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum) {
-  constexpr int HOT = BeamLds<PER, MAXK>::HOT;
-  __shared__ BeamLds<PER, MAXK> S;
+    int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum,
+    StreamArgs sa) {
+  typedef BeamLds<PER, MAXK, STREAM ? MAXK : 1> Lds;
+  constexpr int HOT = Lds::HOT;
+  __shared__ Lds S;
   const int32_t V1 = A.V1, V = V1 - 1;
   const int nt = (int)blockDim.x;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // hypothesis / slot
@@ -306,6 +334,18 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     S.hyp_S[0][threadIdx.x] = scores[(int64_t)b * K + threadIdx.x];
     if (mode == 1 && (s < 0 || s >= n)) S.bad = 1;
     if (s == TB_STATE_TIMEOUT) S.tmo = 1;
+    if constexpr (STREAM) {
+      const tb_hyp hy = sa.hyps[(int64_t)b * K + threadIdx.x];
+      S.hyp_h[0][threadIdx.x] = hy.hash;
+      S.hyp_hp[0][threadIdx.x] = hy.prefix_hash;
+      S.hyp_lv[0][threadIdx.x] = hy.last;
+      S.hyp_node[0][threadIdx.x] = hy.node;
+    }
+  }
+  int32_t tlen = 0;  // tree records of this stream (streaming beam)
+  if constexpr (STREAM) {
+    const int32_t l = sa.tree_len[b];  // clamped: records are only written at [0, cap)
+    tlen = l < 0 ? 0 : (l > sa.cap ? sa.cap : l);
   }
   const RowShape<PER> rs(V1);
   float cur[PER], nxt[PER];
@@ -323,6 +363,9 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   if (T > 0) {
     seg::load_row<Ld, PER>(cur, base, rs);
     load_summary(0, lse_cur, lw_cur);
+    if constexpr (STREAM) {
+      if (lane == 0) S.lse_ahead[0][w] = lse_cur;
+    }
   }
 
   // tables: root row, class map and members; packed state records; marks
@@ -381,6 +424,21 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     }
     const int32_t s_k = __builtin_amdgcn_readfirstlane(S.hyp_s[par][w]);
     const float S_k = S.hyp_S[par][w];
+    // streaming beam: the live slot holding this slot's sequence without its
+    // last label (its extension by that label is this slot's blank
+    // extension); the logit of that label in the partner's row is loaded now
+    int32_t partner = -1, lv_w = -1;
+    float z_partner = 0.f;
+    if constexpr (STREAM) {
+      lv_w = S.hyp_lv[par][w];
+      const uint64_t hp_w = S.hyp_hp[par][w];
+      if (sa.recombine && lv_w >= 0 && lv_w < V && S_k > kNegInf) {
+        for (int32_t j = 0; j < K; ++j)
+          if (j != w && S.hyp_S[par][j] > kNegInf && S.hyp_h[par][j] == hp_w) partner = j;
+      }
+      if (partner >= 0)
+        z_partner = Ld::get(logits + (((int64_t)t * B + b) * K + partner) * stride, lv_w);
+    }
 
     // ---- row to LDS; the normaliser comes from the row summary
 #pragma unroll
@@ -473,12 +531,47 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           if (!over) lv = c + (zrow[tok] + S.tab.rpsi[tok]);
         }
         S.listed[w * kList + lane] = lv;
+        if constexpr (STREAM) S.listed_tok[w * kList + lane] = (int32_t)tok;
       }
     }
 
     // ---- candidates of this lane: dense root moves (unless overridden), the
     // lane's override entries and (lane 0) the blank
-    const float cb = c + (zb + phi_s);
+    float cb = c + (zb + phi_s);
+    if constexpr (STREAM) {
+      // recombination: this slot's blank extension and the partner's
+      // extension by this slot's last label are one hypothesis (state s_k);
+      // the partner's candidate is c_j + (z + psi(s_k)), as the partner
+      // computes it; the better keeps its position with the merged score
+      int32_t mt = -1, md = -1;
+      float mv = kNegInf;
+      if (partner >= 0) {
+        const int32_t sj = __builtin_amdgcn_readfirstlane(S.hyp_s[par][partner]);
+        float phi_j = 0.f, psi_w = 0.f;
+        if (mode == 1) {
+          int32_t fc_u, nc_u, lk_u;
+          G.rec(sj, fc_u, nc_u, lk_u, phi_j);
+          psi_w = G.psi_of(s_k);
+        }
+        const float c_j = (S.hyp_S[par][partner] - S.lse_ahead[par][partner]) - phi_j;
+        const float bj = c_j + (z_partner + psi_w);
+        if (cb > kNegInf && bj > kNegInf) {
+          const float merged = logaddexp32(cb, bj);
+          const int32_t fa = w * V1 + V, fb = partner * V1 + lv_w;
+          const bool keep_a = cb > bj || (cb == bj && fa < fb);
+          mt = lv_w;
+          mv = keep_a ? kNegInf : merged;
+          md = (mode == 1) ? s_k : -1;
+          cb = keep_a ? merged : kNegInf;
+        }
+      }
+      if (lane < K) {
+        const bool mine = lane == partner && mt >= 0;
+        S.mod_tok[lane][w] = mine ? mt : -1;
+        S.mod_val[lane][w] = mv;
+        S.mod_dst[lane][w] = md;
+      }
+    }
     const int32_t fbase = w * V1;
     auto dense_val = [&](int j) -> float {
       const bool okl = (j < PER - 1) || rs.last_ok;
@@ -489,17 +582,57 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       return fbase + ((j < PER - 1) ? 64 * j + lane : rs.last_idx);
     };
     __syncthreads();
-    // theta: the K-th largest listed candidate over all slots
-    const float theta =
-        wave_nth_largest((lane < K * kList) ? S.listed[lane] : kNegInf, K);
+    // the merges into this slot's candidates (lane q: the one from slot q)
+    int32_t my_mt = -1, my_md = -1;
+    float my_mv = kNegInf;
+    bool any_mod = false;
+    int32_t mt_u[STREAM ? MAXK : 1];  // the merged tokens of this slot (uniform, -1: none)
+    if constexpr (STREAM) {
+      if (lane < K) {
+        my_mt = S.mod_tok[w][lane];
+        my_mv = S.mod_val[w][lane];
+        my_md = S.mod_dst[w][lane];
+      }
+      any_mod = __ballot(my_mt >= 0) != 0ull;
+#pragma unroll
+      for (int q = 0; q < MAXK; ++q) mt_u[q] = __builtin_amdgcn_readlane(my_mt, q);
+    }
+    auto modified = [&](int32_t v) -> bool {
+      bool hit = false;
+      if constexpr (STREAM) {
+#pragma unroll
+        for (int q = 0; q < MAXK; ++q) hit = hit || (mt_u[q] == v);
+      }
+      return hit;
+    };
+    // theta: the K-th largest listed candidate over all slots (merged values
+    // where a merge changed a listed move)
+    float lval = (lane < K * kList) ? S.listed[lane] : kNegInf;
+    if constexpr (STREAM) {
+      if (lane < K * kList && lval > kNegInf) {
+        const int32_t lk = lane / kList, ltok = S.listed_tok[lane];
+        for (int32_t q = 0; q < K; ++q)
+          if (S.mod_tok[lk][q] == ltok) lval = S.mod_val[lk][q];
+      }
+    }
+    const float theta = wave_nth_largest(lval, K);
 
     // count and compact every candidate >= theta
     int32_t mine = 0;
     if (theta > kNegInf) {
       mine = (lane == 0 && cb >= theta) ? 1 : 0;
+      if (!any_mod) {
 #pragma unroll
-      for (int j = 0; j < PER; ++j) mine += dense_val(j) >= theta;
-      for (int32_t i = lane; i < n_ov; i += 64) mine += S.ov_val[w][i] >= theta;
+        for (int j = 0; j < PER; ++j) mine += dense_val(j) >= theta;
+        for (int32_t i = lane; i < n_ov; i += 64) mine += S.ov_val[w][i] >= theta;
+      } else {
+#pragma unroll
+        for (int j = 0; j < PER; ++j)
+          mine += (dense_val(j) >= theta && !modified(dense_f(j) - fbase)) ? 1 : 0;
+        for (int32_t i = lane; i < n_ov; i += 64)
+          mine += (S.ov_val[w][i] >= theta && !modified(S.ov_tok[w][i])) ? 1 : 0;
+        mine += (lane < K && my_mt >= 0 && my_mv >= theta) ? 1 : 0;
+      }
     }
     int32_t wtot;
     const int32_t wpre = wave_excl_scan(mine, wtot);
@@ -523,7 +656,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const float v = dense_val(j);
-        if (v >= theta) {
+        if (v >= theta && !(any_mod && modified(dense_f(j) - fbase))) {
           S.cand_val[p] = v;
           S.cand_f[p] = dense_f(j);
           S.cand_dst[p] = -1;
@@ -532,12 +665,18 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       }
       for (int32_t i = lane; i < n_ov; i += 64) {
         const float v = S.ov_val[w][i];
-        if (v >= theta) {
+        if (v >= theta && !(any_mod && modified(S.ov_tok[w][i]))) {
           S.cand_val[p] = v;
           S.cand_f[p] = fbase + S.ov_tok[w][i];
           S.cand_dst[p] = S.ov_dst[w][i];
           ++p;
         }
+      }
+      if (any_mod && lane < K && my_mt >= 0 && my_mv >= theta) {
+        S.cand_val[p] = my_mv;
+        S.cand_f[p] = fbase + my_mt;
+        S.cand_dst[p] = my_md;
+        ++p;
       }
       // pad the list to a multiple of 8 with entries that beat nothing
       const int32_t total8 = (total + 7) & ~7;
@@ -576,9 +715,12 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
         };
         if (lane == 0) offer(cb, fbase + V, -1);
 #pragma unroll
-        for (int jj = 0; jj < PER; ++jj) offer(dense_val(jj), dense_f(jj), -1);
+        for (int jj = 0; jj < PER; ++jj)
+          if (!(any_mod && modified(dense_f(jj) - fbase))) offer(dense_val(jj), dense_f(jj), -1);
         for (int32_t i = lane; i < n_ov; i += 64)
-          offer(S.ov_val[w][i], fbase + S.ov_tok[w][i], S.ov_dst[w][i]);
+          if (!(any_mod && modified(S.ov_tok[w][i])))
+            offer(S.ov_val[w][i], fbase + S.ov_tok[w][i], S.ov_dst[w][i]);
+        if (any_mod && lane < K && my_mt >= 0) offer(my_mv, fbase + my_mt, my_md);
         float wv;
         int32_t wf;
         const int32_t wl = wave_argmax_dpp(bv, bf, wv, wf);
@@ -629,6 +771,40 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       }
       const float z = S.zbuf[k][v];
       const float val = S.sel_val[w];
+      if constexpr (STREAM) {
+        // the slot's hypothesis: the parent's, extended by v unless v is the
+        // blank; kept non-blank extensions get tree records in slot order
+        int32_t before = 0, total = 0;
+        for (int32_t q = 0; q < K; ++q) {
+          int32_t fq = S.sel_f[q];
+          if (fq < 0 || fq >= K * V1) fq = 0;
+          const int32_t nb = (fq % V1 != V) ? 1 : 0;
+          before += (q < w) ? nb : 0;
+          total += nb;
+        }
+        const uint64_t hk = S.hyp_h[par][k];
+        uint64_t nh = hk, nhp = S.hyp_hp[par][k];
+        int32_t nlv = S.hyp_lv[par][k], nnode = S.hyp_node[par][k];
+        if (v != V) {
+          const int32_t r = tlen + before;
+          nhp = hk;
+          nh = hk * (uint64_t)TB_HASH_MUL + (uint64_t)(v + 1);
+          nlv = v;
+          nnode = (r < sa.cap) ? r : -2;
+          if (lane == 0 && r < sa.cap) {
+            sa.tree[((int64_t)b * sa.cap + r) * 2] = v;
+            sa.tree[((int64_t)b * sa.cap + r) * 2 + 1] = S.hyp_node[par][k];
+          }
+        }
+        if (lane == 0) {
+          S.hyp_h[par ^ 1][w] = nh;
+          S.hyp_hp[par ^ 1][w] = nhp;
+          S.hyp_lv[par ^ 1][w] = nlv;
+          S.hyp_node[par ^ 1][w] = nnode;
+          S.lse_ahead[par ^ 1][w] = lse_nxt;
+        }
+        tlen += total;
+      }
       if (lane == 0) {
         const int64_t o = o0 + (int64_t)t * ostride;
         out_tok[o] = v;
@@ -650,16 +826,25 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   if (lane == 0 && T > 0) {
     states[(int64_t)b * K + w] = S.hyp_s[T & 1][w];
     scores[(int64_t)b * K + w] = S.hyp_S[T & 1][w];
+    if constexpr (STREAM) {
+      tb_hyp hy;
+      hy.hash = S.hyp_h[T & 1][w];
+      hy.prefix_hash = S.hyp_hp[T & 1][w];
+      hy.last = S.hyp_lv[T & 1][w];
+      hy.node = S.hyp_node[T & 1][w];
+      sa.hyps[(int64_t)b * K + w] = hy;
+      if (w == 0) sa.tree_len[b] = tlen < sa.cap ? tlen : sa.cap;
+    }
   }
 }
 
-template <class Ld, int PER, int MAXK>
-hipError_t launch_beam_fast_t(const ArenaView& A, const void* logits, int32_t T, int32_t B,
-                              int32_t K, int64_t stride, const int32_t* model_ids,
-                              int32_t* states, float* scores, int32_t* out_tok,
-                              int32_t* out_parent, int32_t* out_state, float* out_step,
-                              float* out_cum, hipStream_t st) {
-  static_assert(sizeof(BeamLds<PER, MAXK>) <= 160 * 1024, "LDS budget");
+template <class Ld, int PER, int MAXK, bool STREAM>
+hipError_t launch_beam_any(const ArenaView& A, const void* logits, int32_t T, int32_t B,
+                           int32_t K, int64_t stride, const int32_t* model_ids, int32_t* states,
+                           float* scores, int32_t* out_tok, int32_t* out_parent,
+                           int32_t* out_state, float* out_step, float* out_cum, hipStream_t st,
+                           StreamArgs sa) {
+  static_assert(sizeof(BeamLds<PER, MAXK, STREAM ? MAXK : 1>) <= 160 * 1024, "LDS budget");
   typedef typename Ld::T TT;
   const int64_t n_rows = (int64_t)T * B * K;
   const int64_t blocks = (n_rows + kPrepThreads / 64 - 1) / (kPrepThreads / 64);
@@ -668,15 +853,45 @@ hipError_t launch_beam_fast_t(const ArenaView& A, const void* logits, int32_t T,
                      states, out_tok, out_parent, out_state, out_step, out_cum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((beam_fast_kernel<Ld, PER, MAXK>), dim3(B), dim3(64 * K), 0, st, A,
+  hipLaunchKernelGGL((beam_fast_kernel<Ld, PER, MAXK, STREAM>), dim3(B), dim3(64 * K), 0, st, A,
                      static_cast<const TT*>(logits), T, B, K, stride, model_ids, states, scores,
-                     out_tok, out_parent, out_state, out_step, out_cum);
+                     out_tok, out_parent, out_state, out_step, out_cum, sa);
   return hipGetLastError();
+}
+
+template <class Ld, int PER, int MAXK>
+hipError_t launch_beam_fast_t(const ArenaView& A, const void* logits, int32_t T, int32_t B,
+                              int32_t K, int64_t stride, const int32_t* model_ids,
+                              int32_t* states, float* scores, int32_t* out_tok,
+                              int32_t* out_parent, int32_t* out_state, float* out_step,
+                              float* out_cum, hipStream_t st) {
+  return launch_beam_any<Ld, PER, MAXK, false>(A, logits, T, B, K, stride, model_ids, states,
+                                               scores, out_tok, out_parent, out_state, out_step,
+                                               out_cum, st, StreamArgs{});
+}
+
+template <class Ld, int PER>
+hipError_t launch_beam_stream_t(const ArenaView& A, const void* logits, int32_t T, int32_t B,
+                                int32_t K, int64_t stride, const int32_t* model_ids,
+                                int32_t* states, float* scores, int32_t* out_tok,
+                                int32_t* out_parent, int32_t* out_state, float* out_step,
+                                float* out_cum, hipStream_t st, StreamArgs sa) {
+  return launch_beam_any<Ld, PER, 8, true>(A, logits, T, B, K, stride, model_ids, states,
+                                           scores, out_tok, out_parent, out_state, out_step,
+                                           out_cum, st, sa);
 }
 
 typedef hipError_t (*BeamLaunch)(const ArenaView&, const void*, int32_t, int32_t, int32_t,
                                  int64_t, const int32_t*, int32_t*, float*, int32_t*, int32_t*,
                                  int32_t*, float*, float*, hipStream_t);
+typedef hipError_t (*BeamStreamLaunch)(const ArenaView&, const void*, int32_t, int32_t, int32_t,
+                                       int64_t, const int32_t*, int32_t*, float*, int32_t*,
+                                       int32_t*, int32_t*, float*, float*, hipStream_t,
+                                       StreamArgs);
+BeamStreamLaunch beam_stream_launcher_1_8(int per, int32_t dtype);
+BeamStreamLaunch beam_stream_launcher_9_16(int per, int32_t dtype);
+BeamStreamLaunch beam_stream_launcher_17_24(int per, int32_t dtype);
+BeamStreamLaunch beam_stream_launcher_25_32(int per, int32_t dtype);
 BeamLaunch beam_launcher_1_8(int per, int maxk, int32_t dtype);
 BeamLaunch beam_launcher_9_16(int per, int maxk, int32_t dtype);
 BeamLaunch beam_launcher_17_24(int per, int maxk, int32_t dtype);

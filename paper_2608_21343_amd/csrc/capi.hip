@@ -110,6 +110,24 @@ extern "C" int tb_init_states(const tb_arena* a, int32_t B, int32_t K, const int
   return TB_OK;
 }
 
+extern "C" int tb_init_beam_stream(const tb_arena* a, int32_t B, int32_t K,
+                                   const int32_t* model_ids, int32_t* states, float* scores,
+                                   tb_hyp* hyps, int32_t* tree_len, void* hip_stream) {
+  int r;
+  if ((r = check_arena(a))) return r;
+  if (B < 1) return fail(TB_EINVAL, "B must be >= 1");
+  if (K < 1 || K > TB_MAX_BEAM) return fail(TB_EINVAL, "K outside [1, TB_MAX_BEAM]");
+  if ((r = check_i32(model_ids, "model_ids"))) return r;
+  if ((r = check_i32(states, "states"))) return r;
+  if ((r = check_i32(scores, "scores"))) return r;
+  if ((r = check_i32(tree_len, "tree_len"))) return r;
+  if (!hyps || !aligned(hyps, 8)) return fail(TB_EINVAL, "hyps NULL or not 8-byte aligned");
+  hipError_t e = launch_init_beam_stream(make_view(*a), B, K, model_ids, states, scores, hyps,
+                                         tree_len, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "init_beam_stream launch");
+  return TB_OK;
+}
+
 extern "C" int tb_reset_stream(const tb_arena* a, int32_t B, int32_t b, int32_t new_model_id,
                                int32_t K, int32_t* model_ids, int32_t* states, float* scores,
                                void* hip_stream) {
@@ -177,5 +195,44 @@ extern "C" int tb_boost_step_beam(const tb_arena* a, const void* logits, int32_t
                              scores, out_tok, out_parent, out_state, out_step, out_cum,
                              static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return hip_fail(e, "beam launch");
+  return TB_OK;
+}
+
+extern "C" int tb_boost_step_beam_stream(const tb_arena* a, const void* logits, int32_t dtype,
+                                         int32_t T, int32_t B, int32_t K, int64_t row_stride,
+                                         const int32_t* model_ids, int32_t* states, float* scores,
+                                         tb_hyp* hyps, int32_t* tree, int32_t tree_cap,
+                                         int32_t* tree_len, int32_t recombine, int32_t* out_tok,
+                                         int32_t* out_parent, int32_t* out_state, float* out_step,
+                                         float* out_cum, void* hip_stream) {
+  int r;
+  if ((r = check_arena(a))) return r;
+  if (T < 0) return fail(TB_EINVAL, "T must be >= 0");
+  if (B < 1) return fail(TB_EINVAL, "B must be >= 1");
+  if (K < 1 || K > 8) return fail(TB_EINVAL, "streaming beam: K outside [1, 8]");
+  if (tree_cap < 0) return fail(TB_EINVAL, "tree_cap must be >= 0");
+  if (!beam_stream_supported(a->layout.v_plus_blank, a->layout.max_override, K))
+    return fail(TB_EINVAL, "streaming beam: V+1 = " + std::to_string(a->layout.v_plus_blank) +
+                               " (needs K <= V+1 <= 2048, not 1857..1984) or an override set of " +
+                               std::to_string(a->layout.max_override) +
+                               " tokens (at most 256) not supported");
+  if (T == 0) return TB_OK;  // no-op: buffers are not touched (and may be NULL)
+  if ((r = check_logits(logits, dtype, row_stride, a->layout.v_plus_blank))) return r;
+  if ((r = check_i32(model_ids, "model_ids"))) return r;
+  if ((r = check_i32(states, "states"))) return r;
+  if ((r = check_i32(scores, "scores"))) return r;
+  if ((r = check_i32(tree_len, "tree_len"))) return r;
+  if (!hyps || !aligned(hyps, 8)) return fail(TB_EINVAL, "hyps NULL or not 8-byte aligned");
+  if (tree_cap > 0 && (r = check_i32(tree, "tree"))) return r;
+  if ((r = check_i32(out_tok, "out_tok"))) return r;
+  if ((r = check_i32(out_parent, "out_parent"))) return r;
+  if ((r = check_i32(out_state, "out_state"))) return r;
+  if ((r = check_i32(out_step, "out_step"))) return r;
+  if ((r = check_i32(out_cum, "out_cum"))) return r;
+  hipError_t e = launch_beam_stream(make_view(*a), logits, dtype, T, B, K, row_stride, model_ids,
+                                    states, scores, hyps, tree, tree_cap, tree_len, recombine,
+                                    out_tok, out_parent, out_state, out_step, out_cum,
+                                    static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return hip_fail(e, "streaming beam launch");
   return TB_OK;
 }

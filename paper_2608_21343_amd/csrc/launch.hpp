@@ -23,6 +23,20 @@ hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, in
                        float* scores, int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
                        float* out_step, float* out_cum, hipStream_t st);
 
+// Streaming beam (recombination and tree): launch_init_beam_stream starts the
+// carry; launch_beam_stream returns hipErrorNotSupported for rows or arenas
+// its kernel does not serve (beam_stream_supported tells in advance).
+hipError_t launch_init_beam_stream(const ArenaView& A, int32_t B, int32_t K,
+                                   const int32_t* model_ids, int32_t* states, float* scores,
+                                   tb_hyp* hyps, int32_t* tree_len, hipStream_t st);
+bool beam_stream_supported(int32_t v_plus_blank, int32_t max_override, int32_t K);
+hipError_t launch_beam_stream(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,
+                              int32_t B, int32_t K, int64_t row_stride, const int32_t* model_ids,
+                              int32_t* states, float* scores, tb_hyp* hyps, int32_t* tree,
+                              int32_t tree_cap, int32_t* tree_len, int32_t recombine,
+                              int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
+                              float* out_step, float* out_cum, hipStream_t st);
+
 // Segmented greedy kernel (plus its boundary fix-up); hipErrorNotSupported
 // when V+1 is too large for it.
 hipError_t launch_greedy_seg(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,

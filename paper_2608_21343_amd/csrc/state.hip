@@ -15,6 +15,25 @@ __global__ void init_states_kernel(ArenaView A, int32_t B, int32_t K, const int3
   if (scores) scores[i] = (k == 0) ? 0.f : -__builtin_huge_valf();
 }
 
+// tb_init_states plus empty hypotheses and trees of the streaming beam.
+__global__ void init_beam_stream_kernel(ArenaView A, int32_t B, int32_t K,
+                                        const int32_t* model_ids, int32_t* states, float* scores,
+                                        tb_hyp* hyps, int32_t* tree_len) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)B * K) return;
+  int32_t b = (int32_t)(i / K), k = (int32_t)(i % K);
+  int32_t m = model_ids[b];
+  states[i] = (m == -1) ? TB_STATE_NONE : ((m < -1 || m >= A.n_models) ? TB_STATE_INVALID : 0);
+  scores[i] = (k == 0) ? 0.f : -__builtin_huge_valf();
+  tb_hyp h;
+  h.hash = 0ull;
+  h.prefix_hash = 0ull;
+  h.last = -1;
+  h.node = -1;
+  hyps[i] = h;
+  if (k == 0) tree_len[b] = 0;
+}
+
 __global__ void reset_stream_kernel(int32_t b, int32_t m, int32_t K, int32_t* model_ids,
                                     int32_t* states, float* scores) {
   int32_t k = threadIdx.x;
@@ -48,6 +67,17 @@ hipError_t launch_init_states(const ArenaView& A, int32_t B, int32_t K, const in
   int blocks = (int)((n + threads - 1) / threads);
   hipLaunchKernelGGL(init_states_kernel, dim3(blocks), dim3(threads), 0, st, A, B, K, model_ids,
                      states, scores);
+  return hipGetLastError();
+}
+
+hipError_t launch_init_beam_stream(const ArenaView& A, int32_t B, int32_t K,
+                                   const int32_t* model_ids, int32_t* states, float* scores,
+                                   tb_hyp* hyps, int32_t* tree_len, hipStream_t st) {
+  int64_t n = (int64_t)B * K;
+  int threads = 256;
+  int blocks = (int)((n + threads - 1) / threads);
+  hipLaunchKernelGGL(init_beam_stream_kernel, dim3(blocks), dim3(threads), 0, st, A, B, K,
+                     model_ids, states, scores, hyps, tree_len);
   return hipGetLastError();
 }
 

@@ -76,6 +76,46 @@ class BoostDecoder:
         capi.tb_boost_step_beam(self.arena, logits, mids, states, scores, *out)
         return out
 
+    def start_beam_stream(self, model_ids: Sequence[int], K: int, tree_cap: int):
+        """Device carry of the streaming beam: a BeamCarry."""
+        B = len(model_ids)
+        dev = self.device
+        c = BeamCarry(
+            mids=torch.tensor(np.asarray(model_ids, np.int32), device=dev),
+            states=torch.empty(B * K, dtype=torch.int32, device=dev),
+            scores=torch.empty(B * K, dtype=torch.float32, device=dev),
+            hyps=torch.empty((B * K, capi.HYP_WORDS), dtype=torch.int64, device=dev),
+            tree=(torch.zeros((B, tree_cap, 2), dtype=torch.int32, device=dev)
+                  if tree_cap > 0 else None),
+            tree_len=torch.empty(B, dtype=torch.int32, device=dev))
+        capi.tb_init_beam_stream(self.arena, B, K, c.mids, c.states, c.scores, c.hyps,
+                                 c.tree_len)
+        return c
+
+    def beam_stream(self, logits: torch.Tensor, carry: "BeamCarry", recombine: bool = True,
+                    out=None):
+        T, B, K = logits.shape[0], logits.shape[1], logits.shape[2]
+        if out is None:
+            i32 = dict(dtype=torch.int32, device=self.device)
+            f32 = dict(dtype=torch.float32, device=self.device)
+            out = (torch.empty((T, B, K), **i32), torch.empty((T, B, K), **i32),
+                   torch.empty((T, B, K), **i32), torch.empty((T, B, K), **f32),
+                   torch.empty((T, B, K), **f32))
+        capi.tb_boost_step_beam_stream(self.arena, logits, carry.mids, carry.states, carry.scores,
+                                       carry.hyps, carry.tree, carry.tree_len, *out,
+                                       recombine=recombine)
+        return out
+
+
+class BeamCarry:
+    """Device state of streaming beams: model ids [B], states and scores
+    [B*K], tb_hyp records [B*K, 3] (int64 words), trees [B, cap, 2], tree
+    lengths [B]."""
+
+    def __init__(self, mids, states, scores, hyps, tree, tree_len):
+        self.mids, self.states, self.scores = mids, states, scores
+        self.hyps, self.tree, self.tree_len = hyps, tree, tree_len
+
 
 def _csr(lists):
     mp = [0]
