@@ -241,6 +241,73 @@ def lifecycle(args) -> int:
     return 0
 
 
+def stream_beam_figures(dec, cfg, rows_dev, mids, stream, reps: int = 4) -> dict:
+    """The beam workload through the streaming beam (recombination and a
+    flattened tree of 4096 records per stream): one call over all steps, and
+    the steps as calls of 16, eager and as one captured HIP graph of the
+    whole chunk loop."""
+    import torch
+    from paper_2608_21343_amd import capi
+    T, B, K = cfg.T, cfg.B, cfg.K
+    chunk = 16
+    i32 = dict(dtype=torch.int32, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+    outs = tuple(torch.empty((T, B, K), **i32) for _ in range(3)) + \
+        tuple(torch.empty((T, B, K), **f32) for _ in range(2))
+    carry = dec.start_beam_stream(mids, K, 4096)
+
+    def restart():
+        capi.tb_init_beam_stream(dec.arena, B, K, carry.mids, carry.states, carry.scores,
+                                 carry.hyps, carry.tree_len)
+
+    def timed(body):
+        ms = []
+        for rep in range(reps + 1):
+            restart()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            body()
+            b.record(stream)
+            torch.cuda.synchronize()
+            if rep > 0:
+                ms.append(a.elapsed_time(b))
+        return float(np.mean(ms))
+
+    one_ms = timed(lambda: dec.beam_stream(rows_dev, carry, out=outs))
+    whole = tuple(o.clone() for o in outs)
+    n = T // chunk
+
+    def chunks():
+        for i in range(n):
+            dec.beam_stream(rows_dev[i * chunk:(i + 1) * chunk], carry,
+                            out=tuple(o[i * chunk:(i + 1) * chunk] for o in outs))
+
+    eager_ms = timed(chunks)
+    same = all(torch.equal(x, y) for x, y in zip(whole, outs))
+    # the chunk loop captured once as a HIP graph (every call on its own
+    # slices of the resident rows) and replayed per step
+    restart()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        chunks()
+    graph_ms = timed(g.replay)
+    same_graph = all(torch.equal(x, y) for x, y in zip(whole, outs))
+    m2, st, sc = dec.start(mids, K)
+
+    def plain():
+        capi.tb_init_states(dec.arena, B, K, m2, st, sc)
+        dec.beam(rows_dev, m2, st, sc, out=outs)
+
+    plain_ms = timed(plain)
+    del g
+    return {"one_call_ms": one_ms, "plain_beam_one_call_ms": plain_ms,
+            "recombination_cost": one_ms / plain_ms,
+            "calls_of_16_eager_ms": eager_ms, "calls_of_16_graph_ms": graph_ms,
+            "chunked_equals_one_call": bool(same), "graph_equals_one_call": bool(same_graph),
+            "tree_cap": 4096}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -476,6 +543,9 @@ def main() -> int:
                                 "frac": whole_bytes / whole_s / 1e9 / HBM_PEAK_GBS,
                                 "kernels": "segmented greedy kernel + boundary fix-up",
                                 "outputs_equal_chunked": bool(same)}
+    if cfg.name == "beam":
+        result["stream_beam"] = stream_beam_figures(dec, cfg, rows_bufs[0], W.model_ids(cfg),
+                                                    stream)
     del logits, bufs, rows_bufs
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg)

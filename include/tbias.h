@@ -304,7 +304,7 @@ int tb_init_beam_stream(const tb_arena* a, int32_t B, int32_t K, const int32_t* 
  *
  * Label sequences are compared by their hashes (a collision of two different
  * sequences among one stream's live slots would merge them). Supports
- * K <= V+1 <= 2048 except V+1 in 1857..1984, K <= 8 and arenas whose largest
+ * K <= V+1 <= 2048, K <= 8 and arenas whose largest
  * override set has at most 256 tokens: TB_EINVAL otherwise. Concurrent calls
  * on the same carry race.
  */

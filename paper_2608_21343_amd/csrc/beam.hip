@@ -328,13 +328,12 @@ hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, in
 }
 
 // The streaming beam runs the one-wave-per-hypothesis kernel with the
-// recombination and tree stages (K <= 8, V+1 <= 2048 except the chunk counts
-// 30 and 31 that are not instantiated, override sets within its lists).
+// recombination and tree stages (K <= 8, V+1 <= 2048, override sets within
+// its lists).
 bool beam_stream_supported(int32_t v_plus_blank, int32_t max_override, int32_t K) {
   if (K < 1 || K > 8 || v_plus_blank < 2 || v_plus_blank > 64 * 32 || K > v_plus_blank)
     return false;
-  const int per = (v_plus_blank + 63) / 64;
-  return per != 30 && per != 31 && max_override <= beamk::kOverCap;
+  return max_override <= beamk::kOverCap;
 }
 
 hipError_t launch_beam_stream(const ArenaView& A, const void* logits, int32_t dtype, int32_t T,

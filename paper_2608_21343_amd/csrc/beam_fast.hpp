@@ -68,9 +68,11 @@ struct alignas(16) BeamFixed {
   Tables<PER> tab;
   float zbuf[MAXK][64 * PER];  // row of every hypothesis
   uint8_t stamps[MAXK][64 * PER];
-  float ov_val[MAXK][kOverCap];  // override candidates of hypothesis k
-  int32_t ov_tok[MAXK][kOverCap];
-  int32_t ov_dst[MAXK][kOverCap];
+  // override candidates of hypothesis k (the streaming beam appends its
+  // merged candidates: up to SK - 1 more)
+  float ov_val[MAXK][kOverCap + SK - 1];
+  int32_t ov_tok[MAXK][kOverCap + SK - 1];
+  int32_t ov_dst[MAXK][kOverCap + SK - 1];
   float cand_val[kCandCap];
   int32_t cand_f[kCandCap];
   int32_t cand_dst[kCandCap];
@@ -89,15 +91,10 @@ struct alignas(16) BeamFixed {
   int32_t bad;
   int32_t tmo;  // a slot carried TB_STATE_TIMEOUT
   // streaming beam (tb_boost_step_beam_stream): hypothesis carry, double
-  // buffered; every slot's normaliser for the step ahead; the listed tokens;
-  // the merges a slot applies to its candidates (entry [j][i] from slot i)
+  // buffered, and the listed tokens
   uint64_t hyp_h[2][SK], hyp_hp[2][SK];
   int32_t hyp_lv[2][SK], hyp_node[2][SK];
-  float lse_ahead[2][SK];
   int32_t listed_tok[SK * kList];
-  int32_t mod_tok[SK][SK];
-  float mod_val[SK][SK];
-  int32_t mod_dst[SK][SK];
 };
 
 // Carry of the streaming beam (tb_boost_step_beam_stream); unused otherwise.
@@ -363,9 +360,6 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   if (T > 0) {
     seg::load_row<Ld, PER>(cur, base, rs);
     load_summary(0, lse_cur, lw_cur);
-    if constexpr (STREAM) {
-      if (lane == 0) S.lse_ahead[0][w] = lse_cur;
-    }
   }
 
   // tables: root row, class map and members; packed state records; marks
@@ -424,20 +418,21 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     }
     const int32_t s_k = __builtin_amdgcn_readfirstlane(S.hyp_s[par][w]);
     const float S_k = S.hyp_S[par][w];
-    // streaming beam: the live slot holding this slot's sequence without its
-    // last label (its extension by that label is this slot's blank
-    // extension); the logit of that label in the partner's row is loaded now
-    int32_t partner = -1, lv_w = -1;
-    float z_partner = 0.f;
+    // streaming beam: bit 8x+y of pairs says that live slot y holds live slot
+    // x's sequence without its last label (lane 8x+y tests it; every wave
+    // forms the same mask); pair_lv on lane 8x is x's last label
+    uint64_t pairs = 0ull;
+    int32_t pair_lv = -1;
     if constexpr (STREAM) {
-      lv_w = S.hyp_lv[par][w];
-      const uint64_t hp_w = S.hyp_hp[par][w];
-      if (sa.recombine && lv_w >= 0 && lv_w < V && S_k > kNegInf) {
-        for (int32_t j = 0; j < K; ++j)
-          if (j != w && S.hyp_S[par][j] > kNegInf && S.hyp_h[par][j] == hp_w) partner = j;
+      static_assert(MAXK <= 8 && kList == 8, "pair mask layout: 8 slots, 8 listed moves");
+      const int32_t x = lane >> 3, y = lane & 7;
+      bool is_pair = false;
+      if (sa.recombine && x < K && y < K) {
+        pair_lv = S.hyp_lv[par][x];
+        is_pair = x != y && pair_lv >= 0 && pair_lv < V && S.hyp_S[par][x] > kNegInf &&
+                  S.hyp_S[par][y] > kNegInf && S.hyp_hp[par][x] == S.hyp_h[par][y];
       }
-      if (partner >= 0)
-        z_partner = Ld::get(logits + (((int64_t)t * B + b) * K + partner) * stride, lv_w);
+      pairs = __ballot(is_pair);
     }
 
     // ---- row to LDS; the normaliser comes from the row summary
@@ -538,40 +533,6 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     // ---- candidates of this lane: dense root moves (unless overridden), the
     // lane's override entries and (lane 0) the blank
     float cb = c + (zb + phi_s);
-    if constexpr (STREAM) {
-      // recombination: this slot's blank extension and the partner's
-      // extension by this slot's last label are one hypothesis (state s_k);
-      // the partner's candidate is c_j + (z + psi(s_k)), as the partner
-      // computes it; the better keeps its position with the merged score
-      int32_t mt = -1, md = -1;
-      float mv = kNegInf;
-      if (partner >= 0) {
-        const int32_t sj = __builtin_amdgcn_readfirstlane(S.hyp_s[par][partner]);
-        float phi_j = 0.f, psi_w = 0.f;
-        if (mode == 1) {
-          int32_t fc_u, nc_u, lk_u;
-          G.rec(sj, fc_u, nc_u, lk_u, phi_j);
-          psi_w = G.psi_of(s_k);
-        }
-        const float c_j = (S.hyp_S[par][partner] - S.lse_ahead[par][partner]) - phi_j;
-        const float bj = c_j + (z_partner + psi_w);
-        if (cb > kNegInf && bj > kNegInf) {
-          const float merged = logaddexp32(cb, bj);
-          const int32_t fa = w * V1 + V, fb = partner * V1 + lv_w;
-          const bool keep_a = cb > bj || (cb == bj && fa < fb);
-          mt = lv_w;
-          mv = keep_a ? kNegInf : merged;
-          md = (mode == 1) ? s_k : -1;
-          cb = keep_a ? merged : kNegInf;
-        }
-      }
-      if (lane < K) {
-        const bool mine = lane == partner && mt >= 0;
-        S.mod_tok[lane][w] = mine ? mt : -1;
-        S.mod_val[lane][w] = mv;
-        S.mod_dst[lane][w] = md;
-      }
-    }
     const int32_t fbase = w * V1;
     auto dense_val = [&](int j) -> float {
       const bool okl = (j < PER - 1) || rs.last_ok;
@@ -582,37 +543,84 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       return fbase + ((j < PER - 1) ? 64 * j + lane : rs.last_idx);
     };
     __syncthreads();
-    // the merges into this slot's candidates (lane q: the one from slot q)
-    int32_t my_mt = -1, my_md = -1;
-    float my_mv = kNegInf;
-    bool any_mod = false;
-    int32_t mt_u[STREAM ? MAXK : 1];  // the merged tokens of this slot (uniform, -1: none)
+    // streaming beam: recombination. Two live slots x and y with
+    // seq(y) = seq(x) without its last label v make one hypothesis of x's
+    // blank extension and y's extension by v (state s_x). Both slots form the
+    // pair from the rows in LDS and decide alike: the better in (value, flat
+    // index) order keeps its place with the merged value, the other becomes
+    // -inf. x updates its blank; y patches its candidate for v (an override
+    // entry, or a new entry that masks the dense root move). A slot pairs
+    // with its lowest-numbered prefix slot only.
     if constexpr (STREAM) {
-      if (lane < K) {
-        my_mt = S.mod_tok[w][lane];
-        my_mv = S.mod_val[w][lane];
-        my_md = S.mod_dst[w][lane];
+      if (pairs != 0ull) {
+        // the class marks of this step exist only when the walk listed
+        // overrides (otherwise tg is stale)
+        const int32_t n_walk = n_ov;
+        struct Merge {
+          float a, bv, merged;
+          bool ok;
+        };
+        auto merge = [&](int32_t x, int32_t y) -> Merge {
+          const int32_t s_x = __builtin_amdgcn_readfirstlane(S.hyp_s[par][x]);
+          const int32_t v = __builtin_amdgcn_readlane(pair_lv, 8 * x);
+          const float phi_x = S.hyp_phi[x], phi_y = S.hyp_phi[y];
+          const float c_x = (S.hyp_S[par][x] - S.hyp_lse[x]) - phi_x;
+          const float c_y = (S.hyp_S[par][y] - S.hyp_lse[y]) - phi_y;
+          const float psi_x = (mode == 1) ? G.psi_of(s_x) : 0.f;
+          Merge r;
+          r.a = c_x + (S.zbuf[x][V] + phi_x);
+          r.bv = c_y + (S.zbuf[y][v] + psi_x);
+          r.ok = r.a > kNegInf && r.bv > kNegInf;
+          r.merged = r.ok ? logaddexp32(r.a, r.bv) : kNegInf;
+          return r;
+        };
+        const uint32_t row_w = (uint32_t)(pairs >> (8 * w)) & 0xffu;
+        if (row_w != 0u) {  // this slot is x; its prefix slot is y
+          const int32_t y = __builtin_ctz(row_w);
+          const Merge r = merge(w, y);
+          if (r.ok) {
+            const int32_t v = __builtin_amdgcn_readlane(pair_lv, 8 * w);
+            const bool keep_a = r.a > r.bv || (r.a == r.bv && w * V1 + V < y * V1 + v);
+            cb = keep_a ? r.merged : kNegInf;
+          }
+        }
+        for (int32_t x = 0; x < K; ++x) {  // this slot is y for every such x
+          const uint32_t row_x = (uint32_t)(pairs >> (8 * x)) & 0xffu;
+          if (row_x == 0u || __builtin_ctz(row_x) != w) continue;
+          const Merge r = merge(x, w);
+          if (!r.ok) continue;
+          const int32_t v = __builtin_amdgcn_readlane(pair_lv, 8 * x);
+          const bool keep_a = r.a > r.bv || (r.a == r.bv && x * V1 + V < w * V1 + v);
+          const float nv = keep_a ? kNegInf : r.merged;
+          const uint32_t cl = S.tab.cls[v];
+          const bool over = n_walk > 0 && cl != 0xffffu && stamps[cl] == tg;
+          if (over) {
+            for (int32_t q = lane; q < n_walk; q += 64)
+              if (S.ov_tok[w][q] == v) S.ov_val[w][q] = nv;
+          } else {
+            if (lane == 0) {
+              S.ov_val[w][n_ov] = nv;
+              S.ov_tok[w][n_ov] = v;
+              S.ov_dst[w][n_ov] = (mode == 1) ? __builtin_amdgcn_readfirstlane(S.hyp_s[par][x]) : -1;
+            }
+            ++n_ov;
+            const bool last = PER > 1 && v >= 64 * (PER - 1);
+            const int32_t ol = last ? v - (V1 - 64) : (v & 63);
+            const int32_t oj = last ? PER - 1 : (v >> 6);
+            if (lane == ol) xm |= 1u << oj;
+          }
+        }
       }
-      any_mod = __ballot(my_mt >= 0) != 0ull;
-#pragma unroll
-      for (int q = 0; q < MAXK; ++q) mt_u[q] = __builtin_amdgcn_readlane(my_mt, q);
     }
-    auto modified = [&](int32_t v) -> bool {
-      bool hit = false;
-      if constexpr (STREAM) {
-#pragma unroll
-        for (int q = 0; q < MAXK; ++q) hit = hit || (mt_u[q] == v);
-      }
-      return hit;
-    };
-    // theta: the K-th largest listed candidate over all slots (merged values
-    // where a merge changed a listed move)
+    // theta: the K-th largest listed candidate over all slots (for the
+    // streaming beam without the listed moves that a merge may change)
     float lval = (lane < K * kList) ? S.listed[lane] : kNegInf;
     if constexpr (STREAM) {
-      if (lane < K * kList && lval > kNegInf) {
+      if (pairs != 0ull && lane < K * kList) {
         const int32_t lk = lane / kList, ltok = S.listed_tok[lane];
-        for (int32_t q = 0; q < K; ++q)
-          if (S.mod_tok[lk][q] == ltok) lval = S.mod_val[lk][q];
+        for (int32_t x = 0; x < K; ++x)
+          if (((pairs >> (8 * x + lk)) & 1ull) && __builtin_amdgcn_readlane(pair_lv, 8 * x) == ltok)
+            lval = kNegInf;
       }
     }
     const float theta = wave_nth_largest(lval, K);
@@ -621,18 +629,9 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     int32_t mine = 0;
     if (theta > kNegInf) {
       mine = (lane == 0 && cb >= theta) ? 1 : 0;
-      if (!any_mod) {
 #pragma unroll
-        for (int j = 0; j < PER; ++j) mine += dense_val(j) >= theta;
-        for (int32_t i = lane; i < n_ov; i += 64) mine += S.ov_val[w][i] >= theta;
-      } else {
-#pragma unroll
-        for (int j = 0; j < PER; ++j)
-          mine += (dense_val(j) >= theta && !modified(dense_f(j) - fbase)) ? 1 : 0;
-        for (int32_t i = lane; i < n_ov; i += 64)
-          mine += (S.ov_val[w][i] >= theta && !modified(S.ov_tok[w][i])) ? 1 : 0;
-        mine += (lane < K && my_mt >= 0 && my_mv >= theta) ? 1 : 0;
-      }
+      for (int j = 0; j < PER; ++j) mine += dense_val(j) >= theta;
+      for (int32_t i = lane; i < n_ov; i += 64) mine += S.ov_val[w][i] >= theta;
     }
     int32_t wtot;
     const int32_t wpre = wave_excl_scan(mine, wtot);
@@ -656,7 +655,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
         const float v = dense_val(j);
-        if (v >= theta && !(any_mod && modified(dense_f(j) - fbase))) {
+        if (v >= theta) {
           S.cand_val[p] = v;
           S.cand_f[p] = dense_f(j);
           S.cand_dst[p] = -1;
@@ -665,18 +664,12 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       }
       for (int32_t i = lane; i < n_ov; i += 64) {
         const float v = S.ov_val[w][i];
-        if (v >= theta && !(any_mod && modified(S.ov_tok[w][i]))) {
+        if (v >= theta) {
           S.cand_val[p] = v;
           S.cand_f[p] = fbase + S.ov_tok[w][i];
           S.cand_dst[p] = S.ov_dst[w][i];
           ++p;
         }
-      }
-      if (any_mod && lane < K && my_mt >= 0 && my_mv >= theta) {
-        S.cand_val[p] = my_mv;
-        S.cand_f[p] = fbase + my_mt;
-        S.cand_dst[p] = my_md;
-        ++p;
       }
       // pad the list to a multiple of 8 with entries that beat nothing
       const int32_t total8 = (total + 7) & ~7;
@@ -715,12 +708,9 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
         };
         if (lane == 0) offer(cb, fbase + V, -1);
 #pragma unroll
-        for (int jj = 0; jj < PER; ++jj)
-          if (!(any_mod && modified(dense_f(jj) - fbase))) offer(dense_val(jj), dense_f(jj), -1);
+        for (int jj = 0; jj < PER; ++jj) offer(dense_val(jj), dense_f(jj), -1);
         for (int32_t i = lane; i < n_ov; i += 64)
-          if (!(any_mod && modified(S.ov_tok[w][i])))
-            offer(S.ov_val[w][i], fbase + S.ov_tok[w][i], S.ov_dst[w][i]);
-        if (any_mod && lane < K && my_mt >= 0) offer(my_mv, fbase + my_mt, my_md);
+          offer(S.ov_val[w][i], fbase + S.ov_tok[w][i], S.ov_dst[w][i]);
         float wv;
         int32_t wf;
         const int32_t wl = wave_argmax_dpp(bv, bf, wv, wf);
@@ -801,7 +791,6 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           S.hyp_hp[par ^ 1][w] = nhp;
           S.hyp_lv[par ^ 1][w] = nlv;
           S.hyp_node[par ^ 1][w] = nnode;
-          S.lse_ahead[par ^ 1][w] = lse_nxt;
         }
         tlen += total;
       }

@@ -4,11 +4,6 @@
 namespace tbias {
 namespace beamk {
 
-// Chunk counts 30 and 31 (V+1 in 1857..1984) are not instantiated: hipcc
-// (ROCm 7.2, gfx950) rejects this translation unit with them ("Illegal
-// instruction detected: Operand has incorrect register class", a comparison
-// against the shared aperture base), although each kernel compiles alone.
-// Those rows take the reference beam kernel.
 BeamLaunch beam_launcher_25_32(int per, int maxk, int32_t dtype) {
   switch (per) {
 #define TB_BEAM_CASE(P)                                                                   \
@@ -16,7 +11,7 @@ BeamLaunch beam_launcher_25_32(int per, int maxk, int32_t dtype) {
     if (maxk == 2) return dtype == TB_F32 ? &launch_beam_fast_t<LoadF32, P, 2> : &launch_beam_fast_t<LoadBF16, P, 2>; \
     if (maxk == 4) return dtype == TB_F32 ? &launch_beam_fast_t<LoadF32, P, 4> : &launch_beam_fast_t<LoadBF16, P, 4>; \
     return dtype == TB_F32 ? &launch_beam_fast_t<LoadF32, P, 8> : &launch_beam_fast_t<LoadBF16, P, 8>;
-     TB_BEAM_CASE(25) TB_BEAM_CASE(26) TB_BEAM_CASE(27) TB_BEAM_CASE(28) TB_BEAM_CASE(29) TB_BEAM_CASE(32)
+     TB_BEAM_CASE(25) TB_BEAM_CASE(26) TB_BEAM_CASE(27) TB_BEAM_CASE(28) TB_BEAM_CASE(29) TB_BEAM_CASE(30) TB_BEAM_CASE(31) TB_BEAM_CASE(32)
 #undef TB_BEAM_CASE
     default:
       return nullptr;

@@ -5,14 +5,12 @@
 namespace tbias {
 namespace beamk {
 
-// Chunk counts 30 and 31 (V+1 in 1857..1984) are not instantiated, as for the
-// plain beam kernel: the entry point rejects those rows.
 BeamStreamLaunch beam_stream_launcher_25_32(int per, int32_t dtype) {
   switch (per) {
 #define TB_STREAM_CASE(P) \
   case P:                 \
     return dtype == TB_F32 ? &launch_beam_stream_t<LoadF32, P> : &launch_beam_stream_t<LoadBF16, P>;
-    TB_STREAM_CASE(25) TB_STREAM_CASE(26) TB_STREAM_CASE(27) TB_STREAM_CASE(28) TB_STREAM_CASE(29) TB_STREAM_CASE(32)
+    TB_STREAM_CASE(25) TB_STREAM_CASE(26) TB_STREAM_CASE(27) TB_STREAM_CASE(28) TB_STREAM_CASE(29) TB_STREAM_CASE(30) TB_STREAM_CASE(31) TB_STREAM_CASE(32)
 #undef TB_STREAM_CASE
     default:
       return nullptr;

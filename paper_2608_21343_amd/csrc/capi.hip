@@ -213,7 +213,7 @@ extern "C" int tb_boost_step_beam_stream(const tb_arena* a, const void* logits, 
   if (tree_cap < 0) return fail(TB_EINVAL, "tree_cap must be >= 0");
   if (!beam_stream_supported(a->layout.v_plus_blank, a->layout.max_override, K))
     return fail(TB_EINVAL, "streaming beam: V+1 = " + std::to_string(a->layout.v_plus_blank) +
-                               " (needs K <= V+1 <= 2048, not 1857..1984) or an override set of " +
+                               " (needs K <= V+1 <= 2048) or an override set of " +
                                std::to_string(a->layout.max_override) +
                                " tokens (at most 256) not supported");
   if (T == 0) return TB_OK;  // no-op: buffers are not touched (and may be NULL)

@@ -172,6 +172,13 @@ __device__ __forceinline__ T sload(const T* p) {
   return *(const __attribute__((address_space(4))) T*)(p);
 }
 
+// A read through an explicitly global pointer: keeps the compiler from merging
+// it with an LDS read of the other branch into one generic (flat) load.
+template <class T>
+__device__ __forceinline__ T gload(const T* p) {
+  return *(const __attribute__((address_space(1))) T*)(p);
+}
+
 __device__ __forceinline__ uint4 sload4(const uint4* p) {
   const uint32_t* q = reinterpret_cast<const uint32_t*>(p);
   return make_uint4(sload(q), sload(q + 1), sload(q + 2), sload(q + 3));
@@ -265,12 +272,12 @@ struct SGraph {
   }
   // psi of state x (uniform): from its LDS record when usable, else the arena
   __device__ __forceinline__ float psi_of(int32_t x) const {
-    uint32_t a = 0u, c = 0x80000000u;
     if (x < nhot) {
-      a = w0[x];
-      c = w2[x];
+      const uint32_t a0 = w0[x], c0 = w2[x];
+      const uint32_t c = __builtin_amdgcn_readfirstlane(c0);
+      if (!(c >> 31)) return vpsi[__builtin_amdgcn_readfirstlane(a0) >> 24];
     }
-    return (c >> 31) ? A->psi[off + x] : vpsi[a >> 24];
+    return sload(A->psi + off + x);
   }
   // the same, from the arena when x has no usable LDS record
   __device__ __forceinline__ void rec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
@@ -427,8 +434,8 @@ __device__ __forceinline__ void child_rec(const SGraph& G, int32_t y, uint2& m, 
     }
   }
   const int64_t q = 2 * ((int64_t)G.off + y);
-  m = make_uint2(G.A->arc_mem[q], G.A->arc_mem[q + 1]);
-  py = G.A->psi[G.off + y];
+  m = make_uint2(gload(G.A->arc_mem + q), gload(G.A->arc_mem + q + 1));
+  py = gload(G.A->psi + G.off + y);
 }
 
 // Marks the classes of the children [fc, fc+nc).

@@ -423,6 +423,23 @@ def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, restore_ke
     assert np.all(gpu[2][:, 4] == -2)
 
 
+@pytest.mark.parametrize("V,K,dtype", [(1860, 8, "f32"), (1950, 4, "bf16"), (1983, 8, "bf16"),
+                                       (1856, 2, "f32")])
+def test_beam_rows_of_30_and_31_chunks(V, K, dtype):
+    """Rows of 1857..1984 logits (30 or 31 chunks of 64 per lane, ragged last
+    chunk) and the boundary below them, through the default beam kernel."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg, lists, rows = _small_case(7, B=6, V=V, n_case=V // 9, K=K, T=24, dtype=dtype)
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, 1, -1, 3, 4, 5], np.int32)
+    say(f"[beam-chunks] V+1={V + 1} K={K} {dtype}")
+    gpu = gpu_beam(dec, to_device_logits(rows), mids, 12)
+    graphs = oracle_graphs(cfg, lists, range(cfg.B), mids)
+    st0, S0 = oracle.init_carry(mids, K)
+    ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+    compare_beam(gpu, ref, range(cfg.B), ATOL)
+
+
 @pytest.mark.parametrize("kernel", ["default", "ref"])
 def test_beam_inside_long_phrases(kernel, restore_kernels):
     """Beam hypotheses deep inside 40-token phrases (chains of several suffix

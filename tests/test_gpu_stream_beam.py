@@ -102,7 +102,9 @@ def _merges(cfg, mids):
 
 
 @pytest.mark.parametrize("K,V,dtype", [(8, 1024, "f32"), (4, 300, "bf16"), (2, 1000, "f32"),
-                                       (8, 1999, "bf16"), (1, 63, "f32"), (5, 64, "f32")])
+                                       (8, 1999, "bf16"), (8, 1600, "f32"), (6, 1900, "f32"),
+                                       (1, 63, "f32"),
+                                       (5, 64, "f32")])
 def test_stream_beam_matches_the_oracle(K, V, dtype):
     cfg = _cfg(K + V, B=12, K=K, V=V, T=48, dtype=dtype)
     mids = np.arange(cfg.B, dtype=np.int32)
