@@ -17,6 +17,10 @@ What it computes (TurboBias 2.0, Sec. II):
 * ``decode.greedy_decode`` / ``decode.beam_decode``: per-stream boosted
   greedy and beam steps over joint-logit rows (Sec. II-B: each stream carries a
   model id, -1 meaning no biasing; Sec. II-C: state carried across chunks).
+* ``variative.build_variative_graph``: the case-insensitive variative BPE
+  graph of Sec. II-A (Fig. 1c, 1e) over a piece vocabulary, with the Eq. (1)
+  split of each backbone token's score over its characters, encoded as one
+  state per arc so that the same steps decode it.
 * ``decode.beam_decode_stream``: the streaming beam of Sec. II-C with
   hypothesis recombination (equal label sequences merged by log-add-exp) and a
   flattened tree of the kept label records.
@@ -36,6 +40,7 @@ chunk invariance).
 """
 
 from .graph import Graph, build_graph  # noqa: F401
+from .variative import build_variative_graph, class_map_of, eq1_split  # noqa: F401
 from .decode import (  # noqa: F401
     beam_decode,
     beam_decode_stream,
