@@ -174,6 +174,56 @@ int tb_graphs_layout(const tb_graphs* g, tb_arena_layout* out);
 int tb_graphs_host_image(const tb_graphs* g, void* dst, int64_t bytes);
 
 /*
+ * tb_compile_variative — per-stream phrase lists written in characters,
+ * compiled into the case-insensitive variative BPE graph (Sec. II-A, Fig. 1c
+ * and 1e) with the Eq. (1) potentials, as an arena image for the same step
+ * calls.
+ *
+ * The vocabulary is given as pieces: token v (0 <= v < V) spells
+ * token_chars[token_char_ptr[v] .. token_char_ptr[v+1]) (at least one
+ * character; codes in [0, n_chars)); lower[c] is the lowercase of character
+ * c. A token's class is the smallest token id with the same lowercased
+ * spelling (the class map of the image; the blank V has class -1). Every
+ * character used by a phrase must also be a single-character piece.
+ *
+ * Per list, the lowercased phrases form a character trie; from every node,
+ * every piece class whose lowercased spelling continues the trie is an arc to
+ * the node it reaches (a DAG: arcs of different lengths converge), with
+ * character-level suffix links. Each phrase's greedy tokenization (longest
+ * lowercased piece from the left) carries the score: backbone token k of
+ * m_k characters gives its i-th character the share
+ * token_w * exp((i+1)^tau) / sum_j exp((j+1)^tau) (float64), the running
+ * sum P along the phrase is kept per node (the largest over the phrases
+ * through it), and phi/E/psi follow `semantics` with P in place of the token
+ * count of tb_compile_graphs. Every arc is one state standing for the node it
+ * reaches: the arcs into a node share its child range, potentials and suffix
+ * link (the first arc into its longest proper suffix node). Nodes are
+ * numbered by increasing length, one length in order of first arc; a node's
+ * out-arcs are consecutive in ascending class order; the root is state 0.
+ *
+ *   model_phrase_ptr, phrase_char_ptr, phrase_chars  CSR as in
+ *                     tb_compile_graphs, over character codes
+ *   token_w, end_bonus, scale  as in tb_compile_graphs
+ *   token_char_ptr    host int64[V+1], token_chars host int32[...]
+ *   v_plus_blank      V + 1, in [2, 32768]
+ *   lower             host int32[n_chars], values in [0, n_chars)
+ *   tau               finite; 0 splits evenly, larger values move the score
+ *                     towards the end of each backbone token
+ *
+ * Errors: TB_EINVAL (null pointers, non-monotone CSR, v_plus_blank < 2,
+ * n_chars < 1, tau not finite, unknown semantics), TB_ERANGE (a character
+ * outside [0, n_chars), a token without characters, an empty phrase, a
+ * phrase character that is not a single-character piece, v_plus_blank >
+ * 32768), TB_ENOMEM.
+ */
+int tb_compile_variative(int32_t n_models, const int64_t* model_phrase_ptr,
+                         const int64_t* phrase_char_ptr, const int32_t* phrase_chars,
+                         const float* token_w, const float* end_bonus, const float* scale,
+                         const int64_t* token_char_ptr, const int32_t* token_chars,
+                         int32_t v_plus_blank, const int32_t* lower, int32_t n_chars, float tau,
+                         int32_t semantics, int32_t n_threads, tb_graphs** out);
+
+/*
  * Copy the arena image into caller-owned device memory dev_base (bytes >=
  * layout.total_bytes, 256-byte aligned) on stream and fill *out. Returns once
  * the copy has completed (the host graphs may be freed afterwards).
@@ -185,9 +235,10 @@ void tb_graphs_free(tb_graphs* g);
 
 /*
  * Check a host copy of an arena image for consistency (every index in range,
- * suffix links pointing to smaller ids, children contiguous with ascending
- * labels, root rows consistent with the root's children, class member lists
- * and arc member records consistent with the class map). TB_OK or TB_ERANGE.
+ * every suffix chain ending at the root, child ranges of non-root states with
+ * ascending labels, root rows consistent with the root's children, class
+ * member lists and arc member records consistent with the class map). TB_OK
+ * or TB_ERANGE.
  */
 int tb_validate_image(const void* host_image, const tb_arena_layout* layout);
 

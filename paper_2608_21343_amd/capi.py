@@ -68,6 +68,8 @@ def _load() -> C.CDLL:
     P, I32, I64 = C.c_void_p, C.c_int32, C.c_int64
     sig = {
         "tb_compile_graphs": [I32, P, P, P, P, P, P, P, I32, I32, I32, C.POINTER(C.c_void_p)],
+        "tb_compile_variative": [I32, P, P, P, P, P, P, P, P, I32, P, I32, C.c_float, I32, I32,
+                                 C.POINTER(C.c_void_p)],
         "tb_graphs_layout": [P, C.POINTER(tb_arena_layout)],
         "tb_graphs_host_image": [P, P, I64],
         "tb_graphs_upload": [P, P, I64, P, C.POINTER(tb_arena)],
@@ -117,7 +119,7 @@ EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb
             "tb_registry_layout", "tb_registry_create", "tb_registry_arena", "tb_registry_model",
             "tb_registry_used_states", "tb_register_models", "tb_unregister_workspace_bytes",
             "tb_unregister_model", "tb_registry_free", "tb_unregister_model_noalloc",
-            "tb_init_beam_stream", "tb_boost_step_beam_stream")
+            "tb_init_beam_stream", "tb_boost_step_beam_stream", "tb_compile_variative")
 
 
 def _check(code: int) -> None:
@@ -204,6 +206,31 @@ def tb_compile_graphs(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, 
                                  _np_ptr(tk) if tk.size else None, _np_ptr(tw), _np_ptr(eb),
                                  _np_ptr(sc) if sc is not None else None, _np_ptr(cm), len(cm),
                                  semantics, n_threads, C.byref(out)))
+    return Graphs(out.value)
+
+
+def tb_compile_variative(model_phrase_ptr, phrase_char_ptr, phrase_chars, token_w, end_bonus,
+                         token_char_ptr, token_chars, lower, tau: float, scale=None,
+                         semantics: int = TB_COMMIT, n_threads: int = 0) -> Graphs:
+    """Variative BPE graphs of character-coded phrase lists over a piece
+    vocabulary (token v spells token_chars[token_char_ptr[v]:token_char_ptr[v+1]])."""
+    mp = np.ascontiguousarray(model_phrase_ptr, dtype=np.int64)
+    pp = np.ascontiguousarray(phrase_char_ptr, dtype=np.int64)
+    pc = np.ascontiguousarray(phrase_chars, dtype=np.int32)
+    n_models = len(mp) - 1
+    tw = np.ascontiguousarray(np.broadcast_to(np.asarray(token_w, np.float32), (n_models,)))
+    eb = np.ascontiguousarray(np.broadcast_to(np.asarray(end_bonus, np.float32), (n_models,)))
+    sc = None if scale is None else np.ascontiguousarray(
+        np.broadcast_to(np.asarray(scale, np.float32), (n_models,)))
+    tp = np.ascontiguousarray(token_char_ptr, dtype=np.int64)
+    tc = np.ascontiguousarray(token_chars, dtype=np.int32)
+    lo = np.ascontiguousarray(lower, dtype=np.int32)
+    out = C.c_void_p()
+    _check(LIB.tb_compile_variative(n_models, _np_ptr(mp), _np_ptr(pp),
+                                    _np_ptr(pc) if pc.size else None, _np_ptr(tw), _np_ptr(eb),
+                                    _np_ptr(sc) if sc is not None else None, _np_ptr(tp),
+                                    _np_ptr(tc) if tc.size else None, len(tp), _np_ptr(lo),
+                                    len(lo), float(tau), semantics, n_threads, C.byref(out)))
     return Graphs(out.value)
 
 

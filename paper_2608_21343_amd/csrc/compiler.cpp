@@ -344,8 +344,15 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   for (int32_t m = 0; m < n_models; ++m)
     if (status[m] != TB_OK)
       return fail(status[m], "model " + std::to_string(m) + ": " + errs[m]);
+  return assemble_image(graphs, class_map, v_plus_blank, out);
+}
 
-  // assemble the arena image
+namespace tbias {
+
+int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_map,
+                   int32_t v_plus_blank, tb_graphs** out) {
+  const int32_t n_models = (int32_t)graphs.size();
+  const int32_t V = v_plus_blank - 1;
   auto* g = new (std::nothrow) tb_graphs();
   if (!g) return fail(TB_ENOMEM, "host allocation failed");
   tb_arena_layout& L = g->layout;
@@ -439,6 +446,8 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   return TB_OK;
 }
 
+}  // namespace tbias
+
 extern "C" int tb_graphs_layout(const tb_graphs* g, tb_arena_layout* out) {
   if (!g || !out) return fail(TB_EINVAL, "NULL argument");
   *out = g->layout;
@@ -478,16 +487,35 @@ extern "C" int tb_validate_image(const void* host_image, const tb_arena_layout* 
     const int32_t* lb = I32(L.off_label) + off;
     if (lk[0] != 0 || lb[0] != -1) return fail(TB_ERANGE, "bad root record");
     for (int32_t s = 0; s < n; ++s) {
-      if (s > 0 && (lk[s] < 0 || lk[s] >= s))
-        return fail(TB_ERANGE, "suffix link of state " + std::to_string(s) +
-                                   " does not point to a smaller id");
+      if (s > 0 && (lk[s] < 0 || lk[s] >= n))
+        return fail(TB_ERANGE, "suffix link of state " + std::to_string(s) + " out of range");
       if (s > 0 && (lb[s] < 0 || lb[s] >= V))
         return fail(TB_ERANGE, "label of state " + std::to_string(s) + " out of range");
-      if (nc[s] < 0 || (nc[s] > 0 && (fc[s] <= s || (int64_t)fc[s] + nc[s] > n)))
+      // children are non-root states; several states may share one child range
+      // (the arcs into one node of a variative graph)
+      if (nc[s] < 0 || (nc[s] > 0 && (fc[s] < 1 || (int64_t)fc[s] + nc[s] > n)))
         return fail(TB_ERANGE, "child range of state " + std::to_string(s) + " out of range");
       for (int32_t j = 1; j < nc[s]; ++j)
         if (lb[fc[s] + j] <= lb[fc[s] + j - 1])
           return fail(TB_ERANGE, "children labels not ascending");
+    }
+    // every suffix chain ends at the root: no cycle among the links
+    {
+      std::vector<uint8_t> col(n, 0);  // 0 unseen, 1 on the current chain, 2 ends at the root
+      std::vector<int32_t> chain;
+      col[0] = 2;
+      for (int32_t s = 1; s < n; ++s) {
+        int32_t x = s;
+        chain.clear();
+        while (col[x] == 0) {
+          col[x] = 1;
+          chain.push_back(x);
+          x = lk[x];
+        }
+        if (col[x] == 1)
+          return fail(TB_ERANGE, "suffix links of model " + std::to_string(m) + " form a cycle");
+        for (int32_t y : chain) col[y] = 2;
+      }
     }
     // root rows: the root move of a token is the root's child on its class,
     // else the root itself; its psi is that state's psi; the blank column is 0

@@ -35,6 +35,11 @@ int compile_model(const int32_t* toks, const int64_t* tok_ptr, int64_t n_phrases
                   const int32_t* class_map, int32_t V, double w, double bonus, double alpha,
                   int32_t semantics, ModelGraph* out);
 
+// Concatenate compiled models into one arena image (offsets, class tables,
+// arc member records, value tables, packed state records); *out owns it.
+int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_map,
+                   int32_t v_plus_blank, tb_graphs** out);
+
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 
 // Offsets (256-byte aligned) and total size of an arena image holding

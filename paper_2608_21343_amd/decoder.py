@@ -38,6 +38,30 @@ class BoostDecoder:
         self.V1 = int(len(class_map))
 
     @classmethod
+    def variative(cls, lists, pieces, lower, tau: float, token_w=1.0, end_bonus=2.0,
+                  scale=None, semantics: int = capi.TB_COMMIT, device="cuda") -> "BoostDecoder":
+        """Phrase lists written in characters, compiled into variative BPE
+        graphs over the piece vocabulary ``pieces`` (token id -> character
+        codes) with lowercasing map ``lower``."""
+        mp, pp, pc = [0], [0], []
+        for lst in lists:
+            for ph in lst:
+                pc.extend(int(c) for c in ph)
+                pp.append(pp[-1] + len(ph))
+            mp.append(len(pp) - 1)
+        tp = np.zeros(len(pieces) + 1, np.int64)
+        tp[1:] = np.cumsum([len(t) for t in pieces])
+        tc = np.asarray([c for t in pieces for c in t], np.int32)
+        self = cls.__new__(cls)
+        self.graphs = capi.tb_compile_variative(np.asarray(mp, np.int64), np.asarray(pp, np.int64),
+                                                np.asarray(pc, np.int32), token_w, end_bonus, tp,
+                                                tc, lower, tau, scale=scale, semantics=semantics)
+        self.arena = capi.tb_graphs_upload(self.graphs, device=device)
+        self.device = device
+        self.V1 = len(pieces) + 1
+        return self
+
+    @classmethod
     def for_arena(cls, arena, device="cuda") -> "BoostDecoder":
         """A decoder over an existing device arena (for example a registry's)."""
         self = cls.__new__(cls)

@@ -1,6 +1,6 @@
-// Host-side driver of the graph compiler and image validator, built with
+// Host-side driver of the graph compilers and image validator, built with
 // AddressSanitizer and UndefinedBehaviorSanitizer by tests/test_sanitize_cpu.py
-// (no GPU code is involved: compiler.cpp and errors.cpp only).
+// (no GPU code is involved: compiler.cpp, variative.cpp and errors.cpp only).
 //
 // It compiles random phrase lists (empty lists, duplicates, nested and long
 // phrases, case classes, several reading flags and thread counts), checks
@@ -104,6 +104,82 @@ void random_models(std::mt19937& rng) {
   }
 }
 
+// Variative graphs: random piece vocabularies over a small alphabet (every
+// character a piece, plus merged pieces, some of them cased), random phrase
+// lists; the image must validate and survive single-word corruption.
+void random_variative(std::mt19937& rng) {
+  const int32_t n_low = 3 + (int32_t)(rng() % 6);  // lowercase letters; then their uppercase
+  const int32_t n_chars = 2 * n_low;
+  std::vector<int32_t> lower(n_chars);
+  for (int32_t c = 0; c < n_chars; ++c) lower[c] = c % n_low;
+  std::vector<std::vector<int32_t>> toks;
+  for (int32_t c = 0; c < n_chars; ++c) toks.push_back({c});
+  const int n_merged = (int)(rng() % 60);
+  for (int i = 0; i < n_merged; ++i) {
+    std::vector<int32_t> t(2 + rng() % 5);
+    for (auto& c : t) c = (int32_t)(rng() % n_chars);
+    toks.push_back(t);
+  }
+  std::vector<int64_t> tp{0};
+  std::vector<int32_t> tc;
+  for (const auto& t : toks) {
+    tc.insert(tc.end(), t.begin(), t.end());
+    tp.push_back((int64_t)tc.size());
+  }
+  const int32_t V1 = (int32_t)toks.size() + 1;
+  Lists L;
+  const int M = 1 + (int)(rng() % 4);
+  for (int m = 0; m < M; ++m) {
+    std::vector<std::vector<int32_t>> ph;
+    const int n = (m == 0) ? 0 : (int)(rng() % 30);
+    for (int i = 0; i < n; ++i) {
+      std::vector<int32_t> p(1 + rng() % 12);
+      for (auto& c : p) c = (int32_t)(rng() % ((rng() & 1) ? 2 : n_chars));
+      ph.push_back(p);
+      if ((rng() & 7) == 0) ph.push_back(p);
+    }
+    L.add_model(ph);
+  }
+  const float taus[] = {0.f, 0.5f, 1.f, 2.f};
+  for (int32_t sem = 0; sem < 2; ++sem) {
+    std::vector<float> w(L.n_models(), 1.0f), be(L.n_models(), 2.0f);
+    tb_graphs* g = nullptr;
+    const int rc = tb_compile_variative(L.n_models(), L.mp.data(), L.tp.data(),
+                                        L.tok.empty() ? nullptr : L.tok.data(), w.data(), be.data(),
+                                        nullptr, tp.data(), tc.data(), V1, lower.data(), n_chars,
+                                        taus[rng() % 4], sem, 1 + (int32_t)(rng() % 3), &g);
+    expect(rc == TB_OK && g, "compile random variative lists");
+    if (!g) continue;
+    tb_arena_layout lay;
+    expect(tb_graphs_layout(g, &lay) == TB_OK, "variative layout");
+    std::vector<unsigned char> img(lay.total_bytes);
+    expect(tb_graphs_host_image(g, img.data(), lay.total_bytes) == TB_OK, "variative image");
+    expect(tb_validate_image(img.data(), &lay) == TB_OK, "validate variative image");
+    std::uniform_int_distribution<int64_t> pos(0, lay.total_bytes / 4 - 1);
+    for (int k = 0; k < 64; ++k) {
+      std::vector<unsigned char> bad = img;
+      const uint32_t vals[] = {0xffffffffu, 0x7fffffffu, 0x80000000u, 0u, 1u, (uint32_t)rng()};
+      std::memcpy(bad.data() + 4 * pos(rng), &vals[rng() % 6], 4);
+      const int r = tb_validate_image(bad.data(), &lay);
+      expect(r == TB_OK || r == TB_ERANGE, "validate corrupted variative image returns a status");
+    }
+    tb_graphs_free(g);
+  }
+  // a phrase character without a single-character piece
+  {
+    std::vector<int64_t> tp2{0, 2};
+    std::vector<int32_t> tc2{0, 1};
+    std::vector<int32_t> lw{0, 1};
+    std::vector<int64_t> mp{0, 1}, pp{0, 2};
+    std::vector<int32_t> pc{0, 1};
+    std::vector<float> one(1, 1.f);
+    tb_graphs* g = nullptr;
+    expect(tb_compile_variative(1, mp.data(), pp.data(), pc.data(), one.data(), one.data(), nullptr,
+                                tp2.data(), tc2.data(), 2, lw.data(), 2, 1.f, 0, 1, &g) ==
+               TB_ERANGE, "missing character piece");
+  }
+}
+
 void argument_errors() {
   const int32_t V = 50;
   const auto cm = class_map(V, 10);
@@ -159,6 +235,7 @@ void argument_errors() {
 int main() {
   std::mt19937 rng(12345);
   for (int i = 0; i < 60; ++i) random_models(rng);
+  for (int i = 0; i < 60; ++i) random_variative(rng);
   argument_errors();
   if (g_fail) {
     std::fprintf(stderr, "%d failures\n", g_fail);

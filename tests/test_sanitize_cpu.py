@@ -1,6 +1,6 @@
-"""The host graph compiler and image validator under AddressSanitizer and
-UndefinedBehaviorSanitizer (CPU only; g++ builds compiler.cpp, errors.cpp and
-tests/sanitize/compiler_driver.cpp, no GPU code)."""
+"""The host graph compilers and image validator under AddressSanitizer and
+UndefinedBehaviorSanitizer (CPU only; g++ builds compiler.cpp, variative.cpp,
+errors.cpp and tests/sanitize/compiler_driver.cpp, no GPU code)."""
 
 import os
 import shutil
@@ -18,7 +18,8 @@ def test_compiler_and_validator_under_asan_and_ubsan(tmp_path):
     cmd = ["g++", "-std=c++17", "-O1", "-g", "-pthread", "-ffp-contract=off",
            "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-fno-omit-frame-pointer",
-           os.path.join(CSRC, "compiler.cpp"), os.path.join(CSRC, "errors.cpp"),
+           os.path.join(CSRC, "compiler.cpp"), os.path.join(CSRC, "variative.cpp"),
+           os.path.join(CSRC, "errors.cpp"),
            os.path.join(ROOT, "tests", "sanitize", "compiler_driver.cpp"), "-o", str(exe)]
     r = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
     assert r.returncode == 0, r.stderr[-4000:]
