@@ -63,6 +63,8 @@ KERNELS = {
                      "(one call of 256 steps)",
     "stress_beam": "wide-row beam kernel, one workgroup per stream (one call of 256 steps)",
     "lifecycle": "greedy short-call kernel on a registry arena (one launch per 16-step chunk)",
+    "variative_streaming": "greedy short-call kernel on variative BPE graphs (one launch per "
+                           "16-step chunk)",
 }
 
 # CPU oracle sample per workload: (streams, steps); None = all
@@ -343,17 +345,37 @@ def main() -> int:
 
     if args.workload == "lifecycle":
         return lifecycle(args)
-    cfg = W.config_by_name(args.workload)
+    variative = args.workload.startswith("variative")
+    if variative:
+        import workloads.pieces as WP
+        cfg = WP.piece_config(args.workload)
+        args.no_cpu_baseline = True   # the oracle's variative compile is far too slow here
+    else:
+        cfg = W.config_by_name(args.workload)
     T, B, K, V1, chunk = cfg.T, cfg.B, cfg.K, cfg.Vp1, cfg.chunk
     item = 4 if cfg.dtype == "f32" else 2
-    lists = W.phrases(cfg)
-    t0 = time.perf_counter()
-    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
-    compile_s = time.perf_counter() - t0
+    if variative:
+        pieces = WP.vocab(cfg)
+        lists = WP.phrases(cfg)
+        t0 = time.perf_counter()
+        dec = BoostDecoder.variative(lists, pieces, WP.LOWER, cfg.tau, token_w=cfg.token_w,
+                                     end_bonus=cfg.end_bonus)
+        compile_s = time.perf_counter() - t0
+        plant_map = {}
+        for b, lst in enumerate(lists):
+            for t, v in WP.plants(cfg, b, pieces, lst):
+                plant_map.setdefault(t, []).append((b, v))
+        chunks_src = WP.logit_chunks(cfg, 16, plant_map=plant_map)
+    else:
+        lists = W.phrases(cfg)
+        t0 = time.perf_counter()
+        dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+        compile_s = time.perf_counter() - t0
+        chunks_src = W.logit_chunks(cfg, 16)
     dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
     logits = torch.empty((T, B, K, V1), dtype=dt, device="cuda")
     t0 = time.perf_counter()
-    for ta, tb, rows in W.logit_chunks(cfg, 16):
+    for ta, tb, rows in chunks_src:
         h = torch.from_numpy(rows if cfg.dtype == "f32" else rows.view(np.int16))
         logits[ta:tb].copy_(h.cuda().view(dt))
         del h, rows
@@ -364,7 +386,7 @@ def main() -> int:
     # consecutive bench steps read different buffers (at least 512 MiB apart).
     n_buf = max(1, -(-ROTATE_BYTES // (logits.numel() * item)))
     bufs = [logits] + [logits.clone() for _ in range(n_buf - 1)]
-    mids, states, scores = dec.start(W.model_ids(cfg), K)
+    mids, states, scores = dec.start(np.arange(B, dtype=np.int32), K)
     i32 = dict(dtype=torch.int32, device="cuda")
     f32 = dict(dtype=torch.float32, device="cuda")
     if K == 1:
@@ -543,6 +565,15 @@ def main() -> int:
                                 "frac": whole_bytes / whole_s / 1e9 / HBM_PEAK_GBS,
                                 "kernels": "segmented greedy kernel + boundary fix-up",
                                 "outputs_equal_chunked": bool(same)}
+    if variative:
+        L = dec.arena.layout
+        result["variative"] = {
+            "pieces": cfg.V, "tau": cfg.tau, "states": int(L.n_states),
+            "states_per_list": int(L.n_states) / B, "arena_MB": L.total_bytes / 1e6,
+            "max_override": int(L.max_override), "compile_s": compile_s,
+            "what": "lists written in characters over a synthetic piece vocabulary, one state "
+                    "per arc of the variative graph; phrases planted as random segmentations "
+                    "and casings every 16 steps"}
     if cfg.name == "beam":
         result["stream_beam"] = stream_beam_figures(dec, cfg, rows_bufs[0], W.model_ids(cfg),
                                                     stream)
