@@ -8,7 +8,10 @@ the factor that makes a plain device-to-device copy of known size read and
 write exactly its size, measured in the same counter run.
 
 Command line (turns two counter runs into the traffic record bench.py reads):
-  python -m paper_2608_21343_amd.profiling traffic FETCH_DIR WRITE_DIR KERNEL OUT.json
+  python -m paper_2608_21343_amd.profiling traffic FETCH_DIR WRITE_DIR KERNEL OUT.json [FIRST]
+FIRST limits the mean to the kernel's first FIRST dispatches (in dispatch
+order): with ``bench.py --steps 1 --warmup 0`` those are the timed step's
+calls, before the bench's context measurements launch the kernel again.
 """
 
 from __future__ import annotations
@@ -63,21 +66,23 @@ def kernel_stats(d: str) -> List[Dict[str, object]]:
 
 
 def counter_per_dispatch(d: str, counter: str) -> Dict[str, List[float]]:
-    """Counter value of every dispatch under d, grouped by kernel name."""
+    """Counter value of every dispatch under d, grouped by kernel name, in
+    dispatch order."""
     with open(_find(d, "counter_collection.csv")) as fh:
         rows = list(csv.DictReader(fh))
+    rows = [r for r in rows if r.get("Counter_Name") == counter]
+    rows.sort(key=lambda r: int(r["Dispatch_Id"]))
     by: Dict[str, List[float]] = {}
     for r in rows:
-        if r.get("Counter_Name") != counter:
-            continue
         by.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
     return by
 
 
-def _mean_for(by: Dict[str, List[float]], key: str) -> float:
-    vals = [v for k, vs in by.items() if key in k for v in vs]
-    if not vals:
-        raise KeyError(f"no dispatch of a kernel matching {key!r}")
+def _mean_for(by: Dict[str, List[float]], key: str, first: Optional[int] = None) -> float:
+    names = [k for k in by if key in k]
+    if len(names) != 1:
+        raise KeyError(f"{len(names)} kernels match {key!r}")
+    vals = by[names[0]][:first] if first else by[names[0]]
     return sum(vals) / len(vals)
 
 
@@ -89,16 +94,18 @@ def _copy_value(by: Dict[str, List[float]]) -> float:
     return max(vals)
 
 
-def traffic_record(fetch_dir: str, write_dir: str, kernel: str) -> Dict[str, object]:
+def traffic_record(fetch_dir: str, write_dir: str, kernel: str,
+                   first: Optional[int] = None) -> Dict[str, object]:
     f = counter_per_dispatch(fetch_dir, "FETCH_SIZE")
     w = counter_per_dispatch(write_dir, "WRITE_SIZE")
     kib = COPY_PROBE_BYTES / 1024.0
     f_scale = kib / _copy_value(f)
     w_scale = kib / _copy_value(w)
-    fetch = _mean_for(f, kernel)
-    write = _mean_for(w, kernel)
+    fetch = _mean_for(f, kernel, first)
+    write = _mean_for(w, kernel, first)
     return {
         "kernel": kernel,
+        "dispatches": first or "all",
         "kernel_hash": source_hash(),
         "fetch_kib_per_dispatch": fetch,
         "write_kib_per_dispatch": write,
@@ -121,8 +128,8 @@ def load_traffic(path: str) -> Optional[float]:
 
 
 def main(argv: List[str]) -> int:
-    if len(argv) == 5 and argv[0] == "traffic":
-        rec = traffic_record(argv[1], argv[2], argv[3])
+    if len(argv) in (5, 6) and argv[0] == "traffic":
+        rec = traffic_record(argv[1], argv[2], argv[3], int(argv[5]) if len(argv) == 6 else None)
         with open(argv[4], "w") as fh:
             json.dump(rec, fh, indent=1)
         print(json.dumps(rec))
