@@ -57,7 +57,7 @@ using seg::StateHot;
 using seg::Tables;
 
 constexpr int kOverCap = 256;  // override members listed per hypothesis
-constexpr int kCandCap = 128;  // candidates compacted for the final selection (multiple of 8)
+constexpr int kCandCap = 64;   // candidates compacted for the final selection (one per lane)
 constexpr int kList = 8;       // best root moves listed per row by beam_prep_kernel
 constexpr int kPrepThreads = 256;
 constexpr uint32_t kNoTok = 0xffffu;
@@ -643,7 +643,11 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       woff += (k < w) ? ck : 0;
       total += ck;
     }
-    const bool fast = theta > kNegInf && total <= kCandCap;
+    // one candidate per lane below: at most 64 take the fast path
+    const bool fast = theta > kNegInf && total <= 64;
+    int32_t sel_f_w = 0, sel_dst_w = -1;  // slot w's selection (uniform)
+    float sel_val_w = kNegInf;
+    int32_t nb_before = 0, nb_total = 0;  // kept non-blank extensions (streaming beam)
     if (fast) {
       int32_t p = woff + wpre;
       if (lane == 0 && cb >= theta) {
@@ -671,30 +675,30 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           ++p;
         }
       }
-      // pad the list to a multiple of 8 with entries that beat nothing
-      const int32_t total8 = (total + 7) & ~7;
-      if ((int32_t)threadIdx.x < total8 - total) {
-        S.cand_val[total + threadIdx.x] = kNegInf;
-        S.cand_f[total + threadIdx.x] = INT_MAX;
-      }
       __syncthreads();
-      // exact K best of the compacted candidates: the rank of a candidate is
-      // the number of candidates before it in (value, flat index) order, and
-      // flat indices are distinct, so ranks are distinct
-      for (int32_t i = threadIdx.x; i < total; i += nt) {
-        const float vi = S.cand_val[i];
-        const int32_t fi = S.cand_f[i];
-        int32_t rank = 0;
-        for (int32_t q0 = 0; q0 < total8; q0 += 8) {
-#pragma unroll
-          for (int q = 0; q < 8; ++q)
-            rank += cbetter(S.cand_val[q0 + q], S.cand_f[q0 + q], vi, fi);
-        }
-        if (rank < K) {
-          S.sel_val[rank] = vi;
-          S.sel_f[rank] = fi;
-          S.sel_dst[rank] = S.cand_dst[i];
-        }
+      // exact K best of the compacted candidates, ranked by every wave (one
+      // candidate per lane): the rank of a candidate is the number of
+      // candidates before it in (value, flat index) order, and flat indices
+      // are distinct, so ranks are distinct; slot w takes rank w
+      const bool in = lane < total;
+      const float vi = in ? S.cand_val[lane] : kNegInf;
+      const int32_t fi = in ? S.cand_f[lane] : INT_MAX;
+      const int32_t di = in ? S.cand_dst[lane] : -1;
+      int32_t rank = 0;
+      for (int32_t q = 0; q < total; ++q) {
+        const float vq = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vi), q));
+        const int32_t fq = __builtin_amdgcn_readlane(fi, q);
+        rank += cbetter(vq, fq, vi, fi) ? 1 : 0;
+      }
+      const uint64_t mine_lane = __ballot(in && rank == w);
+      const int32_t wl = mine_lane ? (int32_t)__builtin_ctzll(mine_lane) : 0;
+      sel_f_w = __builtin_amdgcn_readlane(fi, wl);
+      sel_val_w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vi), wl));
+      sel_dst_w = __builtin_amdgcn_readlane(di, wl);
+      if constexpr (STREAM) {
+        const bool nb = in && rank < K && fi - (fi / V1) * V1 != V;
+        nb_before = (int32_t)__builtin_popcountll(__ballot(nb && rank < w));
+        nb_total = (int32_t)__builtin_popcountll(__ballot(nb));
       }
     } else {
       // K rounds of a workgroup argmax over every candidate not yet taken
@@ -736,12 +740,23 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
         }
         __syncthreads();
       }
+      sel_f_w = __builtin_amdgcn_readfirstlane(S.sel_f[w]);
+      sel_val_w = S.sel_val[w];
+      sel_dst_w = __builtin_amdgcn_readfirstlane(S.sel_dst[w]);
+      if constexpr (STREAM) {
+        for (int32_t q = 0; q < K; ++q) {
+          int32_t fq = S.sel_f[q];
+          if (fq < 0 || fq >= K * V1) fq = 0;
+          const int32_t nb = (fq % V1 != V) ? 1 : 0;
+          nb_before += (q < w) ? nb : 0;
+          nb_total += nb;
+        }
+      }
     }
-    __syncthreads();
 
     // ---- slot w takes the w-th best
     {
-      int32_t f = __builtin_amdgcn_readfirstlane(S.sel_f[w]);
+      int32_t f = sel_f_w;
       if (f < 0 || f >= K * V1) f = 0;  // only reachable with nan logits
       const int32_t k = f / V1, v = f - k * V1;
       const int32_t sp = S.hyp_s[par][k];
@@ -752,7 +767,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
         if (v == V) {
           ns = sp;
         } else {
-          const int32_t d = __builtin_amdgcn_readfirstlane(S.sel_dst[w]);
+          const int32_t d = sel_dst_w;
           ns = (d >= 0) ? d : S.tab.rdst[v];
           bst = ((d >= 0) ? G.psi_of(ns) : S.tab.rpsi[v]) - phi_k;
         }
@@ -760,18 +775,11 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
         ns = unbiased_state(mode, S.tmo != 0);
       }
       const float z = S.zbuf[k][v];
-      const float val = S.sel_val[w];
+      const float val = sel_val_w;
       if constexpr (STREAM) {
         // the slot's hypothesis: the parent's, extended by v unless v is the
         // blank; kept non-blank extensions get tree records in slot order
-        int32_t before = 0, total = 0;
-        for (int32_t q = 0; q < K; ++q) {
-          int32_t fq = S.sel_f[q];
-          if (fq < 0 || fq >= K * V1) fq = 0;
-          const int32_t nb = (fq % V1 != V) ? 1 : 0;
-          before += (q < w) ? nb : 0;
-          total += nb;
-        }
+        const int32_t before = nb_before;
         const uint64_t hk = S.hyp_h[par][k];
         uint64_t nh = hk, nhp = S.hyp_hp[par][k];
         int32_t nlv = S.hyp_lv[par][k], nnode = S.hyp_node[par][k];
@@ -792,7 +800,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           S.hyp_lv[par ^ 1][w] = nlv;
           S.hyp_node[par ^ 1][w] = nnode;
         }
-        tlen += total;
+        tlen += nb_total;
       }
       if (lane == 0) {
         const int64_t o = o0 + (int64_t)t * ostride;
