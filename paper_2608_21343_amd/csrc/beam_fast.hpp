@@ -625,14 +625,35 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     }
     const float theta = wave_nth_largest(lval, K);
 
-    // count and compact every candidate >= theta
+    // count every candidate >= theta, keeping a lane's first two in registers
     int32_t mine = 0;
+    float kv0 = kNegInf, kv1 = kNegInf;
+    int32_t kf0 = 0, kf1 = 0, kd0 = -1, kd1 = -1;
+#define TB_KEEP(pass, v, f, d)                                       \
+  {                                                                  \
+    const bool p0_ = (pass) && mine == 0, p1_ = (pass) && mine == 1; \
+    kv0 = p0_ ? (v) : kv0;                                           \
+    kf0 = p0_ ? (f) : kf0;                                           \
+    kd0 = p0_ ? (d) : kd0;                                           \
+    kv1 = p1_ ? (v) : kv1;                                           \
+    kf1 = p1_ ? (f) : kf1;                                           \
+    kd1 = p1_ ? (d) : kd1;                                           \
+    mine += (pass) ? 1 : 0;                                          \
+  }
     if (theta > kNegInf) {
-      mine = (lane == 0 && cb >= theta) ? 1 : 0;
+      TB_KEEP(lane == 0 && cb >= theta, cb, fbase + V, -1);
 #pragma unroll
-      for (int j = 0; j < PER; ++j) mine += dense_val(j) >= theta;
-      for (int32_t i = lane; i < n_ov; i += 64) mine += S.ov_val[w][i] >= theta;
+      for (int j = 0; j < PER; ++j) {
+        const float v = dense_val(j);
+        TB_KEEP(v >= theta, v, dense_f(j), -1);
+      }
+      for (int32_t i = lane; i < n_ov; i += 64) {
+        const float v = S.ov_val[w][i];
+        const int32_t tk = S.ov_tok[w][i], dd = S.ov_dst[w][i];
+        TB_KEEP(v >= theta, v, fbase + tk, dd);
+      }
     }
+#undef TB_KEEP
     int32_t wtot;
     const int32_t wpre = wave_excl_scan(mine, wtot);
     if (lane == 0) S.cnt_w[w] = wtot;
@@ -648,7 +669,20 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     int32_t sel_f_w = 0, sel_dst_w = -1;  // slot w's selection (uniform)
     float sel_val_w = kNegInf;
     int32_t nb_before = 0, nb_total = 0;  // kept non-blank extensions (streaming beam)
-    if (fast) {
+    if (fast && __ballot(mine > 2) == 0ull) {
+      // every lane's candidates are in its registers
+      const int32_t p = woff + wpre;
+      if (mine > 0) {
+        S.cand_val[p] = kv0;
+        S.cand_f[p] = kf0;
+        S.cand_dst[p] = kd0;
+      }
+      if (mine > 1) {
+        S.cand_val[p + 1] = kv1;
+        S.cand_f[p + 1] = kf1;
+        S.cand_dst[p + 1] = kd1;
+      }
+    } else if (fast) {
       int32_t p = woff + wpre;
       if (lane == 0 && cb >= theta) {
         S.cand_val[p] = cb;
@@ -675,6 +709,8 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           ++p;
         }
       }
+    }
+    if (fast) {
       __syncthreads();
       // exact K best of the compacted candidates, ranked by every wave (one
       // candidate per lane): the rank of a candidate is the number of
