@@ -354,10 +354,9 @@ int tb_init_beam_stream(const tb_arena* a, int32_t B, int32_t K, const int32_t* 
  *   recombine 0: no merging (then the outputs equal tb_boost_step_beam's)
  *
  * Label sequences are compared by their hashes (a collision of two different
- * sequences among one stream's live slots would merge them). Supports
- * K <= V+1 <= 2048, K <= 8 and arenas whose largest
- * override set has at most 256 tokens: TB_EINVAL otherwise. Concurrent calls
- * on the same carry race.
+ * sequences among one stream's live slots would merge them). K in [1,
+ * TB_MAX_BEAM] and K <= V+1, else TB_EINVAL. Concurrent calls on the same
+ * carry race.
  */
 int tb_boost_step_beam_stream(const tb_arena* a, const void* logits, int32_t dtype, int32_t T,
                               int32_t B, int32_t K, int64_t row_stride, const int32_t* model_ids,

@@ -75,12 +75,20 @@ __device__ inline int32_t ac_move(const ArenaView& A, int32_t off, int32_t x, in
   }
 }
 
-template <class Ld, int MAXK>
+// With STREAM, the streaming beam (tb_boost_step_beam_stream) for rows and
+// beams the one-wave-per-hypothesis kernel does not take: every hypothesis'
+// normaliser first, then the recombination of equal label sequences (x's
+// blank extension and the extension of x's prefix slot y by x's last label:
+// the better in (value, flat index) order gets log(e^a + e^b), the other
+// -inf), applied to the candidates as they are formed; hashes and tree
+// records as in the fast kernel.
+template <class Ld, int MAXK, bool STREAM>
 __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int32_t K,
     int64_t stride, const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
     float* __restrict__ scores, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_parent,
-    int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum) {
+    int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum,
+    beamk::StreamArgs sa) {
   extern __shared__ int32_t smem[];
   const int32_t V1 = A.V1, V = V1 - 1;
   int32_t* odst = smem;
@@ -95,6 +103,14 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
   __shared__ int32_t sel_idx[MAXK];
   __shared__ float sel_val[MAXK];
   __shared__ int32_t sh_bad, sh_tmo;
+  // streaming beam: hypothesis carry and this step's merges (slot y's
+  // patched tokens and values; slot x's blank)
+  constexpr int SK = STREAM ? MAXK : 1;
+  __shared__ uint64_t sh_h[SK], sh_hp[SK];
+  __shared__ int32_t sh_lv[SK], sh_node[SK];
+  __shared__ int32_t mod_n[SK], mod_tok[SK][SK];
+  __shared__ float mod_val[SK][SK], blank_val[SK];
+  __shared__ int32_t blank_set[SK];
 
   const int tid = threadIdx.x;
   const int32_t b = blockIdx.x;
@@ -111,6 +127,18 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
     sh_S[tid] = scores[(int64_t)b * K + tid];
     if (mode == 1 && (s < 0 || s >= n)) sh_bad = 1;
     if (s == TB_STATE_TIMEOUT) sh_tmo = 1;
+    if constexpr (STREAM) {
+      const tb_hyp hy = sa.hyps[(int64_t)b * K + tid];
+      sh_h[tid] = hy.hash;
+      sh_hp[tid] = hy.prefix_hash;
+      sh_lv[tid] = hy.last;
+      sh_node[tid] = hy.node;
+    }
+  }
+  int32_t tlen = 0;
+  if constexpr (STREAM) {
+    const int32_t l = sa.tree_len[b];
+    tlen = l < 0 ? 0 : (l > sa.cap ? sa.cap : l);
   }
   for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
   __syncthreads();
@@ -125,8 +153,10 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
 #pragma unroll
     for (int j = 0; j < MAXK; ++j) { lk[j] = -__builtin_huge_valf(); li[j] = INT_MAX; }
 
-    for (int32_t k = 0; k < K; ++k) {
-      const typename Ld::T* row = logits + (((int64_t)t * B + b) * K + k) * stride;
+    auto row_of = [&](int32_t k) {
+      return logits + (((int64_t)t * B + b) * K + k) * stride;
+    };
+    auto row_lse = [&](const typename Ld::T* row) -> float {
       float mx = -__builtin_huge_valf();
       for (int32_t v = tid; v < V1; v += kThreads) mx = fmaxf(mx, Ld::get(row, v));
       mx = bmax(mx, redf);
@@ -134,7 +164,57 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
       const double mxd = (double)mx;
       for (int32_t v = tid; v < V1; v += kThreads) se += exp((double)Ld::get(row, v) - mxd);
       se = bsum_d(se, redd);
-      const float lse = (float)(mxd + log(se));
+      return (float)(mxd + log(se));
+    };
+    if constexpr (STREAM) {
+      // every hypothesis' normaliser and phi, then the merges of the step
+      for (int32_t k = 0; k < K; ++k) {
+        const float l = row_lse(row_of(k));
+        if (tid == 0) {
+          sh_lse[k] = l;
+          sh_phi[k] = (mode == 1) ? A.phi[off + sh_state[k]] : 0.f;
+        }
+      }
+      if (tid < K) {
+        mod_n[tid] = 0;
+        blank_set[tid] = 0;
+      }
+      __syncthreads();
+      if (tid == 0 && sa.recombine) {
+        for (int32_t x = 0; x < K; ++x) {
+          const int32_t v = sh_lv[x];
+          if (!(sh_S[x] > -__builtin_huge_valf()) || v < 0 || v >= V) continue;
+          for (int32_t y = 0; y < K; ++y) {
+            if (y == x || !(sh_S[y] > -__builtin_huge_valf()) || sh_h[y] != sh_hp[x]) continue;
+            const float cx = (sh_S[x] - sh_lse[x]) - sh_phi[x];
+            const float cy = (sh_S[y] - sh_lse[y]) - sh_phi[y];
+            const float psi_x = (mode == 1) ? A.psi[off + sh_state[x]] : 0.f;
+            const float a = cx + (Ld::get(row_of(x), V) + sh_phi[x]);
+            const float bv = cy + (Ld::get(row_of(y), v) + psi_x);
+            if (a > -__builtin_huge_valf() && bv > -__builtin_huge_valf()) {
+              const float merged = beamk::logaddexp32(a, bv);
+              const bool keep_a = a > bv || (a == bv && x * V1 + V < y * V1 + v);
+              blank_set[x] = 1;
+              blank_val[x] = keep_a ? merged : -__builtin_huge_valf();
+              const int32_t q = mod_n[y]++;
+              mod_tok[y][q] = v;
+              mod_val[y][q] = keep_a ? -__builtin_huge_valf() : merged;
+            }
+            break;  // the first prefix slot in index order
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    for (int32_t k = 0; k < K; ++k) {
+      const typename Ld::T* row = row_of(k);
+      float lse;
+      if constexpr (STREAM) {
+        lse = sh_lse[k];
+      } else {
+        lse = row_lse(row);
+      }
       const int32_t s = sh_state[k];
 
       float phi_s = 0.f;
@@ -171,7 +251,15 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
           }
         }
         const float key = z + p;
-        const float cand = ck + key;
+        float cand = ck + key;
+        if constexpr (STREAM) {
+          if (v == V) {
+            if (blank_set[k]) cand = blank_val[k];
+          } else {
+            for (int32_t q = 0; q < mod_n[k]; ++q)
+              if (mod_tok[k][q] == v) cand = mod_val[k][q];
+          }
+        }
         const int32_t f = k * V1 + v;
         if (better(cand, f, lk[MAXK - 1], li[MAXK - 1])) {
           lk[MAXK - 1] = cand;
@@ -206,11 +294,44 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
 
     int32_t ns = 0;
     float nS = 0.f;
+    uint64_t nh = 0ull, nhp = 0ull;
+    int32_t nlv = -1, nnode = -1;
+    int32_t nb_total = 0;  // kept non-blank extensions (streaming beam)
+    if constexpr (STREAM) {
+      for (int32_t q = 0; q < K; ++q) {
+        int32_t fq = sel_idx[q];
+        if (fq < 0 || fq >= K * V1) fq = 0;
+        nb_total += (fq % V1 != V) ? 1 : 0;
+      }
+    }
     if (tid < K) {
       const int32_t j = tid;
       int32_t f = sel_idx[j];
       if (f < 0 || f >= K * V1) f = 0;  // only reachable with NaN logits
       const int32_t k = f / V1, v = f - k * V1;
+      if constexpr (STREAM) {
+        int32_t before = 0;
+        for (int32_t q = 0; q < j; ++q) {
+          int32_t fq = sel_idx[q];
+          if (fq < 0 || fq >= K * V1) fq = 0;
+          before += (fq % V1 != V) ? 1 : 0;
+        }
+        nh = sh_h[k];
+        nhp = sh_hp[k];
+        nlv = sh_lv[k];
+        nnode = sh_node[k];
+        if (v != V) {
+          const int32_t r = tlen + before;
+          nhp = sh_h[k];
+          nh = sh_h[k] * (uint64_t)TB_HASH_MUL + (uint64_t)(v + 1);
+          nlv = v;
+          nnode = (r < sa.cap) ? r : -2;
+          if (r < sa.cap) {
+            sa.tree[((int64_t)b * sa.cap + r) * 2] = v;
+            sa.tree[((int64_t)b * sa.cap + r) * 2 + 1] = sh_node[k];
+          }
+        }
+      }
       const int32_t s = sh_state[k];
       float bst = 0.f;
       if (mode == 1) {
@@ -235,43 +356,62 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
       out_cum[o] = nS;
     }
     __syncthreads();
-    if (tid < K) { sh_state[tid] = ns; sh_S[tid] = nS; }
+    if (tid < K) {
+      sh_state[tid] = ns;
+      sh_S[tid] = nS;
+      if constexpr (STREAM) {
+        sh_h[tid] = nh;
+        sh_hp[tid] = nhp;
+        sh_lv[tid] = nlv;
+        sh_node[tid] = nnode;
+      }
+    }
+    if constexpr (STREAM) tlen += nb_total;
     __syncthreads();
   }
   if (tid < K && T > 0) {
     states[(int64_t)b * K + tid] = sh_state[tid];
     scores[(int64_t)b * K + tid] = sh_S[tid];
+    if constexpr (STREAM) {
+      tb_hyp hy;
+      hy.hash = sh_h[tid];
+      hy.prefix_hash = sh_hp[tid];
+      hy.last = sh_lv[tid];
+      hy.node = sh_node[tid];
+      sa.hyps[(int64_t)b * K + tid] = hy;
+      if (tid == 0) sa.tree_len[b] = tlen < sa.cap ? tlen : sa.cap;
+    }
   }
 }
 
-template <class Ld, int MAXK>
+template <class Ld, int MAXK, bool STREAM>
 void launch_t(const ArenaView& A, const void* logits, int32_t T, int32_t B, int32_t K,
               int64_t stride, const int32_t* model_ids, int32_t* states, float* scores,
               int32_t* out_tok, int32_t* out_parent, int32_t* out_state, float* out_step,
-              float* out_cum, hipStream_t st) {
+              float* out_cum, hipStream_t st, beamk::StreamArgs sa) {
   const size_t lds = (size_t)6 * (A.V1 - 1) + 4;
-  hipLaunchKernelGGL((beam_ref_kernel<Ld, MAXK>), dim3(B), dim3(kThreads), lds, st, A,
+  hipLaunchKernelGGL((beam_ref_kernel<Ld, MAXK, STREAM>), dim3(B), dim3(kThreads), lds, st, A,
                      static_cast<const typename Ld::T*>(logits), T, B, K, stride, model_ids,
-                     states, scores, out_tok, out_parent, out_state, out_step, out_cum);
+                     states, scores, out_tok, out_parent, out_state, out_step, out_cum, sa);
 }
 
-template <class Ld>
+template <class Ld, bool STREAM = false>
 void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int32_t K,
               int64_t stride, const int32_t* model_ids, int32_t* states, float* scores,
               int32_t* out_tok, int32_t* out_parent, int32_t* out_state, float* out_step,
-              float* out_cum, hipStream_t st) {
+              float* out_cum, hipStream_t st, beamk::StreamArgs sa = beamk::StreamArgs{}) {
   if (K <= 2)
-    launch_t<Ld, 2>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
-                    out_state, out_step, out_cum, st);
+    launch_t<Ld, 2, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
+                            out_parent, out_state, out_step, out_cum, st, sa);
   else if (K <= 4)
-    launch_t<Ld, 4>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
-                    out_state, out_step, out_cum, st);
+    launch_t<Ld, 4, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
+                            out_parent, out_state, out_step, out_cum, st, sa);
   else if (K <= 8)
-    launch_t<Ld, 8>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
-                    out_state, out_step, out_cum, st);
+    launch_t<Ld, 8, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
+                            out_parent, out_state, out_step, out_cum, st, sa);
   else
-    launch_t<Ld, 16>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok, out_parent,
-                     out_state, out_step, out_cum, st);
+    launch_t<Ld, 16, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
+                             out_parent, out_state, out_step, out_cum, st, sa);
 }
 
 }  // namespace
@@ -328,8 +468,8 @@ hipError_t launch_beam(const ArenaView& A, const void* logits, int32_t dtype, in
 }
 
 // The streaming beam runs the one-wave-per-hypothesis kernel with the
-// recombination and tree stages (K <= 8, V+1 <= 2048, override sets within
-// its lists).
+// recombination and tree stages where that kernel applies (K <= 8, V+1 <=
+// 2048, override sets within its lists), else the reference kernel's.
 bool beam_stream_supported(int32_t v_plus_blank, int32_t max_override, int32_t K) {
   if (K < 1 || K > 8 || v_plus_blank < 2 || v_plus_blank > 64 * 32 || K > v_plus_blank)
     return false;
@@ -342,21 +482,30 @@ hipError_t launch_beam_stream(const ArenaView& A, const void* logits, int32_t dt
                               int32_t tree_cap, int32_t* tree_len, int32_t recombine,
                               int32_t* out_tok, int32_t* out_parent, int32_t* out_state,
                               float* out_step, float* out_cum, hipStream_t st) {
-  if (!beam_stream_supported(A.V1, A.max_override, K)) return hipErrorNotSupported;
-  const int per = (A.V1 + 63) / 64;
-  beamk::BeamStreamLaunch f = per <= 8    ? beamk::beam_stream_launcher_1_8(per, dtype)
-                              : per <= 16 ? beamk::beam_stream_launcher_9_16(per, dtype)
-                              : per <= 24 ? beamk::beam_stream_launcher_17_24(per, dtype)
-                                          : beamk::beam_stream_launcher_25_32(per, dtype);
-  if (!f) return hipErrorNotSupported;
   beamk::StreamArgs sa;
   sa.hyps = hyps;
   sa.tree = tree;
   sa.cap = tree_cap;
   sa.tree_len = tree_len;
   sa.recombine = recombine;
-  return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
-           out_state, out_step, out_cum, st, sa);
+  if (debug_beam_kernel() != kBeamRef && beam_stream_supported(A.V1, A.max_override, K)) {
+    const int per = (A.V1 + 63) / 64;
+    beamk::BeamStreamLaunch f = per <= 8    ? beamk::beam_stream_launcher_1_8(per, dtype)
+                                : per <= 16 ? beamk::beam_stream_launcher_9_16(per, dtype)
+                                : per <= 24 ? beamk::beam_stream_launcher_17_24(per, dtype)
+                                            : beamk::beam_stream_launcher_25_32(per, dtype);
+    if (f)
+      return f(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok, out_parent,
+               out_state, out_step, out_cum, st, sa);
+  }
+  // any other row width, beam or override set: the reference kernel's stage
+  if (dtype == TB_F32)
+    launch_k<LoadF32, true>(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok,
+                            out_parent, out_state, out_step, out_cum, st, sa);
+  else
+    launch_k<LoadBF16, true>(A, logits, T, B, K, row_stride, model_ids, states, scores, out_tok,
+                             out_parent, out_state, out_step, out_cum, st, sa);
+  return hipGetLastError();
 }
 
 }  // namespace tbias

@@ -209,13 +209,9 @@ extern "C" int tb_boost_step_beam_stream(const tb_arena* a, const void* logits, 
   if ((r = check_arena(a))) return r;
   if (T < 0) return fail(TB_EINVAL, "T must be >= 0");
   if (B < 1) return fail(TB_EINVAL, "B must be >= 1");
-  if (K < 1 || K > 8) return fail(TB_EINVAL, "streaming beam: K outside [1, 8]");
+  if (K < 1 || K > TB_MAX_BEAM) return fail(TB_EINVAL, "K outside [1, TB_MAX_BEAM]");
+  if (K > a->layout.v_plus_blank) return fail(TB_EINVAL, "K exceeds V+1");
   if (tree_cap < 0) return fail(TB_EINVAL, "tree_cap must be >= 0");
-  if (!beam_stream_supported(a->layout.v_plus_blank, a->layout.max_override, K))
-    return fail(TB_EINVAL, "streaming beam: V+1 = " + std::to_string(a->layout.v_plus_blank) +
-                               " (needs K <= V+1 <= 2048) or an override set of " +
-                               std::to_string(a->layout.max_override) +
-                               " tokens (at most 256) not supported");
   if (T == 0) return TB_OK;  // no-op: buffers are not touched (and may be NULL)
   if ((r = check_logits(logits, dtype, row_stride, a->layout.v_plus_blank))) return r;
   if ((r = check_i32(model_ids, "model_ids"))) return r;

@@ -24,3 +24,11 @@ def pytest_collection_modifyitems(config, items):
     for it in items:
         if "gpu" in it.keywords:
             it.add_marker(skip)
+
+
+@pytest.fixture
+def restore_kernels():
+    """Tests that force a kernel family leave the automatic choice behind them."""
+    yield
+    from paper_2608_21343_amd import capi
+    capi.tb_debug_select_kernels(capi.GREEDY_AUTO, capi.BEAM_AUTO)

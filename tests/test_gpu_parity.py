@@ -24,13 +24,6 @@ pytestmark = pytest.mark.gpu
 ATOL = 1e-5
 
 
-@pytest.fixture
-def restore_kernels():
-    """Tests that force a kernel family leave the automatic choice behind them."""
-    yield
-    capi.tb_debug_select_kernels(capi.GREEDY_AUTO, capi.BEAM_AUTO)
-
-
 def _decoder(cfg, lists):
     from paper_2608_21343_amd.decoder import BoostDecoder
     return BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)

@@ -113,6 +113,27 @@ def test_stream_beam_matches_the_oracle(K, V, dtype):
     _run(cfg, mids, chunk=16)
 
 
+@pytest.mark.parametrize("K,V,dtype", [(4, 3000, "f32"), (12, 500, "f32"), (3, 5000, "bf16")])
+def test_stream_beam_on_the_reference_kernel(K, V, dtype):
+    """Rows wider than 2048 and beams wider than 8: the reference kernel's
+    streaming stage."""
+    cfg = _cfg(K * 7 + V, B=6, K=K, V=V, T=32, dtype=dtype)
+    mids = np.arange(cfg.B, dtype=np.int32)
+    mids[2] = -1
+    say(f"[stream-beam-ref] K={K} V={V} {dtype}: merges on {_merges(cfg, mids)} stream-steps")
+    _run(cfg, mids, chunk=16)
+
+
+def test_stream_beam_reference_kernel_forced(restore_kernels):
+    """The reference kernel's streaming stage on a row the fast kernel would
+    take, forced through the test hook."""
+    from paper_2608_21343_amd import capi
+    capi.tb_debug_select_kernels(beam=capi.BEAM_REF)
+    cfg = _cfg(77, B=8, K=8, V=700, T=32)
+    mids = np.arange(cfg.B, dtype=np.int32)
+    _run(cfg, mids, chunk=16)
+
+
 def test_recombination_is_exercised():
     cfg = _cfg(1, B=12, K=8, V=1024, T=24)
     assert _merges(cfg, np.arange(cfg.B, dtype=np.int32)) >= 20
@@ -187,13 +208,16 @@ def test_argument_errors():
     with pytest.raises(ValueError):   # a short hypothesis buffer
         capi.tb_boost_step_beam_stream(dec.arena, rows_dev, c.mids, c.states, c.scores,
                                        c.hyps[:3], c.tree, c.tree_len, *outs(4))
-    # K > 8 is not served by the streaming kernel
-    cfg9 = _cfg(6, B=2, K=9, V=100, T=4)
-    rows9 = to_device_logits(W.logits(cfg9))
-    c9 = dec.start_beam_stream(mids, 9, 16)
+    # K beyond TB_MAX_BEAM
+    cfg17 = _cfg(6, B=2, K=17, V=100, T=4)
+    rows17 = to_device_logits(W.logits(cfg17))
+    c17 = dec.start_beam_stream(mids, 16, 16)
+    hyps17 = torch.zeros((2 * 17, 3), dtype=torch.int64, device="cuda")
     with pytest.raises(capi.TbError) as e:
-        capi.tb_boost_step_beam_stream(dec.arena, rows9, c9.mids, c9.states, c9.scores, c9.hyps,
-                                       c9.tree, c9.tree_len, *outs(9))
+        capi.tb_boost_step_beam_stream(dec.arena, rows17, c17.mids,
+                                       torch.zeros(34, dtype=torch.int32, device="cuda"),
+                                       torch.zeros(34, dtype=torch.float32, device="cuda"),
+                                       hyps17, c17.tree, c17.tree_len, *outs(17))
     assert e.value.code == capi.TB_EINVAL
 
 

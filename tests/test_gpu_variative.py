@@ -119,3 +119,38 @@ def test_variative_matches_class_graph_for_single_character_pieces():
     gb = gpu_greedy(b, to_device_logits(rows), mids, 16)
     for x, y in zip(ga, gb):
         assert np.array_equal(x, y)
+
+
+def test_variative_models_in_a_registry():
+    """Variative graphs through the model lifecycle: register compiled lists,
+    remove one (left-shift compaction; suffix links need not point to smaller
+    ids here), then decode through the registry arena against the oracle."""
+    from paper_2608_21343_amd import capi
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg, toks, lists, rows = _case(B=6, T=64, seed=13)
+    cm = oracle.class_map_of(toks, WP.LOWER)
+    reg = capi.Registry(max_models=6, max_states=200000, class_map=cm)
+
+    def compiled(idx):
+        sub = [lists[i] for i in idx]
+        return BoostDecoder.variative(sub, toks, WP.LOWER, cfg.tau).graphs
+
+    ids = reg.register(compiled([0, 1, 2])) + reg.register(compiled([3, 4, 5]))
+    holds = dict(zip(ids, range(6)))
+    victim = ids[1]
+    reg.unregister(victim)
+    del holds[victim]
+    # stream j carries model id j (model ids[1] is free and decodes unbiased)
+    mids = np.asarray(list(range(6)), np.int32)
+    dec = BoostDecoder.for_arena(reg.arena)
+    gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, 16)
+    graphs = {m: oracle.build_variative_graph(toks, WP.LOWER, lists[holds[m]], tau=cfg.tau)
+              for m in holds}
+    ref_mids = np.asarray([m if m in holds else -1 for m in mids], np.int32)
+    st0 = np.where(ref_mids >= 0, 0, -1).astype(np.int32)
+    ref = oracle.greedy_decode(graphs, ref_mids, rows[:, :, 0, :], st0)
+    assert np.array_equal(gpu[0], ref[0])
+    live = [j for j in range(6) if mids[j] in holds]
+    assert np.array_equal(gpu[1][:, live], ref[1][:, live])
+    assert np.all(gpu[1][:, [j for j in range(6) if j not in live]] == capi.TB_STATE_INVALID)
+    assert np.max(np.abs(gpu[2] - ref[2])) <= 1e-5
