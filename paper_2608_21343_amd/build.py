@@ -43,20 +43,28 @@ def _hipcc() -> str:
     return str(p) if p.exists() else (shutil.which("hipcc") or "hipcc")
 
 
-def build_library(verbose: bool = False) -> Path:
-    """Compile every source and link libtbias.so next to this file."""
-    BUILD.mkdir(exist_ok=True)
+def build_library(verbose: bool = False, poison: bool = False) -> Path:
+    """Compile every source and link libtbias.so next to this file.
+
+    poison=True builds the LDS-poisoning debug variant (every kernel fills its
+    LDS with all bits set before use) as libtbias_poison.so, for the test
+    that decodes through it. A failed build removes the library it would
+    have replaced, so that nothing runs a stale build."""
+    build_dir = BUILD if not poison else PKG / "_build_poison"
+    out_lib = LIB if not poison else PKG / "libtbias_poison.so"
+    extra = [] if not poison else ["-DTB_POISON_LDS"]
+    build_dir.mkdir(exist_ok=True)
     hipcc = _hipcc()
     cxx = shutil.which("g++") or "g++"
     jobs = []
     objs = []
     for src in HIP_SOURCES:
-        obj = BUILD / (src + ".o")
+        obj = build_dir / (src + ".o")
         objs.append(obj)
-        jobs.append([hipcc, *HIPCC_FLAGS, *HIP_EXTRA.get(src, []), "-c", str(CSRC / src), "-o",
-                     str(obj)])
+        jobs.append([hipcc, *HIPCC_FLAGS, *extra, *HIP_EXTRA.get(src, []), "-c", str(CSRC / src),
+                     "-o", str(obj)])
     for src in CXX_SOURCES:
-        obj = BUILD / (src + ".o")
+        obj = build_dir / (src + ".o")
         objs.append(obj)
         jobs.append([cxx, *CXX_FLAGS, "-c", str(CSRC / src), "-o", str(obj)])
     procs = []
@@ -72,19 +80,21 @@ def build_library(verbose: bool = False) -> Path:
         elif verbose and out:
             print(out.decode(errors="replace"), flush=True)
     if failed:
+        out_lib.unlink(missing_ok=True)
         msg = "\n".join(" ".join(c) + "\n" + o for c, o in failed)
         raise RuntimeError("libtbias build failed:\n" + msg)
-    tmp = LIB.with_suffix(".so.tmp")
+    tmp = out_lib.with_suffix(".so.tmp")
     link = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", str(tmp),
             *map(str, objs), "-pthread"]
     if verbose:
         print(" ".join(link), flush=True)
     r = subprocess.run(link, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     if r.returncode != 0:
+        out_lib.unlink(missing_ok=True)
         raise RuntimeError("libtbias link failed:\n" + r.stdout.decode(errors="replace"))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out_lib)
+    return out_lib
 
 
 if __name__ == "__main__":
-    print(build_library(verbose="-v" in sys.argv))
+    print(build_library(verbose="-v" in sys.argv, poison="--poison" in sys.argv))

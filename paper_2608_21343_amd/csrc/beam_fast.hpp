@@ -177,6 +177,10 @@ __global__ __launch_bounds__(kPrepThreads) void beam_prep_kernel(
     const int32_t* __restrict__ states, int32_t* __restrict__ out_tok,
     int32_t* __restrict__ out_parent, int32_t* __restrict__ out_state,
     float* __restrict__ out_step, float* __restrict__ out_cum) {
+  __shared__ float g_key[kPrepThreads / 64][64];
+  __shared__ int32_t g_tok[kPrepThreads / 64][64];
+  lds_poison(g_key, sizeof(g_key));
+  lds_poison(g_tok, sizeof(g_tok));
   const int lane = __lane_id();
   const int64_t r = (int64_t)blockIdx.x * (kPrepThreads / 64) + (threadIdx.x >> 6);
   if (r >= n_rows) return;  // uniform per wave; no barrier follows
@@ -225,8 +229,6 @@ __global__ __launch_bounds__(kPrepThreads) void beam_prep_kernel(
   // theta: the kList-th largest lane maximum; kList lanes hold a move >= theta,
   // so every listed move is >= theta. The moves >= theta (few) are gathered
   // in LDS and ranked in (key, token) order.
-  __shared__ float g_key[kPrepThreads / 64][64];
-  __shared__ int32_t g_tok[kPrepThreads / 64][64];
   const int wv = threadIdx.x >> 6;
   float lm = kNegInf;
 #pragma unroll
@@ -306,6 +308,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
   typedef BeamLds<PER, MAXK, STREAM ? MAXK : 1> Lds;
   constexpr int HOT = Lds::HOT;
   __shared__ Lds S;
+  lds_poison(&S, sizeof(S));
   const int32_t V1 = A.V1, V = V1 - 1;
   const int nt = (int)blockDim.x;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // hypothesis / slot

@@ -243,6 +243,7 @@ __global__ __launch_bounds__(kThreads) void beam_pipe_kernel(
   typedef typename Ld::T RT;
   constexpr int32_t HL = 64 * TPH;  // tokens per half row
   __shared__ PipeLds<RT, TPH> sh;
+  lds_poison(&sh, sizeof(sh));
   const int32_t V1 = A.V1, V = V1 - 1;
   const int lane = __lane_id();
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));

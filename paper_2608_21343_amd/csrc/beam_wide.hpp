@@ -68,6 +68,8 @@ __global__ __launch_bounds__(kThreads) void beam_wide_kernel(
     int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ BeamShared<MAXK> sh;
+  lds_poison(&sh, sizeof(sh));
+  lds_poison(dyn, lds_bytes(A));
   const int32_t V1 = A.V1, V = V1 - 1;
   const int tid = threadIdx.x;
   const int32_t b = blockIdx.x;

@@ -203,6 +203,21 @@ __device__ __forceinline__ double exp_nonpos(double x) {
   return tiny ? 0.0 : __builtin_ldexp(p, (int)k);
 }
 
+// Debug builds (TB_POISON_LDS): a kernel first fills its LDS with all bits
+// set (a NaN, -1, 0xffff: no table or candidate holds that pattern as data),
+// so a read of a word the kernel did not write first changes its results.
+// Every thread of the workgroup calls it (a barrier follows).
+__device__ __forceinline__ void lds_poison(void* p, size_t bytes) {
+#ifdef TB_POISON_LDS
+  uint32_t* w = static_cast<uint32_t*>(p);
+  for (size_t i = threadIdx.x; i < bytes / 4; i += blockDim.x) w[i] = 0xffffffffu;
+  __syncthreads();
+#else
+  (void)p;
+  (void)bytes;
+#endif
+}
+
 // The state written for a stream decoded without biasing (mode != 1 below):
 // -1 for model -1; a carried TB_STATE_TIMEOUT stays TB_STATE_TIMEOUT (the
 // stream's earlier outputs are unreliable until it is reset); any other

@@ -66,6 +66,7 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
     int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
     float* __restrict__ out_score) {
   extern __shared__ int32_t smem[];
+  lds_poison(smem, (size_t)6 * (A.V1 - 1) + 4);  // the launch's dynamic LDS
   const int32_t V1 = A.V1, V = V1 - 1;
   int32_t* odst = smem;
   uint16_t* stamp = reinterpret_cast<uint16_t*>(smem + V);

@@ -1252,6 +1252,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_seg_kernel(
   constexpr int NT = Shape<PER>::NT;
   constexpr int HOT = SegLds<PER>::HOT;
   __shared__ SegLds<PER> S;
+  lds_poison(&S, sizeof(S));
   const int32_t V1 = A.V1, V = V1 - 1;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = __lane_id();
@@ -1409,6 +1410,7 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
     int32_t* __restrict__ states, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
     float* __restrict__ out_score) {
   __shared__ FixLds<PER> S;
+  lds_poison(&S, sizeof(S));
   const int32_t V1 = A.V1, V = V1 - 1;
   const int lane = __lane_id();
   const int32_t b = blockIdx.x;
@@ -1511,6 +1513,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   constexpr int NT = Shape<PER>::NT;
   constexpr int HOT = SegLds<PER>::HOT;
   __shared__ SegLds<PER> S;
+  lds_poison(&S, sizeof(S));
   const int32_t V1 = A.V1, V = V1 - 1;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = __lane_id();

@@ -119,6 +119,8 @@ __global__ __launch_bounds__(kThreads) void greedy_wide_kernel(
     float* __restrict__ out_score) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ Shared sh;
+  lds_poison(&sh, sizeof(sh));
+  lds_poison(dyn, wide::lds_bytes(A));
   const int32_t V1 = A.V1;
   const int32_t b = blockIdx.x % B;
   const int32_t g = blockIdx.x / B;
@@ -170,6 +172,8 @@ __global__ __launch_bounds__(kThreads) void greedy_wide_fix_kernel(
     float* __restrict__ out_score) {
   extern __shared__ __align__(16) unsigned char dyn[];
   __shared__ Shared sh;
+  lds_poison(&sh, sizeof(sh));
+  lds_poison(dyn, wide::lds_bytes(A));
   const int32_t V1 = A.V1;
   const int32_t b = blockIdx.x;
   const typename Ld::T* col = logits + (int64_t)b * stride;

@@ -44,7 +44,7 @@ struct Ctx {
 };
 
 // Bytes of dynamic LDS a workgroup needs: the tag table and the override list.
-inline size_t lds_bytes(const ArenaView& A) {
+__host__ __device__ inline size_t lds_bytes(const ArenaView& A) {
   const int32_t cap = A.max_override > 0 ? A.max_override : 1;
   return 4 * (size_t)(A.V1 - 1) + 8 * (size_t)cap;
 }
