@@ -298,7 +298,7 @@ int tb_boost_step_greedy(const tb_arena* a, const void* logits, int32_t dtype, i
  *
  * T = 0 is a no-op that touches no buffer (they may be NULL).
  */
-enum { TB_MAX_BEAM = 16 };
+enum { TB_MAX_BEAM = 32 }; /* the paper's beam search uses 32 hypotheses */
 int tb_boost_step_beam(const tb_arena* a, const void* logits, int32_t dtype, int32_t T,
                        int32_t B, int32_t K, int64_t row_stride, const int32_t* model_ids,
                        int32_t* states, float* scores, int32_t* out_tok, int32_t* out_parent,

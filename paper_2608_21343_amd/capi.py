@@ -21,7 +21,7 @@ TB_OK, TB_EINVAL, TB_ENOMEM, TB_EHIP, TB_ERANGE = 0, -1, -2, -3, -4
 TB_F32, TB_BF16 = 0, 1
 TB_COMMIT, TB_PURE_POTENTIAL = 0, 1
 TB_STATE_NONE, TB_STATE_INVALID, TB_STATE_TIMEOUT = -1, -2, -3
-TB_MAX_BEAM = 16
+TB_MAX_BEAM = 32
 # tb_debug_select_kernels choices
 GREEDY_AUTO, GREEDY_REF = 0, 1
 BEAM_AUTO, BEAM_REF, BEAM_NO_PIPE = 0, 1, 2

@@ -410,8 +410,11 @@ void launch_k(const ArenaView& A, const void* logits, int32_t T, int32_t B, int3
   else if (K <= 8)
     launch_t<Ld, 8, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
                             out_parent, out_state, out_step, out_cum, st, sa);
-  else
+  else if (K <= 16)
     launch_t<Ld, 16, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
+                             out_parent, out_state, out_step, out_cum, st, sa);
+  else
+    launch_t<Ld, 32, STREAM>(A, logits, T, B, K, stride, model_ids, states, scores, out_tok,
                              out_parent, out_state, out_step, out_cum, st, sa);
 }
 

@@ -113,7 +113,8 @@ def test_stream_beam_matches_the_oracle(K, V, dtype):
     _run(cfg, mids, chunk=16)
 
 
-@pytest.mark.parametrize("K,V,dtype", [(4, 3000, "f32"), (12, 500, "f32"), (3, 5000, "bf16")])
+@pytest.mark.parametrize("K,V,dtype", [(4, 3000, "f32"), (12, 500, "f32"), (3, 5000, "bf16"),
+                                       (32, 300, "f32")])
 def test_stream_beam_on_the_reference_kernel(K, V, dtype):
     """Rows wider than 2048 and beams wider than 8: the reference kernel's
     streaming stage."""
@@ -209,15 +210,16 @@ def test_argument_errors():
         capi.tb_boost_step_beam_stream(dec.arena, rows_dev, c.mids, c.states, c.scores,
                                        c.hyps[:3], c.tree, c.tree_len, *outs(4))
     # K beyond TB_MAX_BEAM
-    cfg17 = _cfg(6, B=2, K=17, V=100, T=4)
-    rows17 = to_device_logits(W.logits(cfg17))
-    c17 = dec.start_beam_stream(mids, 16, 16)
-    hyps17 = torch.zeros((2 * 17, 3), dtype=torch.int64, device="cuda")
+    Kx = capi.TB_MAX_BEAM + 1
+    cfgx = _cfg(6, B=2, K=Kx, V=100, T=4)
+    rowsx = to_device_logits(W.logits(cfgx))
+    cx = dec.start_beam_stream(mids, 4, 16)
     with pytest.raises(capi.TbError) as e:
-        capi.tb_boost_step_beam_stream(dec.arena, rows17, c17.mids,
-                                       torch.zeros(34, dtype=torch.int32, device="cuda"),
-                                       torch.zeros(34, dtype=torch.float32, device="cuda"),
-                                       hyps17, c17.tree, c17.tree_len, *outs(17))
+        capi.tb_boost_step_beam_stream(dec.arena, rowsx, cx.mids,
+                                       torch.zeros(2 * Kx, dtype=torch.int32, device="cuda"),
+                                       torch.zeros(2 * Kx, dtype=torch.float32, device="cuda"),
+                                       torch.zeros((2 * Kx, 3), dtype=torch.int64, device="cuda"),
+                                       cx.tree, cx.tree_len, *outs(Kx))
     assert e.value.code == capi.TB_EINVAL
 
 
