@@ -132,6 +132,62 @@ def cpu_baseline(cfg):
     }
 
 
+def cache_levels(capi, W, cfg, cm, reg, spare, ws) -> dict:
+    """Host wall time to give a stream a new model at each level of the model
+    cache: compile its list, load it from a file, or take it from the
+    host-memory cache, then copy it into the registry arena (each model is
+    removed again afterwards); a model registered before the session only
+    needs the stream's reset to its id. Mean over the spare lists."""
+    import shutil
+    import tempfile
+    import torch
+    cache = capi.GraphsCache(cm)
+    tmp = tempfile.mkdtemp(prefix="tbias_models_")
+    csrs = [W.phrase_csr([lst]) for lst in spare]  # the caller's lists, as the C-ABI takes them
+    try:
+        paths = []
+        for j, csr in enumerate(csrs):
+            g, _ = cache.compile(*csr, cfg.token_w, cfg.end_bonus)
+            paths.append(os.path.join(tmp, f"model{j}.tbg"))
+            capi.tb_graphs_save(g, paths[-1])
+
+        def add_remove(make) -> float:
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            new = reg.register(make())
+            torch.cuda.synchronize()
+            dt = time.perf_counter() - t
+            reg.unregister(new[0], workspace=ws)
+            torch.cuda.synchronize()
+            return dt * 1e3
+
+        out = {
+            "compile": float(np.mean([add_remove(lambda: capi.tb_compile_graphs(
+                *csr, cfg.token_w, cfg.end_bonus, cm)) for csr in csrs])),
+            "disk": float(np.mean([add_remove(lambda: capi.tb_graphs_load(p)) for p in paths])),
+            "memory": float(np.mean([add_remove(lambda: cache.compile(
+                *csr, cfg.token_w, cfg.end_bonus)[0]) for csr in csrs])),
+        }
+        hits = cache.stats()["hits"]
+        mids = torch.zeros(cfg.B, dtype=torch.int32, device="cuda")
+        states = torch.zeros(cfg.B, dtype=torch.int32, device="cuda")
+        walls = []
+        for b in range(len(spare)):
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            capi.tb_reset_stream(reg.arena, b, b, 1, mids, states)
+            torch.cuda.synchronize()
+            walls.append((time.perf_counter() - t) * 1e3)
+        out["decoder"] = float(np.mean(walls))
+        out["memory_hits"] = hits
+        out["what"] = ("host wall ms per model: compile + copy into the arena; file load + copy; "
+                       "host-memory cache hit + copy; registered before the session (the "
+                       "stream's reset to its id)")
+        return out
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+
+
 def lifecycle(args) -> int:
     """Model lifecycle next to the streaming step: the 128 streaming models in
     a registry arena (room for 8 more), then the cost of adding one compiled
@@ -171,6 +227,13 @@ def lifecycle(args) -> int:
 
     add_ms, add_wall, rm_ms, rm_wall, moved = [], [], [], [], []
     ws = torch.empty(max(reg.workspace_bytes(i) for i in ids), dtype=torch.uint8, device="cuda")
+    # untimed: the first launch of a kernel loads its code object (milliseconds)
+    warm = reg.register(spare_g[0])
+    reg.unregister(ids[len(ids) // 2], workspace=ws)
+    reg.unregister(warm[0], workspace=ws)
+    ids = ids[:len(ids) // 2] + ids[len(ids) // 2 + 1:] + reg.register(
+        capi.tb_compile_graphs(*W.phrase_csr([lists[len(ids) // 2]]), cfg.token_w,
+                               cfg.end_bonus, cm))
     for g in spare_g:
         new = []
         d, w = timed(lambda: new.extend(reg.register(g)))
@@ -182,6 +245,7 @@ def lifecycle(args) -> int:
         rm_ms.append(d)
         rm_wall.append(w)
         ids = [i for i in ids if i != victim] + new
+    levels = cache_levels(capi, W, cfg, cm, reg, spare, ws)
     # the streaming workload through the registry arena (every stream on a live model)
     dec = BoostDecoder.for_arena(reg.arena)
     dt = torch.float32
@@ -237,6 +301,8 @@ def lifecycle(args) -> int:
                     "synchronised) and one model removed from the middle of 128 (the later "
                     "records moved left through a workspace, table rebased on the device), "
                     "device time between events and host wall time, mean of 8 each",
+            "add_one_model_by_cache_level_ms": levels,
+            "per_16_step_call_ms": step_s * 1e3 / n_launch,
         },
     }
     print(json.dumps(result), flush=True)

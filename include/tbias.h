@@ -41,7 +41,8 @@ enum {
   TB_EINVAL = -1, /* bad argument (null/misaligned pointer, bad size or flag) */
   TB_ENOMEM = -2, /* host allocation failed, or a caller buffer is too small */
   TB_EHIP = -3,   /* a HIP runtime call or kernel launch failed */
-  TB_ERANGE = -4  /* data out of range (token >= V, blank in a phrase, ...) */
+  TB_ERANGE = -4, /* data out of range (token >= V, blank in a phrase, ...) */
+  TB_EIO = -5     /* a file could not be opened, read or written */
 };
 
 enum { TB_F32 = 0, TB_BF16 = 1 };                     /* logit element type */
@@ -241,6 +242,61 @@ void tb_graphs_free(tb_graphs* g);
  * or TB_ERANGE.
  */
 int tb_validate_image(const void* host_image, const tb_arena_layout* layout);
+
+/*
+ * Model caches (Sec. II-B, lifecycle paragraph: precompiled models kept on
+ * disk and in host memory, copied into the merged GPU model on demand; the
+ * third level, models registered before a session, is tb_register_models).
+ *
+ * tb_graphs_cache_create — a host-memory cache of compiled models for one
+ *   class map (copied). Entries are per model: one phrase list with its
+ *   token_w, end_bonus, scale and semantics, compared exactly. When the held
+ *   models would exceed capacity_bytes the least recently used are dropped;
+ *   a model larger than capacity_bytes is compiled but not kept. Errors:
+ *   TB_EINVAL (null pointer, capacity_bytes < 0, v_plus_blank < 2),
+ *   TB_ERANGE (a class map tb_compile_graphs rejects), TB_ENOMEM.
+ *
+ * tb_graphs_cache_compile — tb_compile_graphs over the cache's class map: a
+ *   model found in the cache is taken from it, the others are compiled and
+ *   added. The result equals tb_compile_graphs' byte for byte. hits (host
+ *   int32*, or NULL) receives the number of models taken from the cache.
+ *   Calls on one cache may run concurrently (lookups and insertions are
+ *   locked; compiles run outside the lock). Errors as tb_compile_graphs;
+ *   TB_EINVAL for a null cache.
+ *
+ * tb_graphs_cache_stats — host int64[5]: hits, misses, models held, bytes
+ *   held (estimated), models dropped.
+ */
+typedef struct tb_graphs_cache tb_graphs_cache;
+int tb_graphs_cache_create(const int32_t* class_map, int32_t v_plus_blank,
+                           int64_t capacity_bytes, tb_graphs_cache** out);
+int tb_graphs_cache_compile(tb_graphs_cache* c, int32_t n_models,
+                            const int64_t* model_phrase_ptr, const int64_t* phrase_tok_ptr,
+                            const int32_t* phrase_tokens, const float* token_w,
+                            const float* end_bonus, const float* scale, int32_t semantics,
+                            int32_t n_threads, int32_t* hits, tb_graphs** out);
+int tb_graphs_cache_stats(tb_graphs_cache* c, int64_t* stats);
+void tb_graphs_cache_free(tb_graphs_cache* c);
+
+/*
+ * tb_graphs_save — write compiled graphs (of tb_compile_graphs,
+ *   tb_graphs_cache_compile, tb_compile_variative or tb_graphs_load) to the
+ *   file at path, in host byte order: a header (format tag, version, the
+ *   layout, the image size and its 64-bit FNV-1a checksum), then the arena
+ *   image. The file is written under a temporary name and renamed, so a
+ *   reader never sees a partial file. Errors: TB_EINVAL (null argument),
+ *   TB_EIO (the file cannot be written).
+ *
+ * tb_graphs_load — read such a file into new graphs (free with
+ *   tb_graphs_free). The layout must be the one its counts imply, the
+ *   checksum must match, the image must pass tb_validate_image, and the
+ *   layout's max_children and max_override must equal the image's. Errors:
+ *   TB_EINVAL (null argument), TB_EIO (missing or unreadable file),
+ *   TB_ERANGE (not a graphs file, another version, wrong size, checksum or
+ *   content), TB_ENOMEM.
+ */
+int tb_graphs_save(const tb_graphs* g, const char* path);
+int tb_graphs_load(const char* path, tb_graphs** out);
 
 /*
  * tb_init_states — start B streams (Sec. II-B: each stream carries a model id

@@ -23,7 +23,7 @@ HIP_SOURCES = ["capi.hip", "greedy.hip", "greedy_seg.hip",
                "beam_pipe_f32.hip", "beam_pipe_bf16.hip", "beam_fast_1_8.hip", "beam_fast_9_16.hip",
                "beam_fast_17_24.hip", "beam_fast_25_32.hip", "beam_stream_1_8.hip",
                "beam_stream_9_16.hip", "beam_stream_17_24.hip", "beam_stream_25_32.hip", "state.hip", "registry.hip"]
-CXX_SOURCES = ["compiler.cpp", "variative.cpp", "errors.cpp"]
+CXX_SOURCES = ["compiler.cpp", "variative.cpp", "cache.cpp", "errors.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -9,6 +9,7 @@ not built, importing this module raises: there is no fallback path.
 from __future__ import annotations
 
 import ctypes as C
+import os
 from pathlib import Path
 from typing import Optional, Sequence, Tuple
 
@@ -17,7 +18,7 @@ import numpy as np
 _PKG = Path(__file__).resolve().parent
 LIB_PATH = _PKG / "libtbias.so"
 
-TB_OK, TB_EINVAL, TB_ENOMEM, TB_EHIP, TB_ERANGE = 0, -1, -2, -3, -4
+TB_OK, TB_EINVAL, TB_ENOMEM, TB_EHIP, TB_ERANGE, TB_EIO = 0, -1, -2, -3, -4, -5
 TB_F32, TB_BF16 = 0, 1
 TB_COMMIT, TB_PURE_POTENTIAL = 0, 1
 TB_STATE_NONE, TB_STATE_INVALID, TB_STATE_TIMEOUT = -1, -2, -3
@@ -92,6 +93,12 @@ def _load() -> C.CDLL:
         "tb_register_models": [P, P, P, P],
         "tb_unregister_model": [P, I32, P, I64, P],
         "tb_unregister_model_noalloc": [P, I32, P],
+        "tb_graphs_cache_create": [P, I32, I64, C.POINTER(C.c_void_p)],
+        "tb_graphs_cache_compile": [P, I32, P, P, P, P, P, P, I32, I32, P,
+                                    C.POINTER(C.c_void_p)],
+        "tb_graphs_cache_stats": [P, P],
+        "tb_graphs_save": [P, C.c_char_p],
+        "tb_graphs_load": [C.c_char_p, C.POINTER(C.c_void_p)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -101,6 +108,8 @@ def _load() -> C.CDLL:
     lib.tb_graphs_free.restype = None
     lib.tb_registry_free.argtypes = [P]
     lib.tb_registry_free.restype = None
+    lib.tb_graphs_cache_free.argtypes = [P]
+    lib.tb_graphs_cache_free.restype = None
     for name in ("tb_registry_used_states", "tb_unregister_workspace_bytes"):
         getattr(lib, name).restype = C.c_int64
     lib.tb_registry_used_states.argtypes = [P]
@@ -119,7 +128,9 @@ EXPORTED = ("tb_compile_graphs", "tb_graphs_layout", "tb_graphs_host_image", "tb
             "tb_registry_layout", "tb_registry_create", "tb_registry_arena", "tb_registry_model",
             "tb_registry_used_states", "tb_register_models", "tb_unregister_workspace_bytes",
             "tb_unregister_model", "tb_registry_free", "tb_unregister_model_noalloc",
-            "tb_init_beam_stream", "tb_boost_step_beam_stream", "tb_compile_variative")
+            "tb_init_beam_stream", "tb_boost_step_beam_stream", "tb_compile_variative",
+            "tb_graphs_cache_create", "tb_graphs_cache_compile", "tb_graphs_cache_stats",
+            "tb_graphs_cache_free", "tb_graphs_save", "tb_graphs_load")
 
 
 def _check(code: int) -> None:
@@ -189,9 +200,8 @@ class Graphs:
             pass
 
 
-def tb_compile_graphs(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, end_bonus,
-                      class_map, scale=None, semantics: int = TB_COMMIT,
-                      n_threads: int = 0) -> Graphs:
+def _list_args(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, end_bonus, scale):
+    """Host arrays of the phrase-list arguments (weights broadcast per model)."""
     mp = np.ascontiguousarray(model_phrase_ptr, dtype=np.int64)
     tp = np.ascontiguousarray(phrase_tok_ptr, dtype=np.int64)
     tk = np.ascontiguousarray(phrase_tokens, dtype=np.int32)
@@ -200,12 +210,71 @@ def tb_compile_graphs(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, 
     eb = np.ascontiguousarray(np.broadcast_to(np.asarray(end_bonus, np.float32), (n_models,)))
     sc = None if scale is None else np.ascontiguousarray(
         np.broadcast_to(np.asarray(scale, np.float32), (n_models,)))
+    keep = (mp, tp, tk, tw, eb, sc)  # alive for the call
+    ptrs = (n_models, _np_ptr(mp), _np_ptr(tp), _np_ptr(tk) if tk.size else None, _np_ptr(tw),
+            _np_ptr(eb), _np_ptr(sc) if sc is not None else None)
+    return keep, ptrs
+
+
+def tb_compile_graphs(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, end_bonus,
+                      class_map, scale=None, semantics: int = TB_COMMIT,
+                      n_threads: int = 0) -> Graphs:
+    keep, ptrs = _list_args(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, end_bonus,
+                            scale)
     cm = np.ascontiguousarray(class_map, dtype=np.int32)
     out = C.c_void_p()
-    _check(LIB.tb_compile_graphs(n_models, _np_ptr(mp), _np_ptr(tp),
-                                 _np_ptr(tk) if tk.size else None, _np_ptr(tw), _np_ptr(eb),
-                                 _np_ptr(sc) if sc is not None else None, _np_ptr(cm), len(cm),
-                                 semantics, n_threads, C.byref(out)))
+    _check(LIB.tb_compile_graphs(*ptrs, _np_ptr(cm), len(cm), semantics, n_threads,
+                                 C.byref(out)))
+    del keep
+    return Graphs(out.value)
+
+
+class GraphsCache:
+    """Host-memory cache of compiled models for one class map
+    (tb_graphs_cache_*). compile() returns what tb_compile_graphs would, byte
+    for byte, taking the models it has compiled before from the cache."""
+
+    def __init__(self, class_map, capacity_bytes: int = 256 << 20):
+        cm = np.ascontiguousarray(class_map, dtype=np.int32)
+        h = C.c_void_p()
+        _check(LIB.tb_graphs_cache_create(_np_ptr(cm), len(cm), int(capacity_bytes), C.byref(h)))
+        self._h = h
+
+    def compile(self, model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w, end_bonus,
+                scale=None, semantics: int = TB_COMMIT, n_threads: int = 0):
+        """(Graphs, number of models taken from the cache)."""
+        keep, ptrs = _list_args(model_phrase_ptr, phrase_tok_ptr, phrase_tokens, token_w,
+                                end_bonus, scale)
+        out, hits = C.c_void_p(), C.c_int32()
+        _check(LIB.tb_graphs_cache_compile(self._h, *ptrs, semantics, n_threads, C.byref(hits),
+                                           C.byref(out)))
+        del keep
+        return Graphs(out.value), int(hits.value)
+
+    def stats(self) -> dict:
+        st = np.zeros(5, dtype=np.int64)
+        _check(LIB.tb_graphs_cache_stats(self._h, _np_ptr(st)))
+        return dict(zip(("hits", "misses", "models", "bytes", "dropped"), (int(x) for x in st)))
+
+    def free(self) -> None:
+        if self._h:
+            LIB.tb_graphs_cache_free(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def tb_graphs_save(graphs: Graphs, path) -> None:
+    _check(LIB.tb_graphs_save(graphs._h, os.fsencode(os.fspath(path))))
+
+
+def tb_graphs_load(path) -> Graphs:
+    out = C.c_void_p()
+    _check(LIB.tb_graphs_load(os.fsencode(os.fspath(path)), C.byref(out)))
     return Graphs(out.value)
 
 

@@ -30,6 +30,8 @@
 #include <algorithm>
 #include <atomic>
 #include <cstring>
+#include <functional>
+#include <system_error>
 #include <thread>
 
 #include "internal.hpp"
@@ -282,13 +284,12 @@ void class_tables(const int32_t* class_map, int32_t V, int32_t* cp, int32_t* ct)
 
 using namespace tbias;
 
-extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_ptr,
-                                 const int64_t* phrase_tok_ptr, const int32_t* phrase_tokens,
-                                 const float* token_w, const float* end_bonus, const float* scale,
-                                 const int32_t* class_map, int32_t v_plus_blank,
-                                 int32_t semantics, int32_t n_threads, tb_graphs** out) {
-  if (!out) return fail(TB_EINVAL, "out is NULL");
-  *out = nullptr;
+namespace tbias {
+
+int check_compile_args(int32_t n_models, const int64_t* model_phrase_ptr,
+                       const int64_t* phrase_tok_ptr, const int32_t* phrase_tokens,
+                       const float* token_w, const float* end_bonus, const int32_t* class_map,
+                       int32_t v_plus_blank, int32_t semantics) {
   if (n_models < 1) return fail(TB_EINVAL, "n_models must be >= 1");
   if (!model_phrase_ptr || !phrase_tok_ptr || !token_w || !end_bonus || !class_map)
     return fail(TB_EINVAL, "NULL input array");
@@ -311,8 +312,10 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
     if (phrase_tok_ptr[p + 1] < phrase_tok_ptr[p])
       return fail(TB_EINVAL, "phrase_tok_ptr not monotone");
   if (phrase_tok_ptr[n_phr] > 0 && !phrase_tokens) return fail(TB_EINVAL, "phrase_tokens NULL");
+  return TB_OK;
+}
 
-  std::vector<ModelGraph> graphs(n_models);
+int run_models(int32_t n_models, int32_t n_threads, const std::function<int(int32_t)>& job) {
   std::vector<int> status(n_models, TB_OK);
   std::vector<std::string> errs(n_models);
   std::atomic<int32_t> next{0};
@@ -320,13 +323,13 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
   nt = std::max(1, std::min(nt, n_models));
   auto work = [&]() {
     for (;;) {
-      int32_t m = next.fetch_add(1);
+      const int32_t m = next.fetch_add(1);
       if (m >= n_models) break;
-      int64_t p0 = model_phrase_ptr[m], p1 = model_phrase_ptr[m + 1];
-      double a = scale ? (double)scale[m] : 1.0;
-      status[m] = compile_model(phrase_tokens, phrase_tok_ptr + p0, p1 - p0, class_map, V,
-                                (double)token_w[m], (double)end_bonus[m], a, semantics,
-                                &graphs[m]);
+      try {
+        status[m] = job(m);
+      } catch (const std::bad_alloc&) {
+        status[m] = fail(TB_ENOMEM, "host allocation failed while compiling");
+      }
       if (status[m] != TB_OK) errs[m] = tb_last_error();
     }
   };
@@ -338,18 +341,49 @@ extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_p
       for (int i = 0; i < nt; ++i) pool.emplace_back(work);
       for (auto& t : pool) t.join();
     }
-  } catch (const std::bad_alloc&) {
-    return fail(TB_ENOMEM, "host allocation failed while compiling");
+  } catch (const std::system_error&) {
+    return fail(TB_ENOMEM, "could not start the compile threads");
   }
   for (int32_t m = 0; m < n_models; ++m)
     if (status[m] != TB_OK)
       return fail(status[m], "model " + std::to_string(m) + ": " + errs[m]);
+  return TB_OK;
+}
+
+}  // namespace tbias
+
+extern "C" int tb_compile_graphs(int32_t n_models, const int64_t* model_phrase_ptr,
+                                 const int64_t* phrase_tok_ptr, const int32_t* phrase_tokens,
+                                 const float* token_w, const float* end_bonus, const float* scale,
+                                 const int32_t* class_map, int32_t v_plus_blank,
+                                 int32_t semantics, int32_t n_threads, tb_graphs** out) {
+  if (!out) return fail(TB_EINVAL, "out is NULL");
+  *out = nullptr;
+  const int st = check_compile_args(n_models, model_phrase_ptr, phrase_tok_ptr, phrase_tokens,
+                                    token_w, end_bonus, class_map, v_plus_blank, semantics);
+  if (st != TB_OK) return st;
+  const int32_t V = v_plus_blank - 1;
+  std::vector<ModelGraph> graphs(n_models);
+  const int rc = run_models(n_models, n_threads, [&](int32_t m) -> int {
+    const int64_t p0 = model_phrase_ptr[m], p1 = model_phrase_ptr[m + 1];
+    const double a = scale ? (double)scale[m] : 1.0;
+    return compile_model(phrase_tokens, phrase_tok_ptr + p0, p1 - p0, class_map, V,
+                         (double)token_w[m], (double)end_bonus[m], a, semantics, &graphs[m]);
+  });
+  if (rc != TB_OK) return rc;
   return assemble_image(graphs, class_map, v_plus_blank, out);
 }
 
 namespace tbias {
 
 int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_map,
+                   int32_t v_plus_blank, tb_graphs** out) {
+  std::vector<const ModelGraph*> ptrs(graphs.size());
+  for (size_t m = 0; m < graphs.size(); ++m) ptrs[m] = &graphs[m];
+  return assemble_image(ptrs, class_map, v_plus_blank, out);
+}
+
+int assemble_image(const std::vector<const ModelGraph*>& graphs, const int32_t* class_map,
                    int32_t v_plus_blank, tb_graphs** out) {
   const int32_t n_models = (int32_t)graphs.size();
   const int32_t V = v_plus_blank - 1;
@@ -358,10 +392,10 @@ int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_m
   tb_arena_layout& L = g->layout;
   std::memset(&L, 0, sizeof(L));
   int64_t N = 0;
-  for (auto& mg : graphs) {
-    N += mg.n;
-    L.max_children = std::max(L.max_children, mg.max_children);
-    L.max_depth = std::max(L.max_depth, mg.max_depth);
+  for (const ModelGraph* mg : graphs) {
+    N += mg->n;
+    L.max_children = std::max(L.max_children, mg->max_children);
+    L.max_depth = std::max(L.max_depth, mg->max_depth);
   }
   if (N > INT32_MAX) { delete g; return fail(TB_ERANGE, "more than 2^31 states in total"); }
   plan_layout(n_models, N, v_plus_blank, &L);
@@ -377,7 +411,7 @@ int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_m
   auto F32 = [&](int64_t o) { return reinterpret_cast<float*>(img + o); };
   int64_t s0 = 0;
   for (int32_t m = 0; m < n_models; ++m) {
-    const ModelGraph& mg = graphs[m];
+    const ModelGraph& mg = *graphs[m];
     I32(L.off_model_off)[m] = (int32_t)s0;
     I32(L.off_model_n)[m] = mg.n;
     std::memcpy(I32(L.off_first_child) + s0, mg.first_child.data(), 4 * (size_t)mg.n);
@@ -397,27 +431,7 @@ int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_m
   int32_t* cp = I32(L.off_cls_ptr);
   int32_t* ct = I32(L.off_cls_tok);
   class_tables(class_map, V, cp, ct);
-  // largest override set: over all states, the member tokens of the classes
-  // of the children along the state's suffix chain (root excluded), each
-  // class counted once
-  {
-    std::vector<int32_t> seen(V, -1);
-    int32_t gen = 0;
-    for (int32_t m = 0; m < n_models; ++m) {
-      const ModelGraph& mg = graphs[m];
-      for (int32_t x = 1; x < mg.n; ++x, ++gen) {
-        int32_t members = 0;
-        for (int32_t c = x; c != 0; c = mg.link[c])
-          for (int32_t j = 0; j < mg.n_child[c]; ++j) {
-            const int32_t lab = mg.label[mg.first_child[c] + j];
-            if (seen[lab] == gen) continue;
-            seen[lab] = gen;
-            members += cp[lab + 1] - cp[lab];
-          }
-        L.max_override = std::max(L.max_override, members);
-      }
-    }
-  }
+  L.max_override = image_max_override(img, L);
   // member tokens of the class on the arc into every state (see arc_mem in tbias.h)
   uint32_t* am = reinterpret_cast<uint32_t*>(img + L.off_arc_mem);
   for (int64_t y = 0; y < N; ++y) {
@@ -437,7 +451,7 @@ int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_m
   // value tables and packed state records
   for (int32_t m = 0; m < n_models; ++m) {
     const int32_t so = I32(L.off_model_off)[m];
-    state_records(graphs[m].n, I32(L.off_first_child) + so, I32(L.off_n_child) + so,
+    state_records(graphs[m]->n, I32(L.off_first_child) + so, I32(L.off_n_child) + so,
                   I32(L.off_link) + so, I32(L.off_label) + so, F32(L.off_phi) + so,
                   F32(L.off_psi) + so, cp, F32(L.off_value_tab) + 512 * (int64_t)m,
                   reinterpret_cast<uint32_t*>(img + L.off_state_rec) + 3 * (int64_t)so);
@@ -462,6 +476,40 @@ extern "C" int tb_graphs_host_image(const tb_graphs* g, void* dst, int64_t bytes
 }
 
 extern "C" void tb_graphs_free(tb_graphs* g) { delete g; }
+
+namespace tbias {
+
+int32_t image_max_override(const unsigned char* img, const tb_arena_layout& L) {
+  // over all states, the member tokens of the classes of the children along
+  // the state's suffix chain (root excluded), each class counted once
+  auto I32 = [&](int64_t o) { return reinterpret_cast<const int32_t*>(img + o); };
+  const int32_t V = L.v_plus_blank - 1;
+  const int32_t* cp = I32(L.off_cls_ptr);
+  std::vector<int64_t> seen(V, -1);
+  int64_t gen = 0;
+  int32_t best = 0;
+  for (int32_t m = 0; m < L.n_models; ++m) {
+    const int32_t so = I32(L.off_model_off)[m], n = I32(L.off_model_n)[m];
+    const int32_t* fc = I32(L.off_first_child) + so;
+    const int32_t* nc = I32(L.off_n_child) + so;
+    const int32_t* lk = I32(L.off_link) + so;
+    const int32_t* lb = I32(L.off_label) + so;
+    for (int32_t x = 1; x < n; ++x, ++gen) {
+      int32_t members = 0;
+      for (int32_t c = x; c != 0; c = lk[c])
+        for (int32_t j = 0; j < nc[c]; ++j) {
+          const int32_t lab = lb[fc[c] + j];
+          if (seen[lab] == gen) continue;
+          seen[lab] = gen;
+          members += cp[lab + 1] - cp[lab];
+        }
+      best = std::max(best, members);
+    }
+  }
+  return best;
+}
+
+}  // namespace tbias
 
 extern "C" int tb_validate_image(const void* host_image, const tb_arena_layout* Lp) {
   if (!host_image || !Lp) return fail(TB_EINVAL, "NULL argument");

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <cstdint>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -39,6 +40,23 @@ int compile_model(const int32_t* toks, const int64_t* tok_ptr, int64_t n_phrases
 // arc member records, value tables, packed state records); *out owns it.
 int assemble_image(const std::vector<ModelGraph>& graphs, const int32_t* class_map,
                    int32_t v_plus_blank, tb_graphs** out);
+int assemble_image(const std::vector<const ModelGraph*>& graphs, const int32_t* class_map,
+                   int32_t v_plus_blank, tb_graphs** out);
+
+// The argument checks of tb_compile_graphs (same codes and messages).
+int check_compile_args(int32_t n_models, const int64_t* model_phrase_ptr,
+                       const int64_t* phrase_tok_ptr, const int32_t* phrase_tokens,
+                       const float* token_w, const float* end_bonus, const int32_t* class_map,
+                       int32_t v_plus_blank, int32_t semantics);
+
+// Runs job(m) for every model m on up to n_threads host threads (<= 0:
+// hardware concurrency); the first failing model's code, with its message.
+int run_models(int32_t n_models, int32_t n_threads, const std::function<int(int32_t)>& job);
+
+// The most tokens any state of the image overrides: the members of the
+// classes of the children along its suffix chain, each class once (the
+// image's links must end at the root).
+int32_t image_max_override(const unsigned char* img, const tb_arena_layout& L);
 
 inline int64_t align256(int64_t x) { return (x + 255) & ~int64_t(255); }
 

@@ -24,6 +24,13 @@ struct tb_registry {
   int64_t used = 0;                // states in use: [0, used)
   std::vector<int32_t> off, n;     // host copy of the model table (n == 0: free id)
   std::vector<int32_t> class_map;  // the arena's class map
+  // pinned host staging of tb_register_models (grown on demand): copies from
+  // it run asynchronously, without the per-copy staging of pageable memory
+  unsigned char* stage = nullptr;
+  size_t stage_bytes = 0;
+  ~tb_registry() {
+    if (stage) (void)hipHostFree(stage);
+  }
 };
 
 namespace tbias {
@@ -281,41 +288,66 @@ extern "C" int tb_register_models(tb_registry* r, const tb_graphs* g, int32_t* i
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   unsigned char* base = dev_bytes(r);
   const int32_t V1 = L.v_plus_blank;
-  auto up = [&](int64_t dst_off, int64_t src_off, size_t bytes) -> hipError_t {
-    if (bytes == 0) return hipSuccess;
-    return hipMemcpyAsync(base + dst_off, img + src_off, bytes, hipMemcpyHostToDevice, st);
+  // the pieces to copy: (destination offset in the arena, source, bytes);
+  // every source is packed into the pinned staging buffer first
+  struct Piece {
+    int64_t dst;
+    const void* src;
+    size_t bytes;
   };
+  std::vector<Piece> pieces;
   // per-state arrays: every model of g, appended in one range
   StateArray da[8], sa[8];
   const int na = state_arrays(L, da);
   state_arrays(G, sa);
-  hipError_t e = hipSuccess;
-  for (int k = 0; k < na && e == hipSuccess; ++k)
-    e = up(da[k].off + 4 * r->used * da[k].words, sa[k].off, 4 * (size_t)G.n_states * sa[k].words);
+  for (int k = 0; k < na; ++k)
+    pieces.push_back({da[k].off + 4 * r->used * da[k].words, img + sa[k].off,
+                      4 * (size_t)G.n_states * sa[k].words});
   // per-model rows into the id slots
   const int32_t* g_off = reinterpret_cast<const int32_t*>(img + G.off_model_off);
   const int32_t* g_n = reinterpret_cast<const int32_t*>(img + G.off_model_n);
-  for (int32_t i = 0; i < G.n_models && e == hipSuccess; ++i) {
+  for (int32_t i = 0; i < G.n_models; ++i) {
     const int64_t id = take[i];
-    e = up(L.off_root_psi + 4 * id * V1, G.off_root_psi + 4 * (int64_t)i * V1, 4 * (size_t)V1);
-    if (e == hipSuccess)
-      e = up(L.off_root_dst + 4 * id * V1, G.off_root_dst + 4 * (int64_t)i * V1, 4 * (size_t)V1);
-    if (e == hipSuccess)
-      e = up(L.off_value_tab + 4 * 512 * id, G.off_value_tab + 4 * 512 * (int64_t)i, 4 * 512);
+    pieces.push_back({L.off_root_psi + 4 * id * V1, img + G.off_root_psi + 4 * (int64_t)i * V1,
+                      4 * (size_t)V1});
+    pieces.push_back({L.off_root_dst + 4 * id * V1, img + G.off_root_dst + 4 * (int64_t)i * V1,
+                      4 * (size_t)V1});
+    pieces.push_back({L.off_value_tab + 4 * 512 * id, img + G.off_value_tab + 4 * 512 * (int64_t)i,
+                      4 * 512});
   }
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
   std::vector<int32_t> off = r->off, n = r->n;
   for (int32_t i = 0; i < G.n_models; ++i) {
     off[take[i]] = (int32_t)(r->used + g_off[i]);
     n[take[i]] = g_n[i];
   }
-  e = hipMemcpyAsync(base + L.off_model_off, off.data(), 4 * (size_t)r->max_models,
-                     hipMemcpyHostToDevice, st);
-  if (e == hipSuccess)
-    e = hipMemcpyAsync(base + L.off_model_n, n.data(), 4 * (size_t)r->max_models,
-                       hipMemcpyHostToDevice, st);
-  if (e == hipSuccess) e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return hip_fail(e, "model table upload");
+  pieces.push_back({L.off_model_off, off.data(), 4 * (size_t)r->max_models});
+  pieces.push_back({L.off_model_n, n.data(), 4 * (size_t)r->max_models});
+  size_t total = 0;
+  for (const Piece& q : pieces) total += (q.bytes + 255) & ~(size_t)255;
+  hipError_t e = hipSuccess;
+  if (total > r->stage_bytes) {
+    if (r->stage) (void)hipHostFree(r->stage);
+    r->stage = nullptr;
+    r->stage_bytes = 0;
+    e = hipHostMalloc(reinterpret_cast<void**>(&r->stage), total, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      r->stage = nullptr;
+      return hip_fail(e, "hipHostMalloc of the registration staging buffer");
+    }
+    r->stage_bytes = total;
+  }
+  size_t at = 0;
+  for (const Piece& q : pieces) {
+    if (q.bytes == 0) continue;
+    std::memcpy(r->stage + at, q.src, q.bytes);
+    e = hipMemcpyAsync(base + q.dst, r->stage + at, q.bytes, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) break;
+    at += (q.bytes + 255) & ~(size_t)255;
+  }
+  // the staging buffer is reused by the next call: wait for every copy
+  const hipError_t es = hipStreamSynchronize(st);
+  if (e == hipSuccess) e = es;
+  if (e != hipSuccess) return hip_fail(e, "model upload");
   r->off.swap(off);
   r->n.swap(n);
   r->used += G.n_states;

@@ -1,16 +1,22 @@
-// Host-side driver of the graph compilers and image validator, built with
-// AddressSanitizer and UndefinedBehaviorSanitizer by tests/test_sanitize_cpu.py
-// (no GPU code is involved: compiler.cpp, variative.cpp and errors.cpp only).
+// Host-side driver of the graph compilers, the image validator and the model
+// caches, built with AddressSanitizer and UndefinedBehaviorSanitizer by
+// tests/test_sanitize_cpu.py (no GPU code is involved: compiler.cpp,
+// variative.cpp, cache.cpp and errors.cpp only).
 //
 // It compiles random phrase lists (empty lists, duplicates, nested and long
 // phrases, case classes, several reading flags and thread counts), checks
 // that every compiled image validates, corrupts images byte by byte and
 // checks that validation rejects or accepts them without any memory error,
-// and drives every documented argument error of tb_compile_graphs.
+// and drives every documented argument error of tb_compile_graphs. The
+// host-memory cache is driven with overlapping random lists under small
+// budgets, every result compared with a fresh compile; saved files are
+// loaded back and damaged (header fields, image bytes with and without a
+// matching checksum) to check that loading refuses them cleanly.
 #include <cstdint>
 #include <cstdio>
 #include <cstring>
 #include <random>
+#include <string>
 #include <vector>
 
 #include "../../include/tbias.h"
@@ -180,6 +186,151 @@ void random_variative(std::mt19937& rng) {
   }
 }
 
+std::vector<unsigned char> image_of(const tb_graphs* g, tb_arena_layout* lay) {
+  tb_graphs_layout(g, lay);
+  std::vector<unsigned char> img(lay->total_bytes);
+  tb_graphs_host_image(g, img.data(), lay->total_bytes);
+  return img;
+}
+
+// Overlapping random lists through one cache (budget from none to ample),
+// every result equal to a fresh compile.
+void random_cache(std::mt19937& rng) {
+  const int32_t V = 40 + (int32_t)(rng() % 200);
+  const auto cm = class_map(V, 1 + (int32_t)(rng() % (V / 3)));
+  std::uniform_int_distribution<int32_t> tokd(0, V - 1);
+  std::vector<std::vector<std::vector<int32_t>>> pool(8);
+  for (auto& lst : pool) {
+    const int n = (int)(rng() % 12);
+    for (int i = 0; i < n; ++i) {
+      std::vector<int32_t> p(1 + rng() % 6);
+      for (auto& t : p) t = tokd(rng);
+      lst.push_back(p);
+    }
+  }
+  const int64_t caps[] = {0, 2000, 20000, 1 << 24};
+  tb_graphs_cache* c = nullptr;
+  expect(tb_graphs_cache_create(cm.data(), (int32_t)cm.size(), caps[rng() % 4], &c) == TB_OK,
+         "cache create");
+  if (!c) return;
+  for (int round = 0; round < 6; ++round) {
+    Lists L;
+    const int M = 1 + (int)(rng() % 5);
+    for (int m = 0; m < M; ++m) L.add_model(pool[rng() % pool.size()]);
+    const int32_t sem = (int32_t)(rng() & 1), threads = 1 + (int32_t)(rng() % 4);
+    std::vector<float> w(M, 1.0f), be(M, 2.0f), sc(M, 1.5f);
+    const float* scp = (rng() & 1) ? sc.data() : nullptr;
+    tb_graphs* a = nullptr;
+    tb_graphs* b = nullptr;
+    int32_t hits = -1;
+    const int ra = tb_graphs_cache_compile(c, M, L.mp.data(), L.tp.data(),
+                                           L.tok.empty() ? nullptr : L.tok.data(), w.data(),
+                                           be.data(), scp, sem, threads, &hits, &a);
+    const int rb = tb_compile_graphs(M, L.mp.data(), L.tp.data(),
+                                     L.tok.empty() ? nullptr : L.tok.data(), w.data(), be.data(),
+                                     scp, cm.data(), (int32_t)cm.size(), sem, threads, &b);
+    expect(ra == TB_OK && rb == TB_OK && hits >= 0 && hits <= M, "cached and fresh compile");
+    if (a && b) {
+      tb_arena_layout la, lb;
+      const auto ia = image_of(a, &la), ib = image_of(b, &lb);
+      expect(std::memcmp(&la, &lb, sizeof la) == 0 && ia == ib, "cached compile equals fresh");
+    }
+    tb_graphs_free(a);
+    tb_graphs_free(b);
+  }
+  int64_t st[5];
+  expect(tb_graphs_cache_stats(c, st) == TB_OK && st[0] + st[1] > 0, "cache stats");
+  expect(tb_graphs_cache_compile(nullptr, 1, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                 nullptr, 0, 1, nullptr, nullptr) == TB_EINVAL, "NULL cache");
+  tb_graphs_cache_free(c);
+}
+
+uint64_t fnv1a64(const unsigned char* p, size_t n) {
+  uint64_t h = 0xcbf29ce484222325ull;
+  for (size_t i = 0; i < n; ++i) h = (h ^ p[i]) * 0x100000001b3ull;
+  return h;
+}
+
+bool write_file(const std::string& path, const std::vector<unsigned char>& bytes) {
+  FILE* f = std::fopen(path.c_str(), "wb");
+  if (!f) return false;
+  const bool ok = bytes.empty() || std::fwrite(bytes.data(), bytes.size(), 1, f) == 1;
+  return std::fclose(f) == 0 && ok;
+}
+
+std::vector<unsigned char> read_file(const std::string& path) {
+  std::vector<unsigned char> out;
+  FILE* f = std::fopen(path.c_str(), "rb");
+  if (!f) return out;
+  unsigned char buf[65536];
+  size_t n;
+  while ((n = std::fread(buf, 1, sizeof buf, f)) > 0) out.insert(out.end(), buf, buf + n);
+  std::fclose(f);
+  return out;
+}
+
+// Save, load back, then load damaged copies: every load returns a status
+// and never touches memory out of bounds.
+void files(std::mt19937& rng, const std::string& dir) {
+  const int32_t V = 60;
+  const auto cm = class_map(V, 12);
+  Lists L;
+  L.add_model({{1, 2, 3}, {4, 5}, {1, 2, 9}});
+  L.add_model({});
+  L.add_model({{7}, {7, 8, 9, 10}, {8, 9}});
+  int rc = 0;
+  tb_graphs* g = compile(L, cm, 0, 2, &rc);
+  expect(rc == TB_OK && g, "compile for files");
+  if (!g) return;
+  const std::string path = dir + "/driver.tbg";
+  expect(tb_graphs_save(g, path.c_str()) == TB_OK, "save");
+  tb_graphs* back = nullptr;
+  expect(tb_graphs_load(path.c_str(), &back) == TB_OK && back, "load");
+  tb_arena_layout lg, lb;
+  if (back) {
+    const auto ig = image_of(g, &lg), ib = image_of(back, &lb);
+    expect(std::memcmp(&lg, &lb, sizeof lg) == 0 && ig == ib, "load equals save");
+    tb_graphs_free(back);
+  }
+  const auto raw = read_file(path);
+  const size_t head = 32 + sizeof(tb_arena_layout);
+  expect(raw.size() == head + (size_t)lg.total_bytes, "file size");
+  const std::string bad = dir + "/bad.tbg";
+  std::uniform_int_distribution<size_t> anyb(0, raw.size() - 1), headb(0, head - 1);
+  for (int k = 0; k < 200; ++k) {
+    auto d = raw;
+    const int kind = k % 4;
+    if (kind == 0) {  // a header byte
+      d[headb(rng)] ^= (unsigned char)(1 + rng() % 255);
+    } else if (kind == 1) {  // an image byte, checksum left stale
+      d[anyb(rng)] ^= (unsigned char)(1 + rng() % 255);
+    } else if (kind == 2) {  // an image word, checksum updated: validation decides
+      const size_t i = head + 4 * (rng() % ((raw.size() - head) / 4));
+      const uint32_t vals[] = {0xffffffffu, 0x7fffffffu, 0x80000000u, 0u, (uint32_t)rng()};
+      std::memcpy(d.data() + i, &vals[rng() % 5], 4);
+      const uint64_t h = fnv1a64(d.data() + head, d.size() - head);
+      std::memcpy(d.data() + 24, &h, 8);
+    } else {  // truncated or extended
+      d.resize((rng() & 1) ? rng() % raw.size() : raw.size() + 1 + rng() % 64);
+    }
+    expect(write_file(bad, d), "write damaged file");
+    tb_graphs* x = nullptr;
+    const int r = tb_graphs_load(bad.c_str(), &x);
+    expect(r == TB_OK || r == TB_ERANGE || r == TB_EIO || r == TB_ENOMEM,
+           "damaged file gives a status");
+    expect((r == TB_OK) == (x != nullptr), "graphs only on success");
+    tb_graphs_free(x);
+  }
+  tb_graphs* x = nullptr;
+  expect(tb_graphs_load((dir + "/missing.tbg").c_str(), &x) == TB_EIO && !x, "missing file");
+  expect(tb_graphs_save(g, (dir + "/no/such/dir.tbg").c_str()) == TB_EIO, "unwritable path");
+  expect(tb_graphs_save(nullptr, path.c_str()) == TB_EINVAL, "NULL graphs");
+  expect(tb_graphs_load(nullptr, &x) == TB_EINVAL, "NULL path");
+  std::remove(path.c_str());
+  std::remove(bad.c_str());
+  tb_graphs_free(g);
+}
+
 void argument_errors() {
   const int32_t V = 50;
   const auto cm = class_map(V, 10);
@@ -232,10 +383,12 @@ void argument_errors() {
 
 }  // namespace
 
-int main() {
+int main(int argc, char** argv) {
   std::mt19937 rng(12345);
   for (int i = 0; i < 60; ++i) random_models(rng);
   for (int i = 0; i < 60; ++i) random_variative(rng);
+  for (int i = 0; i < 30; ++i) random_cache(rng);
+  files(rng, argc > 1 ? argv[1] : ".");
   argument_errors();
   if (g_fail) {
     std::fprintf(stderr, "%d failures\n", g_fail);

@@ -201,3 +201,40 @@ def test_beam_through_the_registry_after_compaction():
     ref = oracle.beam_decode(graphs, mids, rk, st0, S0)
     from tests.gpu_cases import compare_beam
     compare_beam(gpu, ref, range(len(mids)), 1e-5)
+
+
+def test_models_from_the_host_cache_and_from_files(tmp_path):
+    """The paper's cache levels feeding the registry: models taken from the
+    host-memory cache and loaded from files give the same arena records and
+    decodes as freshly compiled ones."""
+    from paper_2608_21343_amd.decoder import to_device_logits
+    cfg, lists, cm = _setup(seed=4)
+    reg = capi.Registry(max_models=6, max_states=20000, class_map=cm)
+    model = Model(reg, cm)
+    cache = capi.GraphsCache(cm)
+    rows = W.logits(cfg, 0, 48, streams=range(cfg.B))[:, :, 0, :]
+    rows_dev = to_device_logits(rows)
+
+    def add(graphs, idx):
+        ids = reg.register(graphs)
+        for i, j in zip(idx, ids):
+            model.live[j] = i
+        return ids
+
+    g, hits = cache.compile(*W.phrase_csr([lists[0], lists[1]]), 1.0, 2.0)
+    assert hits == 0
+    add(g, [0, 1])
+    path = tmp_path / "list2.tbg"
+    capi.tb_graphs_save(_compile([lists[2]], cm), path)
+    add(capi.tb_graphs_load(path), [2])
+    say("[lifecycle] lists 0, 1 from the cache, 2 from a file")
+    _check_records(model, lists)
+    _decode(model, lists, rows_dev, rows)
+    victim = [m for m, li in model.live.items() if li == 0][0]
+    model.unregister(victim)
+    g, hits = cache.compile(*W.phrase_csr([lists[0], lists[4]]), 1.0, 2.0)
+    assert hits == 1
+    add(g, [0, 4])
+    say("[lifecycle] list 0 again from the cache after its removal")
+    _check_records(model, lists)
+    _decode(model, lists, rows_dev, rows)
