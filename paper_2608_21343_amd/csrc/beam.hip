@@ -14,6 +14,7 @@
 #include "beam_pipe.hpp"
 #include "beam_wide.hpp"
 #include "device.hpp"
+#include "ref_table.hpp"
 #include "launch.hpp"
 
 namespace tbias {
@@ -90,10 +91,11 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
     int32_t* __restrict__ out_state, float* __restrict__ out_step, float* __restrict__ out_cum,
     beamk::StreamArgs sa) {
   extern __shared__ int32_t smem[];
-  lds_poison(smem, (size_t)6 * (A.V1 - 1) + 4);  // the launch's dynamic LDS
+  lds_poison(smem, ref_table_bytes(A.V1 - 1));  // the launch's dynamic LDS
   const int32_t V1 = A.V1, V = V1 - 1;
   int32_t* odst = smem;
-  uint16_t* stamp = reinterpret_cast<uint16_t*>(smem + V);
+  uint32_t* mark = reinterpret_cast<uint32_t*>(smem + V);
+  const int32_t n_mark = (V + 31) >> 5;
   __shared__ float redf[kWaves];
   __shared__ int32_t redi[kWaves];
   __shared__ double redd[kWaves];
@@ -141,10 +143,7 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
     const int32_t l = sa.tree_len[b];
     tlen = l < 0 ? 0 : (l > sa.cap ? sa.cap : l);
   }
-  for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
-  __syncthreads();
   if (mode == 1 && sh_bad) mode = -1;
-  uint32_t tag = 0;
   const float* rpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
   const int32_t* rdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
 
@@ -221,18 +220,15 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
       float phi_s = 0.f;
       if (mode == 1) {
         phi_s = A.phi[off + s];
-        if (++tag == 65536u) {
-          for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
-          __syncthreads();
-          tag = 1;
-        }
+        for (int32_t i = tid; i < n_mark; i += kThreads) mark[i] = 0u;
+        __syncthreads();
         for (int32_t x = s; x != 0; x = A.link[off + x]) {
           const int32_t fc = A.first_child[off + x], nc = A.n_child[off + x];
           for (int32_t j = tid; j < nc; j += kThreads) {
             const int32_t y = fc + j;
             const int32_t c = A.label[off + y];
-            if (stamp[c] != tag) {
-              stamp[c] = (uint16_t)tag;
+            if (!ref_marked(mark, c)) {  // children of one state: distinct classes
+              atomicOr(&mark[c >> 5], 1u << (c & 31));
               odst[c] = y;
             }
           }
@@ -248,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
             p = phi_s;
           } else {
             const int32_t c = A.class_map[v];
-            p = (c >= 0 && stamp[c] == tag) ? A.psi[off + odst[c]] : rpsi[v];
+            p = (c >= 0 && ref_marked(mark, c)) ? A.psi[off + odst[c]] : rpsi[v];
           }
         }
         const float key = z + p;
@@ -390,7 +386,8 @@ void launch_t(const ArenaView& A, const void* logits, int32_t T, int32_t B, int3
               int64_t stride, const int32_t* model_ids, int32_t* states, float* scores,
               int32_t* out_tok, int32_t* out_parent, int32_t* out_state, float* out_step,
               float* out_cum, hipStream_t st, beamk::StreamArgs sa) {
-  const size_t lds = (size_t)6 * (A.V1 - 1) + 4;
+  const size_t lds = ref_table_bytes(A.V1 - 1);
+  allow_dynamic_lds(&beam_ref_kernel<Ld, MAXK, STREAM>, lds);
   hipLaunchKernelGGL((beam_ref_kernel<Ld, MAXK, STREAM>), dim3(B), dim3(kThreads), lds, st, A,
                      static_cast<const typename Ld::T*>(logits), T, B, K, stride, model_ids,
                      states, scores, out_tok, out_parent, out_state, out_step, out_cum, sa);

@@ -7,12 +7,14 @@
 //      override the root move of their class, the deepest state winning;
 //   3. forms key[v] = z[v] + psi[delta(s, class v)] (blank: z[V] + phi[s]),
 //      takes the lowest-index maximum and advances the state.
-// The override table lives in LDS, indexed by class: a 16-bit tag per class
-// marks the entries written in the current step (cleared once every 65535
-// steps) next to the overriding target state.
+// The override table lives in LDS, indexed by class: the overriding target
+// state of every class, and one bit per class marking the entries written for
+// the current state (cleared every step), 4 B + 1 bit per class, so any V up
+// to the 32767 tokens the boundary accepts fits.
 #include <climits>
 
 #include "device.hpp"
+#include "ref_table.hpp"
 #include "launch.hpp"
 
 namespace tbias {
@@ -66,10 +68,11 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
     int32_t* __restrict__ out_tok, int32_t* __restrict__ out_state,
     float* __restrict__ out_score) {
   extern __shared__ int32_t smem[];
-  lds_poison(smem, (size_t)6 * (A.V1 - 1) + 4);  // the launch's dynamic LDS
+  lds_poison(smem, ref_table_bytes(A.V1 - 1));  // the launch's dynamic LDS
   const int32_t V1 = A.V1, V = V1 - 1;
   int32_t* odst = smem;
-  uint16_t* stamp = reinterpret_cast<uint16_t*>(smem + V);
+  uint32_t* mark = reinterpret_cast<uint32_t*>(smem + V);
+  const int32_t n_mark = (V + 31) >> 5;
   __shared__ float redf[kWaves];
   __shared__ int32_t redi[kWaves];
   __shared__ int32_t s_next;
@@ -81,9 +84,6 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
   int32_t off = 0, n = 0;
   const int mode = resolve_stream(A, m, s, off, n);  // 1 biased, 0 none, -1 invalid
   const int32_t fixed = unbiased_state(mode, s == TB_STATE_TIMEOUT);
-  for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
-  __syncthreads();
-  uint32_t tag = 0;
   const float* rpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
   const int32_t* rdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;
 
@@ -100,18 +100,15 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
     float phi_s = 0.f;
     if (mode == 1) {
       phi_s = A.phi[off + s];
-      if (++tag == 65536u) {  // uniform: clear the tags and restart
-        for (int32_t c = tid; c < V; c += kThreads) stamp[c] = 0;
-        __syncthreads();
-        tag = 1;
-      }
+      for (int32_t i = tid; i < n_mark; i += kThreads) mark[i] = 0u;
+      __syncthreads();
       for (int32_t x = s; x != 0; x = A.link[off + x]) {
         const int32_t fc = A.first_child[off + x], nc = A.n_child[off + x];
         for (int32_t j = tid; j < nc; j += kThreads) {
           const int32_t y = fc + j;
           const int32_t c = A.label[off + y];
-          if (stamp[c] != tag) {
-            stamp[c] = (uint16_t)tag;
+          if (!ref_marked(mark, c)) {  // children of one state: distinct classes
+            atomicOr(&mark[c >> 5], 1u << (c & 31));
             odst[c] = y;
           }
         }
@@ -129,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
           p = phi_s;
         } else {
           const int32_t c = A.class_map[v];
-          p = (c >= 0 && stamp[c] == tag) ? A.psi[off + odst[c]] : rpsi[v];
+          p = (c >= 0 && ref_marked(mark, c)) ? A.psi[off + odst[c]] : rpsi[v];
         }
       }
       const float key = z + p;
@@ -146,7 +143,7 @@ __global__ __launch_bounds__(kThreads) void greedy_ref_kernel(
           ns = s;
         } else {
           const int32_t c = A.class_map[v];
-          ns = (c >= 0 && stamp[c] == tag) ? odst[c] : rdst[v];
+          ns = (c >= 0 && ref_marked(mark, c)) ? odst[c] : rdst[v];
           bst = A.psi[off + ns] - phi_s;
         }
       } else {
@@ -183,12 +180,14 @@ hipError_t launch_greedy(const ArenaView& A, const void* logits, int32_t dtype, 
     if (e != hipErrorNotSupported) return e;
     (void)hipGetLastError();
   }
-  const size_t lds = (size_t)6 * (A.V1 - 1) + 4;
+  const size_t lds = ref_table_bytes(A.V1 - 1);
   if (dtype == TB_F32) {
+    allow_dynamic_lds(&greedy_ref_kernel<LoadF32>, lds);
     hipLaunchKernelGGL(greedy_ref_kernel<LoadF32>, dim3(B), dim3(kThreads), lds, st, A,
                        static_cast<const float*>(logits), T, B, row_stride, model_ids, states,
                        out_tok, out_state, out_score);
   } else {
+    allow_dynamic_lds(&greedy_ref_kernel<LoadBF16>, lds);
     hipLaunchKernelGGL(greedy_ref_kernel<LoadBF16>, dim3(B), dim3(kThreads), lds, st, A,
                        static_cast<const uint16_t*>(logits), T, B, row_stride, model_ids, states,
                        out_tok, out_state, out_score);

@@ -51,8 +51,9 @@ hipError_t launch_greedy_wide(const ArenaView& A, const void* logits, int32_t dt
                               int32_t* states, int32_t* out_tok, int32_t* out_state,
                               float* out_score, hipStream_t st);
 
-// Largest V+1 the step kernels accept (LDS tables are sized by it).
-constexpr int32_t kMaxV1 = 10241;
+// Largest V+1 the step kernels accept: the compiler's limit (the reference
+// kernels' per-class LDS table, 4 B and one bit per class, fits up to it).
+constexpr int32_t kMaxV1 = 32768;
 
 // Test hooks (tb_debug_select_kernels, tb_debug_set_spin_limit): kernel
 // choices forced by tests, and the poll limit of the greedy hand-off wait
