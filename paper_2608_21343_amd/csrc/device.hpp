@@ -27,6 +27,7 @@ struct ArenaView {
   const uint32_t* arc_mem;  // two words per state (see tb_arena_layout)
   const float* value_tab;      // per model: 256 psi values, 256 phi values
   const uint32_t* state_rec;   // three words per state (see tb_arena_layout)
+  int64_t n_states;      // over all models
   int32_t n_models;
   int32_t V1;            // V + 1
   int32_t max_override;  // most tokens any state overrides
@@ -52,6 +53,7 @@ inline ArenaView make_view(const tb_arena& a) {
   v.arc_mem = reinterpret_cast<const uint32_t*>(b + L.off_arc_mem);
   v.value_tab = reinterpret_cast<const float*>(b + L.off_value_tab);
   v.state_rec = reinterpret_cast<const uint32_t*>(b + L.off_state_rec);
+  v.n_states = L.n_states;
   v.n_models = L.n_models;
   v.V1 = L.v_plus_blank;
   v.max_override = L.max_override;

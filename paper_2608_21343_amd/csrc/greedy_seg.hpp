@@ -236,10 +236,13 @@ struct Graph {
   }
 };
 
-// Graph records for the greedy kernels: packed records from LDS for states <
-// nhot whose record is usable, else the plain arena arrays by scalar loads
-// (state ids are uniform; the arena is immutable while a step runs).
-struct SGraph {
+// Graph records for the greedy kernels: the packed record of a state from LDS
+// for states < nhot; with FAR, the others from the arena's packed records
+// (the arena is immutable while a step runs); the plain arena arrays for a
+// record that is not usable (flagged) and, without FAR, for states >= nhot.
+template <bool FAR>
+struct SGraphT {
+  static constexpr bool kFar = FAR;
   const ArenaView* A;
   int32_t off, nhot;
   const uint32_t* w0;
@@ -249,20 +252,32 @@ struct SGraph {
   const float* vphi;
   const uint16_t* cls_tok;  // class members (LDS copy of the arena's cls_tok)
   template <int HOT, int PER>
-  __device__ __forceinline__ SGraph(const ArenaView& a, int32_t o, int32_t nh,
-                                    const StateHot<HOT>& h, const Tables<PER>& tb)
+  __device__ __forceinline__ SGraphT(const ArenaView& a, int32_t o, int32_t nh,
+                                     const StateHot<HOT>& h, const Tables<PER>& tb)
       : A(&a), off(o), nhot(nh), w0(h.w0), w1(h.w1), w2(h.w2), vpsi(h.vpsi), vphi(h.vphi),
         cls_tok(tb.cls_tok) {}
-  // first child, child count, suffix link and phi of state x from LDS
-  // (uniform); false when x has no usable LDS record
+  // first child, child count, suffix link and phi of state x from its packed
+  // record (uniform); false when there is no usable one (see above), or when
+  // the value tables are not in LDS (no hot states)
   __device__ __forceinline__ bool srec(int32_t x, int32_t& fc, int32_t& nc, int32_t& lnk,
                                        float& phi) const {
-    if (x >= nhot) return false;
-    // the three words are read together (one LDS round trip), then checked
-    const uint32_t a0 = w0[x], b0 = w1[x], c0 = w2[x];
-    const uint32_t c = __builtin_amdgcn_readfirstlane(c0);
-    const uint32_t a = __builtin_amdgcn_readfirstlane(a0);
-    const uint32_t b = __builtin_amdgcn_readfirstlane(b0);
+    uint32_t a, b, c;
+    if (x < nhot) {
+      // the three words are read together (one LDS round trip), then checked
+      const uint32_t a0 = w0[x], b0 = w1[x], c0 = w2[x];
+      c = __builtin_amdgcn_readfirstlane(c0);
+      a = __builtin_amdgcn_readfirstlane(a0);
+      b = __builtin_amdgcn_readfirstlane(b0);
+    } else if constexpr (FAR) {
+      if (nhot == 0) return false;  // no value tables in LDS
+      const uint32_t* g = A->state_rec + 3 * ((int64_t)off + x);
+      const uint32_t a0 = gload(g), b0 = gload(g + 1), c0 = gload(g + 2);
+      c = __builtin_amdgcn_readfirstlane(c0);
+      a = __builtin_amdgcn_readfirstlane(a0);
+      b = __builtin_amdgcn_readfirstlane(b0);
+    } else {
+      return false;
+    }
     if (c >> 31) return false;
     fc = (int32_t)(a & 0xffffu);
     nc = (int32_t)((a >> 16) & 0xffu);
@@ -290,6 +305,7 @@ struct SGraph {
     }
   }
 };
+using SGraph = SGraphT<false>;
 
 // Arc member record fields.
 __device__ __forceinline__ int32_t arc_class(uint2 m) { return (int32_t)((m.y >> 16) & 0x7fffu); }
@@ -420,7 +436,8 @@ __device__ __forceinline__ void child_rec(const Graph& G, int32_t y, uint2& m, f
 
 // Arc record (as arc_mem) and psi of child y: rebuilt from its LDS record
 // when it has a usable one, else read from the arena.
-__device__ __forceinline__ void child_rec(const SGraph& G, int32_t y, uint2& m, float& py) {
+template <bool F>
+__device__ __forceinline__ void child_rec(const SGraphT<F>& G, int32_t y, uint2& m, float& py) {
   if (y < G.nhot) {
     const uint32_t a = G.w0[y], b = G.w1[y], c = G.w2[y];
     if (!(c >> 31)) {
@@ -439,7 +456,8 @@ __device__ __forceinline__ void child_rec(const SGraph& G, int32_t y, uint2& m, 
 }
 
 // Marks the classes of the children [fc, fc+nc).
-__device__ __forceinline__ void mark_children(const SGraph& G, uint32_t* marks, int32_t fc,
+template <bool F>
+__device__ __forceinline__ void mark_children(const SGraphT<F>& G, uint32_t* marks, int32_t fc,
                                               int32_t nc) {
   for (int32_t j = __lane_id(); j < nc; j += 64) {
     uint2 m;
@@ -504,8 +522,8 @@ __device__ __forceinline__ void root_scan(const Tables<PER>& tb, const float* zr
 // (the row's best of those is r.r1 unless its class is overridden); the blank
 // keeps the state. Class marks are needed only when the chain has more than
 // one state (to let deeper states win) or when r.r1's class is overridden.
-template <int PER>
-__device__ __forceinline__ Answer eval_general(const SGraph& G, const Tables<PER>& tb,
+template <int PER, class GR>
+__device__ __forceinline__ Answer eval_general(const GR& G, const Tables<PER>& tb,
                                                const float* zrow, uint32_t* marks,
                                                const RowShape<PER>& rs, int32_t x, const RowSum& r,
                                                const LaneTop* top, int32_t V) {
@@ -631,14 +649,14 @@ __device__ __forceinline__ Answer eval_general(const SGraph& G, const Tables<PER
 
 // The step from state x given the first children and child counts of its
 // suffix chain (x first, levels non-root states, kChainMax at most): up to
-// 128 children, two per lane (slot i in lane i, slot 64 + i in lane i's
-// second register), provided the children of every level but the shallowest
-// fit in the first 64 slots (the shadowing scan reads them by readlane).
-// Returns false, with no output, on any other shape.
+// 64*NS children, NS per lane (slot 64*i + lane in the lane's i-th register),
+// provided the children of every level but the shallowest fit in the first 64
+// slots (the shadowing scan reads them by readlane). Returns false, with no
+// output, on any other shape.
 constexpr int kChainMax = 8;
 
-template <int PER>
-__device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PER>& tb,
+template <int PER, int NS, class GR>
+__device__ __forceinline__ bool eval_chain_wide(const GR& G, const Tables<PER>& tb,
                                                 const float* zrow, uint32_t* marks,
                                                 const RowShape<PER>& rs, int32_t x, float phi_x,
                                                 const int32_t (&fl)[kChainMax],
@@ -655,7 +673,7 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
   int32_t last = 0;  // first slot of the shallowest level
 #pragma unroll
   for (int i = 1; i < kLv; ++i) last = (i < levels) ? st[i] : last;
-  if (total > 128 || last > 64) return false;
+  if (total > 64 * NS || last > 64) return false;
 
   // a slot's child: its level, state record and best member
   auto slot = [&](int32_t q, int32_t& lv, int32_t& y, int32_t& lab, float& py, float& kb,
@@ -677,6 +695,13 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
       c0 = G.w0[y];
       c1 = G.w1[y];
       c2 = G.w2[y];
+    } else if constexpr (GR::kFar) {
+      if (in && G.nhot > 0) {  // the arena's packed record
+        const uint32_t* g = G.A->state_rec + 3 * ((int64_t)G.off + y);
+        c0 = gload(g);
+        c1 = gload(g + 1);
+        c2 = gload(g + 2);
+      }
     }
     const int32_t mc = (int32_t)(c2 & 0xffu);
     bad = in && ((c2 >> 31) != 0u || mc > 3);
@@ -694,53 +719,86 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
     if (k1 > kb) { kb = k1; tk = t1; zb = z1; }  // members ascend: ties keep the lower
     if (k2 > kb) { kb = k2; tk = t2; zb = z2; }
   };
-  int32_t lvA, yA, labA, tkA, lvB, yB, labB, tkB;
-  float pyA, kA, zA, pyB, kB, zB;
-  bool inA, inB, badA, badB;
-  slot(lane, lvA, yA, labA, pyA, kA, zA, tkA, inA, badA);
-  slot(64 + lane, lvB, yB, labB, pyB, kB, zB, tkB, inB, badB);
-  if (__ballot(badA || badB) != 0ull) return false;
+  int32_t lvS[NS], yS[NS], labS[NS], tkS[NS];
+  float pyS[NS], kS[NS], zS[NS];
+  bool inS[NS];
+  bool anybad = false;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) {
+    bool bad;
+    slot(64 * i + lane, lvS[i], yS[i], labS[i], pyS[i], kS[i], zS[i], tkS[i], inS[i], bad);
+    anybad = anybad || bad;
+  }
+  if (__ballot(anybad) != 0ull) return false;
   // A class that a deeper chain state (a lower level) also has is shadowed;
   // the deeper levels' slots are all below 64 (lane = slot). The best of all
   // children is the answer unless it is shadowed (a shadowing child has the
   // same tokens; see eval_walk), which is checked on the winner alone.
-  auto best = [&](bool tA, bool tB, int32_t& wl, bool& useB, float& ok, int32_t& ot) {
-    const float kAt = tA ? kA : kNegInf, kBt = tB ? kB : kNegInf;
-    const int32_t tAt = tA ? tkA : INT_MAX, tBt = tB ? tkB : INT_MAX;
-    useB = better(kBt, tBt, kAt, tAt);
-    wl = wave_argmax_dpp(useB ? kBt : kAt, useB ? tBt : tAt, ok, ot);
-  };
-  float ok = kNegInf, o_psi = 0.f, o_z = 0.f;
-  int32_t ot = INT_MAX, wl;
-  bool useB;
-  best(inA, inB, wl, useB, ok, ot);
-  {
-    const bool wB = rl((int32_t)useB, wl) != 0;
-    const int32_t lw = rl(wB ? labB : labA, wl), vw = rl(wB ? lvB : lvA, wl);
-    if (__ballot((inA && labA == lw && lvA < vw) || (inB && labB == lw && lvB < vw)) != 0ull) {
-      bool takeA = inA, takeB = inB;
-      for (int32_t j = 0; j < last; ++j) {
-        const int32_t cj = __builtin_amdgcn_readlane(labA, j);
-        const int32_t lvj = __builtin_amdgcn_readlane(lvA, j);
-        takeA = takeA && !(lvj < lvA && cj == labA);
-        takeB = takeB && !(lvj < lvB && cj == labB);
+  // the winner's class, level, child, psi and logit (uniform)
+  int32_t w_lab = 0, w_lv = 0, w_y = 0;
+  float w_py = 0.f, w_z = 0.f;
+  auto best = [&](const bool (&take)[NS], float& ok, int32_t& ot) {
+    float bk = kNegInf;
+    int32_t bt = INT_MAX, blab = 0, blv = 0, by = 0;
+    float bpy = 0.f, bz = 0.f;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {  // strict: ties keep the lower slot
+      const float k = take[i] ? kS[i] : kNegInf;
+      const int32_t t = take[i] ? tkS[i] : INT_MAX;
+      if (better(k, t, bk, bt)) {
+        bk = k;
+        bt = t;
+        blab = labS[i];
+        blv = lvS[i];
+        by = yS[i];
+        bpy = pyS[i];
+        bz = zS[i];
       }
-      best(takeA, takeB, wl, useB, ok, ot);
+    }
+    const int32_t wl = wave_argmax_dpp(bk, bt, ok, ot);
+    w_lab = rl(blab, wl);
+    w_lv = rl(blv, wl);
+    w_y = rl(by, wl);
+    w_py = rlf(bpy, wl);
+    w_z = rlf(bz, wl);
+  };
+  float ok = kNegInf;
+  int32_t ot = INT_MAX;
+  best(inS, ok, ot);
+  {
+    const int32_t lw = w_lab, vw = w_lv;
+    bool sh = false;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) sh = sh || (inS[i] && labS[i] == lw && lvS[i] < vw);
+    if (__ballot(sh) != 0ull) {
+      bool take[NS];
+#pragma unroll
+      for (int i = 0; i < NS; ++i) take[i] = inS[i];
+      for (int32_t j = 0; j < last; ++j) {
+        const int32_t cj = __builtin_amdgcn_readlane(labS[0], j);
+        const int32_t lvj = __builtin_amdgcn_readlane(lvS[0], j);
+#pragma unroll
+        for (int i = 0; i < NS; ++i) take[i] = take[i] && !(lvj < lvS[i] && cj == labS[i]);
+      }
+      best(take, ok, ot);
     }
   }
-  const int32_t o_ns = rl(useB ? yB : yA, wl);
-  o_psi = rlf(useB ? pyB : pyA, wl);
-  o_z = rlf(useB ? zB : zA, wl);
+  const int32_t o_ns = w_y;
+  const float o_psi = w_py, o_z = w_z;
   // every chain child's class overrides its root move; the remaining root
   // moves have keys at most r.ymax, so when the best child or the blank is
   // above it no root move can win
-  const bool hit = __ballot((inA && labA == r.r1_cls) || (inB && labB == r.r1_cls)) != 0ull;
+  bool h = false;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) h = h || (inS[i] && labS[i] == r.r1_cls);
+  const bool hit = __ballot(h) != 0ull;
   const bool root_lost = hit && (ok > r.ymax || r.zb + phi_x > r.ymax);
   const bool over = hit && !root_lost;
   if (over) {
     marks_clear<PER>(marks);
-    if (inA) mark(marks, labA);
-    if (inB) mark(marks, labB);
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+      if (inS[i]) mark(marks, labS[i]);
     marks_fence();
   }
 
@@ -779,6 +837,26 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
   return true;
 }
 
+// eval_chain_wide with two children per lane, or four (when NSMAX allows it)
+// when the chain has more than 128.
+template <int PER, int NSMAX = 2, class GR = SGraph>
+__device__ __forceinline__ bool eval_chain_any(const GR& G, const Tables<PER>& tb,
+                                               const float* zrow, uint32_t* marks,
+                                               const RowShape<PER>& rs, int32_t x, float phi_x,
+                                               const int32_t (&fl)[kChainMax],
+                                               const int32_t (&nl)[kChainMax], int32_t levels,
+                                               const RowSum& r, const LaneTop* top, int32_t V,
+                                               Answer& a) {
+  int32_t total = 0;
+#pragma unroll
+  for (int i = 0; i < kChainMax; ++i) total += nl[i];
+  if (NSMAX < 4 || total <= 128)
+    return eval_chain_wide<PER, 2, GR>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top,
+                                       V, a);
+  return eval_chain_wide<PER, 4, GR>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top, V,
+                                     a);
+}
+
 
 // The step from state x from the packed state records in LDS. The children of
 // the states on x's suffix chain (x, link(x), ... up to four non-root states,
@@ -788,12 +866,14 @@ __device__ __forceinline__ bool eval_chain_wide(const SGraph& G, const Tables<PE
 // class is overridden, else the best unmarked one from the lanes' two best
 // root moves (top) or a masked scan of the row. The blank keeps the state.
 // Returns false, with no output, on any other shape (a state or child without
-// a usable LDS record, a class of more than three members).
-template <int PER>
-__device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb,
+// a usable record, a class of more than three members, too many children);
+// longer is set when the reason is a chain of more than four states.
+template <int PER, int NSMAX = 2, class GR = SGraph>
+__device__ __forceinline__ bool eval_walk(const GR& G, const Tables<PER>& tb,
                                           const float* zrow, uint32_t* marks,
                                           const RowShape<PER>& rs, int32_t x, const RowSum& r,
-                                          const LaneTop* top, int32_t V, Answer& a) {
+                                          const LaneTop* top, int32_t V, Answer& a,
+                                          bool& longer) {
   const int lane = __lane_id();
   int32_t fc, nc, lnk;
   float phi_x;
@@ -804,7 +884,10 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
     n0 = nc;
     levels = 1;
     while (lnk != 0) {
-      if (levels == 4) return false;
+      if (levels == 4) {
+        longer = true;
+        return false;
+      }
       float phi_unused;
       if (!G.srec(lnk, fc, nc, lnk, phi_unused)) return false;
       if (levels == 1) { f1 = fc; n1 = nc; }
@@ -817,7 +900,8 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
   if (total > 64) {  // more children than lanes: two per lane
     const int32_t fl[kChainMax] = {f0, f1, f2, f3, 0, 0, 0, 0};
     const int32_t nl[kChainMax] = {n0, n1, n2, n3, 0, 0, 0, 0};
-    return eval_chain_wide<PER>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top, V, a);
+    return eval_chain_any<PER, NSMAX, GR>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top,
+                                      V, a);
   }
 
   // best override candidate (none when the chain has no children)
@@ -835,6 +919,13 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
       c0 = G.w0[y];
       c1 = G.w1[y];
       c2 = G.w2[y];
+    } else if constexpr (GR::kFar) {
+      if (in && G.nhot > 0) {  // the arena's packed record
+        const uint32_t* g = G.A->state_rec + 3 * ((int64_t)G.off + y);
+        c0 = gload(g);
+        c1 = gload(g + 1);
+        c2 = gload(g + 2);
+      }
     }
     const int32_t mc = (int32_t)(c2 & 0xffu);
     if (__ballot(in && ((c2 >> 31) != 0u || mc > 3)) != 0ull) return false;
@@ -925,8 +1016,8 @@ __device__ __forceinline__ bool eval_walk(const SGraph& G, const Tables<PER>& tb
 
 // eval_walk for chains of up to kChainMax non-root states (and the child
 // sets of eval_chain_wide). Returns false, with no output, on any other shape.
-template <int PER>
-__device__ __forceinline__ bool eval_walk2(const SGraph& G, const Tables<PER>& tb,
+template <int PER, int NSMAX = 2, class GR = SGraph>
+__device__ __forceinline__ bool eval_walk2(const GR& G, const Tables<PER>& tb,
                                            const float* zrow, uint32_t* marks,
                                            const RowShape<PER>& rs, int32_t x, const RowSum& r,
                                            const LaneTop* top, int32_t V, Answer& a) {
@@ -951,20 +1042,23 @@ __device__ __forceinline__ bool eval_walk2(const SGraph& G, const Tables<PER>& t
     }
   }
   if (lnk != 0) return false;
-  return eval_chain_wide<PER>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top, V, a);
+  return eval_chain_any<PER, NSMAX, GR>(G, tb, zrow, marks, rs, x, phi_x, fl, nl, levels, r, top,
+                                    V, a);
 }
 
 // The boosted step from state x: from the LDS records when they apply, else
 // the general path.
-template <int PER>
-__device__ __forceinline__ Answer eval_state(const SGraph& G, const Tables<PER>& tb,
+template <int PER, int NSMAX = 2, class GR = SGraph>
+__device__ __forceinline__ Answer eval_state(const GR& G, const Tables<PER>& tb,
                                              const float* zrow, uint32_t* marks,
                                              const RowShape<PER>& rs, int32_t x, const RowSum& r,
                                              const LaneTop* top, int32_t V) {
   Answer a;
-  if (eval_walk<PER>(G, tb, zrow, marks, rs, x, r, top, V, a)) return a;
-  if (eval_walk2<PER>(G, tb, zrow, marks, rs, x, r, top, V, a)) return a;
-  return eval_general<PER>(G, tb, zrow, marks, rs, x, r, top, V);
+  bool longer = false;
+  if (eval_walk<PER, NSMAX, GR>(G, tb, zrow, marks, rs, x, r, top, V, a, longer)) return a;
+  // only a longer chain is a shape eval_walk2 takes that eval_walk does not
+  if (longer && eval_walk2<PER, NSMAX, GR>(G, tb, zrow, marks, rs, x, r, top, V, a)) return a;
+  return eval_general<PER, GR>(G, tb, zrow, marks, rs, x, r, top, V);
 }
 
 // log(sum(exp(z))) of a row from this lane's elements and their maximum:
@@ -1058,8 +1152,8 @@ __device__ __forceinline__ float row_lse_lds(const float* zrow, const RowShape<P
 }
 
 // The step from state s on a summarised row (zrow in LDS).
-template <int PER>
-__device__ __forceinline__ Answer step_from(const SGraph& G, const Tables<PER>& tb,
+template <int PER, int NSMAX = 2, class GR = SGraph>
+__device__ __forceinline__ Answer step_from(const GR& G, const Tables<PER>& tb,
                                             const float* zrow, uint32_t* marks,
                                             const RowShape<PER>& rs, const RowSum& r, int32_t s,
                                             int mode, int32_t V, const LaneTop* top = nullptr) {
@@ -1072,7 +1166,7 @@ __device__ __forceinline__ Answer step_from(const SGraph& G, const Tables<PER>& 
     a.zv = blank ? r.zb : r.ymax;
     return a;
   }
-  return eval_state<PER>(G, tb, zrow, marks, rs, s, r, top, V);
+  return eval_state<PER, NSMAX, GR>(G, tb, zrow, marks, rs, s, r, top, V);
 }
 
 // One complete step on a row held in registers.
@@ -1502,9 +1596,15 @@ __global__ __launch_bounds__(kFixThreads) void greedy_fix_kernel(
 // walker evaluation in the stream with the longest match: three rounds
 // measured best on 128 streams of 16-row chunks (two and four were slower).
 // While wave 0 walks, the other waves take the rows' normalisers.
+//
+// FAR: for arenas whose models are larger than the LDS records on average,
+// states beyond them are read from the arena's packed records and suffix
+// chains with up to 256 children (four per lane) stay on the fast path; the
+// other instance, which every model that fits runs, reads such states through
+// the general path. Both give the same results.
 constexpr int kSpecRounds = 3;
 
-template <class Ld, int PER>
+template <class Ld, int PER, bool FAR>
 __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     ArenaView A, const typename Ld::T* __restrict__ logits, int32_t T, int32_t B, int64_t stride,
     const int32_t* __restrict__ model_ids, int32_t* __restrict__ states,
@@ -1512,6 +1612,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     float* __restrict__ out_score) {
   constexpr int NT = Shape<PER>::NT;
   constexpr int HOT = SegLds<PER>::HOT;
+  constexpr int NSMAX = FAR ? 4 : 2;
   __shared__ SegLds<PER> S;
   lds_poison(&S, sizeof(S));
   const int32_t V1 = A.V1, V = V1 - 1;
@@ -1552,7 +1653,7 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   }
   __syncthreads();
 
-  const SGraph Gr(A, off, nhot, S.hot, S.tab);
+  const SGraphT<FAR> Gr(A, off, nhot, S.hot, S.tab);
   const int32_t fixed = unbiased_state(mode, s0 == TB_STATE_TIMEOUT);
   int32_t x;  // guessed start state of row w
   if (mode != 1) {
@@ -1566,7 +1667,8 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
   bool need = own;
 #pragma unroll
   for (int round = 0; round < kSpecRounds; ++round) {
-    if (need) a = step_from<PER>(Gr, S.tab, S.zbuf[w], S.marks[w], rs, r, x, mode, V, &top);
+    if (need)
+      a = step_from<PER, NSMAX>(Gr, S.tab, S.zbuf[w], S.marks[w], rs, r, x, mode, V, &top);
     if (own && lane == 0) lds_st(&S.spec_ns[round & 1][w], a.ns);
     __syncthreads();
     if (round + 1 < kSpecRounds) {
@@ -1634,7 +1736,8 @@ __global__ __launch_bounds__(Shape<PER>::NT) void greedy_chunk_kernel(
     rt.r1_cls = rl(rl_.r1_cls, t);
     rt.r1_dst = rl(rl_.r1_dst, t);
     const LaneTop tt = {(int32_t)(tp & 0xffffu), (int32_t)(tp >> 16), 0.f, 0.f};
-    const Answer e = step_from<PER>(Gr, S.tab, S.zbuf[t], S.marks[0], rs, rt, s, mode, V, &tt);
+    const Answer e =
+        step_from<PER, NSMAX>(Gr, S.tab, S.zbuf[t], S.marks[0], rs, rt, s, mode, V, &tt);
     if (lane == t) ans = make_int4(e.tok, e.ns, __float_as_int(e.b), __float_as_int(e.zv));
     s = __builtin_amdgcn_readfirstlane(e.ns);
     ++t;
@@ -1679,9 +1782,15 @@ hipError_t launch_seg(const ArenaView& A, const void* logits, int32_t T, int32_t
   static_assert(sizeof(SegLds<PER>) <= Shape<PER>::kBudget + 1024, "LDS budget");
   static_assert(SegLds<PER>::HOT >= 64, "room for hot states");
   if (T <= Shape<PER>::W) {
-    hipLaunchKernelGGL((greedy_chunk_kernel<Ld, PER>), dim3(B), dim3(Shape<PER>::NT), 0, st, A,
-                       static_cast<const TT*>(logits), T, B, stride, model_ids, states, out_tok,
-                       out_state, out_score);
+    const bool far = A.n_states > (int64_t)SegLds<PER>::HOT * A.n_models;
+    if (far)
+      hipLaunchKernelGGL((greedy_chunk_kernel<Ld, PER, true>), dim3(B), dim3(Shape<PER>::NT), 0,
+                         st, A, static_cast<const TT*>(logits), T, B, stride, model_ids, states,
+                         out_tok, out_state, out_score);
+    else
+      hipLaunchKernelGGL((greedy_chunk_kernel<Ld, PER, false>), dim3(B), dim3(Shape<PER>::NT), 0,
+                         st, A, static_cast<const TT*>(logits), T, B, stride, model_ids, states,
+                         out_tok, out_state, out_score);
     return hipGetLastError();
   }
   int32_t G, L;
