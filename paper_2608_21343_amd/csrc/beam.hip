@@ -143,6 +143,7 @@ __global__ __launch_bounds__(kThreads) void beam_ref_kernel(
     const int32_t l = sa.tree_len[b];
     tlen = l < 0 ? 0 : (l > sa.cap ? sa.cap : l);
   }
+  __syncthreads();  // sh_bad and sh_tmo are complete
   if (mode == 1 && sh_bad) mode = -1;
   const float* rpsi = A.root_psi + (int64_t)(mode == 1 ? m : 0) * V1;
   const int32_t* rdst = A.root_dst + (int64_t)(mode == 1 ? m : 0) * V1;

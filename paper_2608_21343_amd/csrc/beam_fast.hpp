@@ -88,8 +88,6 @@ struct alignas(16) BeamFixed {
   float red_val[MAXK];
   int32_t red_f[MAXK];
   int32_t red_dst[MAXK];
-  int32_t bad;
-  int32_t tmo;  // a slot carried TB_STATE_TIMEOUT
   // streaming beam (tb_boost_step_beam_stream): hypothesis carry, double
   // buffered, and the listed tokens
   uint64_t hyp_h[2][SK], hyp_hp[2][SK];
@@ -326,14 +324,15 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     off = A.model_off[m];
     n = A.model_n[m];
   }
-  if (threadIdx.x == 0) { S.bad = 0; S.tmo = 0; }
-  __syncthreads();
+  // every wave reads the carried states and takes the same decision: a slot
+  // out of range decodes the stream unbiased, before any table is filled
+  const int32_t s_lane = (lane < K) ? states[(int64_t)b * K + lane] : 0;
+  if (mode == 1 && __ballot(lane < K && (s_lane < 0 || s_lane >= n)) != 0ull) mode = -1;
+  const bool tmo = __ballot(lane < K && s_lane == TB_STATE_TIMEOUT) != 0ull;
   if (threadIdx.x < K) {
-    const int32_t s = states[(int64_t)b * K + threadIdx.x];
+    const int32_t s = s_lane;
     S.hyp_s[0][threadIdx.x] = s;
     S.hyp_S[0][threadIdx.x] = scores[(int64_t)b * K + threadIdx.x];
-    if (mode == 1 && (s < 0 || s >= n)) S.bad = 1;
-    if (s == TB_STATE_TIMEOUT) S.tmo = 1;
     if constexpr (STREAM) {
       const tb_hyp hy = sa.hyps[(int64_t)b * K + threadIdx.x];
       S.hyp_h[0][threadIdx.x] = hy.hash;
@@ -396,7 +395,6 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
       reinterpret_cast<uint32_t*>(&S.stamps[0][0])[i] = 0u;
   }
   __syncthreads();
-  if (mode == 1 && S.bad) mode = -1;  // uniform: every thread read the same flag
   const int32_t nhot = (mode == 1) ? (n < HOT ? n : HOT) : 0;
   const seg::SGraph G(A, off, nhot, S.hot, S.tab);
   float* zrow = S.zbuf[w];
@@ -811,7 +809,7 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
           bst = ((d >= 0) ? G.psi_of(ns) : S.tab.rpsi[v]) - phi_k;
         }
       } else {
-        ns = unbiased_state(mode, S.tmo != 0);
+        ns = unbiased_state(mode, tmo);
       }
       const float z = S.zbuf[k][v];
       const float val = sel_val_w;

@@ -417,6 +417,41 @@ def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, restore_ke
     assert np.all(gpu[2][:, 4] == -2)
 
 
+@pytest.mark.parametrize("kernel,V,K", [("default", 300, 3), ("default", 300, 8), ("ref", 300, 3),
+                                        ("default", 2600, 4), ("wide", 2600, 4)])
+def test_beam_bad_carried_states_decode_unbiased(kernel, V, K, restore_kernels):
+    """A valid model id with a carried state out of range, TB_STATE_INVALID or
+    TB_STATE_TIMEOUT in one of its slots: the stream is decoded without
+    biasing (tokens, parents and scores of the oracle's model -1 run) and
+    writes TB_STATE_INVALID, or TB_STATE_TIMEOUT when a slot carried it."""
+    import torch
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
+    cfg, lists, rows = _small_case(8, B=4, V=V, n_case=V // 10, K=K, T=20, dtype="f32")
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, 1, 2, 3], np.int32)
+    say(f"[beam-bad-carry] {kernel} V+1={V + 1} K={K}")
+    m, states, scores = dec.start(mids, K)
+    carried = {1 * K + K - 1: 10 ** 6, 2 * K: capi.TB_STATE_TIMEOUT, 3 * K: capi.TB_STATE_INVALID}
+    for i, v in carried.items():
+        states[i] = v
+    out = dec.beam(to_device_logits(rows), m, states, scores)
+    torch.cuda.synchronize()
+    gpu = [o.cpu().numpy() for o in out]
+    graphs = oracle_graphs(cfg, lists, [0], mids)
+    st0, S0 = oracle.init_carry(mids, K)
+    ref = oracle.beam_decode(graphs, mids, rows, st0, S0, streams=[0])
+    compare_beam(gpu, ref, [0], ATOL)
+    free = np.array([0, -1, -1, -1], np.int32)
+    st1, S1 = oracle.init_carry(free, K)
+    ref1 = oracle.beam_decode(graphs, free, rows, st1, S1, streams=[1, 2, 3])
+    for i in (0, 1, 4):
+        assert np.array_equal(gpu[i][:, 1:], ref1[i][:, 1:]), i
+    assert float(np.max(np.abs(gpu[3][:, 1:] - ref1[3][:, 1:]))) <= ATOL
+    assert np.all(gpu[2][:, [1, 3]] == capi.TB_STATE_INVALID)
+    assert np.all(gpu[2][:, 2] == capi.TB_STATE_TIMEOUT)
+
+
 @pytest.mark.parametrize("V,K,dtype", [(1860, 8, "f32"), (1950, 4, "bf16"), (1983, 8, "bf16"),
                                        (1856, 2, "f32")])
 def test_beam_rows_of_30_and_31_chunks(V, K, dtype):
