@@ -452,6 +452,69 @@ def test_beam_bad_carried_states_decode_unbiased(kernel, V, K, restore_kernels):
     assert np.all(gpu[2][:, 2] == capi.TB_STATE_TIMEOUT)
 
 
+@pytest.mark.parametrize("kernel,V,K", [("default", 300, 3), ("ref", 300, 3), ("ref", 300, 12)])
+def test_streaming_beam_bad_carried_states_decode_unbiased(kernel, V, K, restore_kernels):
+    """The streaming beam with the carried states of the test above: the bad
+    streams follow the oracle's streaming beam on model -1, chunk by chunk."""
+    import torch
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
+    cfg, lists, rows = _small_case(9, B=4, V=V, n_case=V // 10, K=K, T=24, dtype="f32")
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, 1, 2, 3], np.int32)
+    say(f"[stream-beam-bad-carry] {kernel} V+1={V + 1} K={K}")
+    carry = dec.start_beam_stream(mids, K, 64)
+    carried = {1 * K + K - 1: 10 ** 6, 2 * K: capi.TB_STATE_TIMEOUT, 3 * K: capi.TB_STATE_INVALID}
+    for i, v in carried.items():
+        carry.states[i] = v
+    graphs = oracle_graphs(cfg, lists, range(4), mids)
+    ref = oracle.init_stream_carry(mids, K)
+    free = np.array([0, -1, -1, -1], np.int32)
+    ref1 = oracle.init_stream_carry(free, K)
+    rows_dev = to_device_logits(rows)
+    for t0 in range(0, cfg.T, 8):
+        gpu = [o.cpu().numpy() for o in dec.beam_stream(rows_dev[t0:t0 + 8], carry)]
+        want = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + 8], ref, tree_cap=64)
+        compare_beam(gpu, want, [0], ATOL)
+        want1 = oracle.beam_decode_stream(graphs, free, rows[t0:t0 + 8], ref1, tree_cap=64)
+        for i in (0, 1, 4):
+            assert np.array_equal(gpu[i][:, 1:], want1[i][:, 1:]), (t0, i)
+        assert float(np.max(np.abs(gpu[3][:, 1:] - want1[3][:, 1:]))) <= ATOL
+        assert np.all(gpu[2][:, [1, 3]] == capi.TB_STATE_INVALID)
+        assert np.all(gpu[2][:, 2] == capi.TB_STATE_TIMEOUT)
+
+
+GREEDY_KERNEL = {"default": capi.GREEDY_AUTO, "ref": capi.GREEDY_REF}
+
+
+@pytest.mark.parametrize("kernel,V,chunk", [("default", 300, 16), ("default", 300, 200),
+                                            ("default", 2600, 16), ("default", 2600, 200),
+                                            ("ref", 300, 16)])
+def test_greedy_bad_carried_states_decode_unbiased(kernel, V, chunk, restore_kernels):
+    """Greedy with a valid model id and a carried state out of range,
+    TB_STATE_INVALID or TB_STATE_TIMEOUT, through the short-call, segmented,
+    wide-row and reference kernels: such a stream decodes without biasing and
+    writes TB_STATE_INVALID (TB_STATE_TIMEOUT when it carried it)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    capi.tb_debug_select_kernels(greedy=GREEDY_KERNEL[kernel])
+    cfg, lists, rows = _small_case(10, B=4, V=V, n_case=V // 10, T=200)
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, 1, 2, 3], np.int32)
+    say(f"[greedy-bad-carry] {kernel} V+1={V + 1} chunk={chunk}")
+    s0 = np.array([0, 10 ** 6, capi.TB_STATE_TIMEOUT, capi.TB_STATE_INVALID], np.int32)
+    tok, st, sc, carry = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, chunk,
+                                    states0=s0)
+    graphs = oracle_graphs(cfg, lists, [0], mids)
+    ref = oracle.greedy_decode(graphs, mids, rows, np.zeros(4, np.int32), streams=[0])
+    compare_greedy((tok, st, sc), ref, [0], ATOL)
+    free = np.array([0, -1, -1, -1], np.int32)
+    ref1 = oracle.greedy_decode(graphs, free, rows, np.full(4, -1, np.int32), streams=[1, 2, 3])
+    assert np.array_equal(tok[:, 1:], ref1[0][:, 1:])
+    assert float(np.max(np.abs(sc[:, 1:] - ref1[2][:, 1:]))) <= ATOL
+    assert np.all(st[:, [1, 3]] == capi.TB_STATE_INVALID) and np.all(st[:, 2] == capi.TB_STATE_TIMEOUT)
+    assert list(carry[1:]) == [capi.TB_STATE_INVALID, capi.TB_STATE_TIMEOUT, capi.TB_STATE_INVALID]
+
+
 @pytest.mark.parametrize("V,K,dtype", [(1860, 8, "f32"), (1950, 4, "bf16"), (1983, 8, "bf16"),
                                        (1856, 2, "f32")])
 def test_beam_rows_of_30_and_31_chunks(V, K, dtype):
