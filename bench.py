@@ -31,10 +31,13 @@ single-process figure beside it.
 
 Other workloads (--workload): batched, beam, stress_greedy, stress_beam, each
 in its own launch pattern, for context; stress_beam prepares 4.3 GB of
-logits on the host first (about two minutes).
+logits on the host first (about two minutes). The default run also measures
+batched, beam, stress_greedy and variative_streaming in short runs of their
+own (child processes, 5 steps after 2 warm-up steps) and reports them under
+``other_workloads`` (--no-others skips them).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                       [--copy-probe] [--workload NAME]
+                       [--copy-probe] [--workload NAME] [--no-others]
 """
 
 from __future__ import annotations
@@ -376,6 +379,41 @@ def stream_beam_figures(dec, cfg, rows_dev, mids, stream, reps: int = 4) -> dict
             "tree_cap": 4096}
 
 
+# Workloads the default run also measures, each in a child process with a
+# short run of its own (the stress beam's 4.3 GB of host-side logits take too
+# long for the default run).
+OTHER_WORKLOADS = ("batched", "beam", "stress_greedy", "variative_streaming")
+
+
+def other_workloads(steps: int, warmup: int) -> dict:
+    """Short bench runs of the other workloads (child processes, one at a
+    time): per workload its step time, throughput and roofline figures."""
+    import subprocess
+    out = {}
+    for w in OTHER_WORKLOADS:
+        print(f"bench: workload {w}", file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        cmd = [sys.executable, os.path.abspath(__file__), "--workload", w, "--steps", str(steps),
+               "--warmup", str(warmup), "--no-cpu-baseline", "--no-others"]
+        try:
+            p = subprocess.run(cmd, capture_output=True, text=True, timeout=300)
+        except subprocess.TimeoutExpired:
+            out[w] = {"error": "timed out after 300 s"}
+            continue
+        lines = [ln for ln in p.stdout.splitlines() if ln.startswith("{")]
+        if p.returncode != 0 or not lines:
+            out[w] = {"error": f"exit {p.returncode}: {p.stderr.strip()[-300:]}"}
+            continue
+        d = json.loads(lines[-1])
+        r = d["roofline"]
+        out[w] = {"workload": d["config"]["workload"], "ms_per_step": d["ms_per_step"],
+                  "value": d["value"], "unit": d["unit"], "dtype": d["dtype"],
+                  "avg_launch_us": r["avg_launch_us"], "achieved_GBps": r["achieved"],
+                  "frac": r["frac"], "kernel": r["kernel"], "steps": d["steps"],
+                  "run_s": time.perf_counter() - t0}
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -385,6 +423,8 @@ def main() -> int:
     ap.add_argument("--copy-probe", action="store_true",
                     help="first run one plain 256 MiB device copy (counter calibration)")
     ap.add_argument("--workload", default="streaming", choices=sorted(KERNELS))
+    ap.add_argument("--no-others", action="store_true",
+                    help="streaming only: skip the short runs of the other workloads")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the "
@@ -644,6 +684,9 @@ def main() -> int:
         result["stream_beam"] = stream_beam_figures(dec, cfg, rows_bufs[0], W.model_ids(cfg),
                                                     stream)
     del logits, bufs, rows_bufs
+    if cfg.name == "streaming" and not args.no_others:
+        torch.cuda.empty_cache()
+        result["other_workloads"] = other_workloads(steps=5, warmup=2)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg)
     print(json.dumps(result), flush=True)

@@ -170,7 +170,7 @@ __device__ __forceinline__ float wave_nth_largest(float x, int32_t n) {
 // wave per row (t, b, k), rows in (t*B + b)*K + k order.
 template <class Ld, int PER>
 __global__ __launch_bounds__(kPrepThreads) void beam_prep_kernel(
-    ArenaView A, const typename Ld::T* __restrict__ logits, int64_t n_rows, int32_t B,
+    ArenaView A, const typename Ld::T* __restrict__ logits, int64_t r0, int64_t n_rows, int32_t B,
     int32_t K, int64_t stride, const int32_t* __restrict__ model_ids,
     const int32_t* __restrict__ states, int32_t* __restrict__ out_tok,
     int32_t* __restrict__ out_parent, int32_t* __restrict__ out_state,
@@ -180,7 +180,7 @@ __global__ __launch_bounds__(kPrepThreads) void beam_prep_kernel(
   lds_poison(g_key, sizeof(g_key));
   lds_poison(g_tok, sizeof(g_tok));
   const int lane = __lane_id();
-  const int64_t r = (int64_t)blockIdx.x * (kPrepThreads / 64) + (threadIdx.x >> 6);
+  const int64_t r = r0 + (int64_t)blockIdx.x * (kPrepThreads / 64) + (threadIdx.x >> 6);
   if (r >= n_rows) return;  // uniform per wave; no barrier follows
   const int32_t V1 = A.V1, V = V1 - 1;
   const int32_t b = (int32_t)((r / K) % B);
@@ -880,13 +880,18 @@ hipError_t launch_beam_any(const ArenaView& A, const void* logits, int32_t T, in
                            StreamArgs sa) {
   static_assert(sizeof(BeamLds<PER, MAXK, STREAM ? MAXK : 1>) <= 160 * 1024, "LDS budget");
   typedef typename Ld::T TT;
+  // rows [r0, n_rows) in launches of at most 2^30 workgroups
   const int64_t n_rows = (int64_t)T * B * K;
-  const int64_t blocks = (n_rows + kPrepThreads / 64 - 1) / (kPrepThreads / 64);
-  hipLaunchKernelGGL((beam_prep_kernel<Ld, PER>), dim3((uint32_t)blocks), dim3(kPrepThreads), 0,
-                     st, A, static_cast<const TT*>(logits), n_rows, B, K, stride, model_ids,
-                     states, out_tok, out_parent, out_state, out_step, out_cum);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  constexpr int64_t kRowsPerLaunch = (int64_t)(kPrepThreads / 64) << 30;
+  for (int64_t r0 = 0; r0 < n_rows; r0 += kRowsPerLaunch) {
+    const int64_t nr = (n_rows - r0 < kRowsPerLaunch) ? n_rows - r0 : kRowsPerLaunch;
+    const int64_t blocks = (nr + kPrepThreads / 64 - 1) / (kPrepThreads / 64);
+    hipLaunchKernelGGL((beam_prep_kernel<Ld, PER>), dim3((uint32_t)blocks), dim3(kPrepThreads),
+                       0, st, A, static_cast<const TT*>(logits), r0, n_rows, B, K, stride,
+                       model_ids, states, out_tok, out_parent, out_state, out_step, out_cum);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL((beam_fast_kernel<Ld, PER, MAXK, STREAM>), dim3(B), dim3(64 * K), 0, st, A,
                      static_cast<const TT*>(logits), T, B, K, stride, model_ids, states, scores,
                      out_tok, out_parent, out_state, out_step, out_cum, sa);
