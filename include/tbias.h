@@ -445,7 +445,9 @@ int tb_reset_stream(const tb_arena* a, int32_t B, int32_t b, int32_t new_model_i
  * removed model should be reset. Lifecycle calls and step calls on one
  * registry must be ordered on one stream (the step calls read the model
  * table and the moved ranges). The registry handle is host memory owned by
- * the library (tb_registry_free).
+ * the library (tb_registry_free); calls that take it must not overlap in
+ * time (the lifecycle calls update its host copy of the model table and its
+ * staging buffer), so host threads that share one registry serialise them.
  *
  * tb_registry_layout — layout (and total_bytes) of a registry's device
  *   arena; max_models >= 1, max_states in [max_models, 2^31), v_plus_blank
