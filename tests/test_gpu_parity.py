@@ -515,6 +515,48 @@ def test_greedy_bad_carried_states_decode_unbiased(kernel, V, chunk, restore_ker
     assert list(carry[1:]) == [capi.TB_STATE_INVALID, capi.TB_STATE_TIMEOUT, capi.TB_STATE_INVALID]
 
 
+@pytest.mark.parametrize("kernel,V,K,chunk", [
+    ("default", 300, 1, 16), ("default", 300, 1, 96), ("ref", 300, 1, 16),
+    ("default", 2600, 1, 16), ("default", 2600, 1, 96),
+    ("default", 300, 3, 96), ("default", 300, 8, 40), ("ref", 300, 3, 96),
+    ("default", 2600, 4, 96), ("wide", 2600, 4, 96), ("stream", 300, 3, 32)])
+def test_padded_row_stride_every_kernel(kernel, V, K, chunk, restore_kernels):
+    """Rows farther apart than V+1 (seven values of 1e30 after each row, which
+    any read of them would make win) through every greedy and beam kernel and
+    the streaming beam, against the oracle on the unpadded rows."""
+    import torch
+    from paper_2608_21343_amd.decoder import BoostDecoder
+    if K == 1:
+        capi.tb_debug_select_kernels(greedy=GREEDY_KERNEL[kernel])
+    elif kernel != "stream":
+        capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
+    cfg, lists, rows = _small_case(11, B=4, V=V, n_case=V // 10, K=K, T=96)
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, 1, -1, 3], np.int32)
+    T, B, V1 = cfg.T, cfg.B, cfg.Vp1
+    say(f"[padded-stride] {kernel} V+1={V1} K={K} chunk={chunk}")
+    pad = torch.full((T, B, K, V1 + 7), 1e30, dtype=torch.float32, device="cuda")
+    pad[..., :V1] = torch.from_numpy(rows).cuda()
+    view = pad[..., :V1]
+    graphs = oracle_graphs(cfg, lists, range(B), mids)
+    if K == 1:
+        gpu = gpu_greedy(dec, view[:, :, 0, :], mids, chunk)
+        ref = oracle.greedy_decode(graphs, mids, rows, np.where(mids >= 0, 0, -1).astype(np.int32))
+        compare_greedy(gpu, ref, range(B), ATOL)
+    elif kernel == "stream":
+        carry = dec.start_beam_stream(mids, K, 128)
+        want = oracle.init_stream_carry(mids, K)
+        for t0 in range(0, T, chunk):
+            got = [o.cpu().numpy() for o in dec.beam_stream(view[t0:t0 + chunk], carry)]
+            exp = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + chunk], want, tree_cap=128)
+            compare_beam(got, exp, range(B), ATOL)
+    else:
+        gpu = gpu_beam(dec, view, mids, chunk)
+        st0, S0 = oracle.init_carry(mids, K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(B), ATOL)
+
+
 @pytest.mark.parametrize("V,K,dtype", [(1860, 8, "f32"), (1950, 4, "bf16"), (1983, 8, "bf16"),
                                        (1856, 2, "f32")])
 def test_beam_rows_of_30_and_31_chunks(V, K, dtype):
