@@ -391,8 +391,8 @@ BEAM_KERNEL = {"default": capi.BEAM_AUTO, "wide": capi.BEAM_NO_PIPE, "ref": capi
 
 
 @pytest.mark.parametrize("kernel", ["default", "ref"])
-@pytest.mark.parametrize("K,dtype", [(2, "f32"), (3, "bf16"), (8, "f32"), (20, "f32"),
-                                     (32, "bf16")])
+@pytest.mark.parametrize("K,dtype", [(1, "f32"), (2, "f32"), (3, "bf16"), (5, "bf16"), (8, "f32"),
+                                     (20, "f32"), (32, "bf16")])
 def test_beam_kernels_match_oracle_on_mixed_streams(kernel, K, dtype, restore_kernels):
     """Every beam kernel against the oracle: ragged V+1 = 301, model -1, an
     empty list and an out-of-range id (decoded unbiased, states -2)."""
