@@ -443,10 +443,8 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     const float zb = seg::rlf(cur[PER - 1], PER > 1 ? 63 : V);
     const float lse = lse_cur;  // every lane loaded the same entry
     float phi_s = 0.f;
-    if (mode == 1) {
-      int32_t fc_u, nc_u, lk_u;
-      G.rec(s_k, fc_u, nc_u, lk_u, phi_s);
-    }
+    int32_t fc_s = 0, nc_s = 0, lk_s = 0;  // s_k's record, for the listing below
+    if (mode == 1) G.rec(s_k, fc_s, nc_s, lk_s, phi_s);
     const float c = (S_k - lse) - phi_s;
     if (lane == 0) {
       S.hyp_lse[w] = lse;
@@ -459,9 +457,8 @@ __global__ __launch_bounds__(64 * MAXK) void beam_fast_kernel(
     uint8_t tg = 0;
     if (mode == 1 && s_k != 0) {
       tg = seg::next_tag<PER>(stamps, tag);
-      int32_t fc, nc, lnk;
+      int32_t fc = fc_s, nc = nc_s, lnk = lk_s;
       float phi_unused;
-      G.rec(s_k, fc, nc, lnk, phi_unused);
       for (int32_t lvl = 0;; ++lvl) {
         for (int32_t j0 = 0; j0 < nc; j0 += 64) {
           const int32_t j = j0 + lane;
