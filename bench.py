@@ -427,8 +427,9 @@ def main() -> int:
                     help="streaming only: skip the short runs of the other workloads")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the "
-              f"streams are independent and shard by stream, see DESIGN.md)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the streams "
+              f"are independent: more GPUs would each run their own share of the streams with "
+              f"no exchange between steps)", file=sys.stderr)
         return 2
 
     import torch
