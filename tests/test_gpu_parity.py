@@ -557,6 +557,29 @@ def test_padded_row_stride_every_kernel(kernel, V, K, chunk, restore_kernels):
         compare_beam(gpu, ref, range(B), ATOL)
 
 
+@pytest.mark.parametrize("V", [2046, 2047, 2048])
+@pytest.mark.parametrize("K,chunk", [(1, 16), (1, 100), (4, 100), (8, 50)])
+def test_rows_at_the_wide_kernel_boundary(V, K, chunk):
+    """V+1 = 2047, 2048 (the widest rows of the one-wave-per-row kernels) and
+    2049 (the narrowest of the wide-row kernels), greedy in short and long
+    calls and beam, against the oracle."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg, lists, rows = _small_case(12, B=4, V=V, n_case=V // 9, K=K, T=100, dtype="bf16")
+    dec = BoostDecoder(lists, W.class_map(cfg), token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    mids = np.array([0, 1, -1, 3], np.int32)
+    say(f"[boundary] V+1={V + 1} K={K} chunk={chunk}")
+    graphs = oracle_graphs(cfg, lists, range(cfg.B), mids)
+    if K == 1:
+        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, chunk)
+        ref = oracle.greedy_decode(graphs, mids, rows, np.where(mids >= 0, 0, -1).astype(np.int32))
+        compare_greedy(gpu, ref, range(cfg.B), ATOL)
+    else:
+        gpu = gpu_beam(dec, to_device_logits(rows), mids, chunk)
+        st0, S0 = oracle.init_carry(mids, K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(cfg.B), ATOL)
+
+
 @pytest.mark.parametrize("V,K,dtype", [(1860, 8, "f32"), (1950, 4, "bf16"), (1983, 8, "bf16"),
                                        (1856, 2, "f32")])
 def test_beam_rows_of_30_and_31_chunks(V, K, dtype):
