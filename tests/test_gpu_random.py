@@ -1,0 +1,88 @@
+"""Seeded random configurations through the automatic kernel choice, against
+the oracle: vocabulary sizes on both sides of every dispatch boundary (one
+token, one wave, 2048 logits, wide rows), beams of 1 to 12 hypotheses, any
+chunk length, fp32 and bf16, empty and nested lists, unbiased streams, and
+phrases planted in the logits so that states go deep. Greedy, plain beam and
+streaming beam, every stream compared element by element."""
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from tests.gpu_cases import compare_beam, compare_greedy, gpu_beam, gpu_greedy, say
+from workloads.synth import _f32_to_bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+ATOL = 1e-5
+N_CASES = 120
+
+
+def _case(seed):
+    rng = np.random.default_rng(7000 + seed)
+    V = int(rng.choice([1, 2, 5, 63, 64, 65, 200, 1023, 1024, 2047, 2048, 2600, 4200]))
+    K = int(rng.choice([1, 1, 2, 3, 4, 5, 8, 12]))
+    K = min(K, V + 1)
+    T = int(rng.integers(1, 49))
+    cfg = W.Config(7000 + seed, "random", B=int(rng.integers(1, 7)), K=K, V=V, T=T,
+                   chunk=int(rng.integers(1, T + 1)), dtype=str(rng.choice(["f32", "bf16"])),
+                   n_phrases=int(rng.integers(1, 60)), len_lo=1, len_hi=int(rng.integers(1, 9)),
+                   token_dist=str(rng.choice(["uniform", "zipf"])), zipf_s=1.1,
+                   logit_std=float(rng.choice([0.5, 1.0, 2.0])),
+                   blank_offset=float(rng.choice([0.0, 1.0])), n_case=int(rng.integers(0, V // 3 + 1)))
+    lists = [list(lst) for lst in W.phrases(cfg)]
+    lists[0].append(lists[0][0][:1])  # a nested (or repeated) phrase
+    for b in range(1, cfg.B):
+        if rng.random() < 0.15:
+            lists[b] = []  # an empty list: root only, no biasing
+    mids = np.arange(cfg.B, dtype=np.int32)
+    mids[rng.random(cfg.B) < 0.2] = -1
+    rows = W.logits(cfg.__class__(**{**cfg.__dict__, "dtype": "f32"}))
+    for b in range(cfg.B):
+        if mids[b] < 0 or not len(lists[b]):
+            continue
+        t = int(rng.integers(0, 3))
+        while True:
+            ph = lists[b][int(rng.integers(len(lists[b])))]
+            if t + len(ph) > T:
+                break
+            for i, v in enumerate(ph):
+                rows[t + i, b, :, int(v)] += np.float32(4.0)
+            t += len(ph) + int(rng.integers(0, 4))
+    if cfg.dtype == "bf16":
+        rows = _f32_to_bf16_bits(rows)
+    return cfg, lists, mids, np.ascontiguousarray(rows), str(rng.choice(["plain", "stream"]))
+
+
+@pytest.mark.parametrize("seed", range(N_CASES))
+def test_random_configuration(seed):
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg, lists, mids, rows, beam_kind = _case(seed)
+    cm = W.class_map(cfg)
+    dec = BoostDecoder(lists, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    graphs = {int(m): oracle.build_graph(lists[m], cm, token_w=cfg.token_w,
+                                         end_bonus=cfg.end_bonus)
+              for m in set(mids.tolist()) if m >= 0}
+    kind = "greedy" if cfg.K == 1 else beam_kind
+    say(f"[random {seed}] {kind} V+1={cfg.Vp1} K={cfg.K} B={cfg.B} T={cfg.T} chunk={cfg.chunk} "
+        f"{cfg.dtype} phrases={cfg.n_phrases}")
+    if cfg.K == 1:
+        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, cfg.chunk)
+        st0 = np.where(mids >= 0, 0, -1).astype(np.int32)
+        ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :], st0)
+        compare_greedy(gpu, ref, range(cfg.B), ATOL)
+    elif kind == "plain":
+        gpu = gpu_beam(dec, to_device_logits(rows), mids, cfg.chunk)
+        st0, S0 = oracle.init_carry(mids, cfg.K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(cfg.B), ATOL)
+    else:
+        rows_dev = to_device_logits(rows)
+        carry = dec.start_beam_stream(mids, cfg.K, 64)
+        want = oracle.init_stream_carry(mids, cfg.K)
+        for t0 in range(0, cfg.T, cfg.chunk):
+            got = [o.cpu().numpy() for o in dec.beam_stream(rows_dev[t0:t0 + cfg.chunk], carry)]
+            exp = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + cfg.chunk], want,
+                                            tree_cap=64)
+            compare_beam(got, exp, range(cfg.B), ATOL)
