@@ -1,8 +1,9 @@
 """Seeded random configurations through the automatic kernel choice, against
 the oracle: vocabulary sizes on both sides of every dispatch boundary (one
 token, one wave, 2048 logits, wide rows), beams of 1 to 12 hypotheses, any
-chunk length, fp32 and bf16, empty and nested lists, unbiased streams, and
-phrases planted in the logits so that states go deep. Greedy, plain beam and
+chunk length, fp32 and bf16, empty and nested lists, unbiased streams, rows
+farther apart than V+1, and phrases planted in the logits so that states go
+deep. Greedy, plain beam and
 streaming beam, every stream compared element by element."""
 
 import numpy as np
@@ -52,13 +53,29 @@ def _case(seed):
             t += len(ph) + int(rng.integers(0, 4))
     if cfg.dtype == "bf16":
         rows = _f32_to_bf16_bits(rows)
-    return cfg, lists, mids, np.ascontiguousarray(rows), str(rng.choice(["plain", "stream"]))
+    pad = int(rng.choice([0, 0, 1, 5, 64]))  # row stride V+1+pad
+    return (cfg, lists, mids, np.ascontiguousarray(rows), str(rng.choice(["plain", "stream"])),
+            pad)
+
+
+def _device_rows(rows, pad):
+    """rows on the device, each row followed by pad values of 1e30 that no
+    kernel may read."""
+    import torch
+    from paper_2608_21343_amd.decoder import to_device_logits
+    dev = to_device_logits(rows)
+    if pad == 0:
+        return dev
+    full = torch.empty(dev.shape[:-1] + (dev.shape[-1] + pad,), dtype=dev.dtype, device=dev.device)
+    full.fill_(1e30)
+    full[..., :dev.shape[-1]] = dev
+    return full[..., :dev.shape[-1]]
 
 
 @pytest.mark.parametrize("seed", range(N_CASES))
 def test_random_configuration(seed):
-    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
-    cfg, lists, mids, rows, beam_kind = _case(seed)
+    from paper_2608_21343_amd.decoder import BoostDecoder
+    cfg, lists, mids, rows, beam_kind, pad = _case(seed)
     cm = W.class_map(cfg)
     dec = BoostDecoder(lists, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
     graphs = {int(m): oracle.build_graph(lists[m], cm, token_w=cfg.token_w,
@@ -66,19 +83,19 @@ def test_random_configuration(seed):
               for m in set(mids.tolist()) if m >= 0}
     kind = "greedy" if cfg.K == 1 else beam_kind
     say(f"[random {seed}] {kind} V+1={cfg.Vp1} K={cfg.K} B={cfg.B} T={cfg.T} chunk={cfg.chunk} "
-        f"{cfg.dtype} phrases={cfg.n_phrases}")
+        f"{cfg.dtype} phrases={cfg.n_phrases} pad={pad}")
     if cfg.K == 1:
-        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, cfg.chunk)
+        gpu = gpu_greedy(dec, _device_rows(rows, pad)[:, :, 0, :], mids, cfg.chunk)
         st0 = np.where(mids >= 0, 0, -1).astype(np.int32)
         ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :], st0)
         compare_greedy(gpu, ref, range(cfg.B), ATOL)
     elif kind == "plain":
-        gpu = gpu_beam(dec, to_device_logits(rows), mids, cfg.chunk)
+        gpu = gpu_beam(dec, _device_rows(rows, pad), mids, cfg.chunk)
         st0, S0 = oracle.init_carry(mids, cfg.K)
         ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
         compare_beam(gpu, ref, range(cfg.B), ATOL)
     else:
-        rows_dev = to_device_logits(rows)
+        rows_dev = _device_rows(rows, pad)
         carry = dec.start_beam_stream(mids, cfg.K, 64)
         want = oracle.init_stream_carry(mids, cfg.K)
         for t0 in range(0, cfg.T, cfg.chunk):
