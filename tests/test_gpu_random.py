@@ -103,3 +103,58 @@ def test_random_configuration(seed):
             exp = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + cfg.chunk], want,
                                             tree_cap=64)
             compare_beam(got, exp, range(cfg.B), ATOL)
+
+
+def _variative_case(seed):
+    import workloads.pieces as WP
+    rng = np.random.default_rng(9000 + seed)
+    K = int(rng.choice([1, 1, 2, 4, 8]))
+    T = int(rng.integers(1, 41))
+    cfg = WP.piece_config("variative_small", index=9000 + seed, B=int(rng.integers(1, 6)), K=K,
+                          V=int(rng.choice([WP.N_CHARS, 120, 400, 1100, 2100])), T=T,
+                          chunk=int(rng.integers(1, T + 1)), dtype=str(rng.choice(["f32", "bf16"])),
+                          n_phrases=int(rng.integers(1, 25)), n_lexicon=600,
+                          tau=float(rng.choice([0.0, 1.0, 2.0])))
+    return cfg, int(rng.integers(0, 2)), str(rng.choice(["plain", "stream"]))
+
+
+@pytest.mark.parametrize("seed", range(N_CASES // 4))
+def test_random_variative_configuration(seed):
+    """Variative BPE graphs (lists in characters over a piece vocabulary,
+    Eq. (1) potentials, both readings of the potentials) in random
+    configurations, against the oracle's variative graph."""
+    import workloads.pieces as WP
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg, semantics, beam_kind = _variative_case(seed)
+    toks, lists, rows = WP.vocab(cfg), WP.phrases(cfg), WP.logits(cfg)
+    mids = np.arange(cfg.B, dtype=np.int32)
+    if cfg.B > 1:
+        mids[-1] = -1
+    kind = "greedy" if cfg.K == 1 else beam_kind
+    say(f"[random variative {seed}] {kind} pieces={cfg.V} K={cfg.K} B={cfg.B} T={cfg.T} "
+        f"chunk={cfg.chunk} {cfg.dtype} tau={cfg.tau} semantics={semantics}")
+    dec = BoostDecoder.variative(lists, toks, WP.LOWER, cfg.tau, token_w=cfg.token_w,
+                                 end_bonus=cfg.end_bonus, semantics=semantics)
+    graphs = {int(m): oracle.build_variative_graph(toks, WP.LOWER, lists[int(m)],
+                                                   token_w=cfg.token_w, end_bonus=cfg.end_bonus,
+                                                   tau=cfg.tau, semantics=semantics)
+              for m in set(mids.tolist()) if m >= 0}
+    if cfg.K == 1:
+        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, cfg.chunk)
+        st0 = np.where(mids >= 0, 0, -1).astype(np.int32)
+        ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :], st0)
+        compare_greedy(gpu, ref, range(cfg.B), ATOL)
+    elif kind == "plain":
+        gpu = gpu_beam(dec, to_device_logits(rows), mids, cfg.chunk)
+        st0, S0 = oracle.init_carry(mids, cfg.K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(cfg.B), ATOL)
+    else:
+        rows_dev = to_device_logits(rows)
+        carry = dec.start_beam_stream(mids, cfg.K, 64)
+        want = oracle.init_stream_carry(mids, cfg.K)
+        for t0 in range(0, cfg.T, cfg.chunk):
+            got = [o.cpu().numpy() for o in dec.beam_stream(rows_dev[t0:t0 + cfg.chunk], carry)]
+            exp = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + cfg.chunk], want,
+                                            tree_cap=64)
+            compare_beam(got, exp, range(cfg.B), ATOL)
