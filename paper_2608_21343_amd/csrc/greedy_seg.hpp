@@ -290,7 +290,8 @@ struct SGraphT {
     if (x < nhot) {
       const uint32_t a0 = w0[x], c0 = w2[x];
       const uint32_t c = __builtin_amdgcn_readfirstlane(c0);
-      if (!(c >> 31)) return vpsi[__builtin_amdgcn_readfirstlane(a0) >> 24];
+      // the value index is the record's top byte: an unsigned shift
+      if (!(c >> 31)) return vpsi[(uint32_t)__builtin_amdgcn_readfirstlane(a0) >> 24];
     }
     return sload(A->psi + off + x);
   }
