@@ -1,7 +1,8 @@
 """Seeded random configurations through the automatic kernel choice, against
 the oracle: vocabulary sizes on both sides of every dispatch boundary (one
 token, one wave, 2048 logits, wide rows), beams of 1 to 12 hypotheses, any
-chunk length, fp32 and bf16, empty and nested lists, unbiased streams, rows
+chunk length, fp32 and bf16, case classes of three or five members, empty
+and nested lists, unbiased streams, rows
 farther apart than V+1, and phrases planted in the logits so that states go
 deep. Greedy, plain beam and
 streaming beam, every stream compared element by element."""
@@ -54,8 +55,16 @@ def _case(seed):
     if cfg.dtype == "bf16":
         rows = _f32_to_bf16_bits(rows)
     pad = int(rng.choice([0, 0, 1, 5, 64]))  # row stride V+1+pad
+    cm = W.class_map(cfg)
+    if V >= 10 and rng.random() < 0.3:
+        # classes of five members (more than an arc record holds inline)
+        n5 = int(rng.integers(1, V // 5 + 1))
+        cm = np.arange(V + 1, dtype=np.int32)
+        for k in range(1, 5):
+            cm[k * n5:(k + 1) * n5] = np.arange(n5)
+        cm[V] = -1
     return (cfg, lists, mids, np.ascontiguousarray(rows), str(rng.choice(["plain", "stream"])),
-            pad)
+            pad, cm)
 
 
 def _device_rows(rows, pad):
@@ -75,8 +84,7 @@ def _device_rows(rows, pad):
 @pytest.mark.parametrize("seed", range(N_CASES))
 def test_random_configuration(seed):
     from paper_2608_21343_amd.decoder import BoostDecoder
-    cfg, lists, mids, rows, beam_kind, pad = _case(seed)
-    cm = W.class_map(cfg)
+    cfg, lists, mids, rows, beam_kind, pad, cm = _case(seed)
     dec = BoostDecoder(lists, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
     graphs = {int(m): oracle.build_graph(lists[m], cm, token_w=cfg.token_w,
                                          end_bonus=cfg.end_bonus)
