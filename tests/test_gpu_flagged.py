@@ -26,11 +26,13 @@ ATOL = 1e-5
 LONG = 300  # tokens of the long phrase (model 1)
 
 
-def _lists(V, fan_out=True):
+def _lists(V, fan=300):
     rng = np.random.default_rng(11)
-    # state (1, 2): 300 children (without it, the largest override set fits
-    # the one-wave-per-hypothesis beam kernel's lists)
-    fan = [[1, 2, 3 + i] for i in range(300 if fan_out else 30)]
+    # state (1, 2) with fan children: 300 is more than its record holds; 250
+    # fills most of the beam kernel's override list (256) and, in the
+    # short-call kernel's far-record instance, four children per lane; 30 is
+    # an ordinary state
+    fan = [[1, 2, 3 + i] for i in range(fan)]
     long = [[4 + (i % (V - 8)) for i in range(LONG)]]           # depths up to 300
     big = {tuple(int(t) for t in rng.integers(0, V, size=10)) for _ in range(7200)}
     big = [list(p) for p in sorted(big)]                        # about 70 k states
@@ -61,16 +63,16 @@ def _rows(V, T, K, lists, big_graph, seed):
 _CACHE = {}
 
 
-def _setup(V, fan_out=True):
+def _setup(V, fan=300):
     from paper_2608_21343_amd.decoder import BoostDecoder
-    if (V, fan_out) not in _CACHE:
+    if (V, fan) not in _CACHE:
         cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
-        lists = _lists(V, fan_out)
+        lists = _lists(V, fan)
         dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
         graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0)
                   for m, l in enumerate(lists)}
-        _CACHE[(V, fan_out)] = (cm, lists, dec, graphs)
-    return _CACHE[(V, fan_out)]
+        _CACHE[(V, fan)] = (cm, lists, dec, graphs)
+    return _CACHE[(V, fan)]
 
 
 def test_records_are_flagged_where_expected():
@@ -91,34 +93,35 @@ BEAM_KERNEL = {"default": capi.BEAM_AUTO, "wide": capi.BEAM_NO_PIPE, "ref": capi
 T_STEPS = 320
 
 
-@pytest.mark.parametrize("kernel,V,chunk", [("default", 1024, 16), ("default", 1024, 320),
-                                            ("default", 2600, 16), ("default", 2600, 320),
-                                            ("ref", 1024, 16)])
-def test_greedy_through_flagged_records(kernel, V, chunk, restore_kernels):
+@pytest.mark.parametrize("kernel,V,chunk,fan", [("default", 1024, 16, 300), ("default", 1024, 320, 300),
+                                                ("default", 2600, 16, 300), ("default", 2600, 320, 300),
+                                                ("ref", 1024, 16, 300), ("default", 1024, 16, 250),
+                                                ("default", 1024, 320, 250)])
+def test_greedy_through_flagged_records(kernel, V, chunk, fan, restore_kernels):
     from paper_2608_21343_amd.decoder import to_device_logits
     capi.tb_debug_select_kernels(greedy=GREEDY_KERNEL[kernel])
-    cm, lists, dec, graphs = _setup(V)
+    cm, lists, dec, graphs = _setup(V, fan)
     rows = _rows(V, T_STEPS, 1, lists, graphs[2], 3)
     mids = np.arange(4, dtype=np.int32)
-    say(f"[flagged] greedy {kernel} V+1={V + 1} chunk={chunk}")
+    say(f"[flagged] greedy {kernel} V+1={V + 1} chunk={chunk} fan-out={fan}")
     gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, chunk)
     ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :], np.zeros(4, np.int32))
     compare_greedy(gpu, ref, range(4), ATOL)
     assert ref[1][:, 1].max() >= 290 and ref[1][:, 2].max() >= 65536
 
 
-@pytest.mark.parametrize("kernel,V,K,fan_out", [("default", 1024, 4, True), ("default", 1024, 8, True),
-                                                ("ref", 1024, 4, True), ("default", 2600, 4, True),
-                                                ("wide", 2600, 4, True), ("default", 1024, 4, False),
-                                                ("default", 1024, 8, False),
-                                                ("default", 2600, 4, False)])
-def test_beam_through_flagged_records(kernel, V, K, fan_out, restore_kernels):
+@pytest.mark.parametrize("kernel,V,K,fan", [("default", 1024, 4, 300), ("default", 1024, 8, 300),
+                                            ("ref", 1024, 4, 300), ("default", 2600, 4, 300),
+                                            ("wide", 2600, 4, 300), ("default", 1024, 4, 30),
+                                            ("default", 1024, 8, 30), ("default", 2600, 4, 30),
+                                            ("default", 1024, 4, 250), ("default", 1024, 8, 250)])
+def test_beam_through_flagged_records(kernel, V, K, fan, restore_kernels):
     from paper_2608_21343_amd.decoder import to_device_logits
     capi.tb_debug_select_kernels(beam=BEAM_KERNEL[kernel])
-    cm, lists, dec, graphs = _setup(V, fan_out)
+    cm, lists, dec, graphs = _setup(V, fan)
     rows = _rows(V, T_STEPS, K, lists, graphs[2], 4)
     mids = np.arange(4, dtype=np.int32)
-    say(f"[flagged] beam {kernel} V+1={V + 1} K={K} fan-out={fan_out}")
+    say(f"[flagged] beam {kernel} V+1={V + 1} K={K} fan-out={fan}")
     gpu = gpu_beam(dec, to_device_logits(rows), mids, 80)
     st0, S0 = oracle.init_carry(mids, K)
     ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
@@ -130,7 +133,7 @@ def test_streaming_beam_through_flagged_records(K):
     """The streaming beam's merges take the psi of the merged state (a state
     of the long phrase, whose value index exceeds 127)."""
     from paper_2608_21343_amd.decoder import to_device_logits
-    cm, lists, dec, graphs = _setup(1024, False)
+    cm, lists, dec, graphs = _setup(1024, 30)
     rows = _rows(1024, T_STEPS, K, lists, graphs[2], 5)
     mids = np.arange(4, dtype=np.int32)
     say(f"[flagged] streaming beam K={K}")
