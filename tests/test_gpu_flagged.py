@@ -144,3 +144,30 @@ def test_streaming_beam_through_flagged_records(K):
         got = [o.cpu().numpy() for o in dec.beam_stream(rows_dev[t0:t0 + 80], carry)]
         exp = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + 80], want, tree_cap=4096)
         compare_beam(got, exp, range(4), ATOL)
+
+
+@pytest.mark.parametrize("chunk", [16, 320])
+def test_greedy_wide_fan_out_in_small_models(chunk):
+    """States with 100 and 200 children in models that fit the short-call
+    kernel's LDS (its instance without far records: chains of 65 to 128
+    children two per lane, larger ones level by level)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V = 1024
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    lists = [[[1, 2, 3 + i] for i in range(100)], [[1, 2, 3 + i] for i in range(200)],
+             [[5, 6, 7], [6, 7]], [[1, 2, 3 + i] for i in range(70)] + [[2, 3 + i] for i in range(60)]]
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    rng = np.random.default_rng(21)
+    T = 320
+    rows = rng.normal(0.0, 0.3, size=(T, 4, V + 1)).astype(np.float32)
+    rows[..., V] += 0.5
+    for b in range(4):
+        seq = [v for i in range(T) for v in lists[b][(11 * i + b) % len(lists[b])]]
+        for t, v in enumerate(seq[:T]):
+            rows[t, b, int(v)] += 6.0
+    mids = np.arange(4, dtype=np.int32)
+    say(f"[flagged] greedy wide fan-out, small models, chunk={chunk}")
+    gpu = gpu_greedy(dec, to_device_logits(rows), mids, chunk)
+    ref = oracle.greedy_decode(graphs, mids, rows, np.zeros(4, np.int32))
+    compare_greedy(gpu, ref, range(4), ATOL)
