@@ -171,3 +171,38 @@ def test_greedy_wide_fan_out_in_small_models(chunk):
     gpu = gpu_greedy(dec, to_device_logits(rows), mids, chunk)
     ref = oracle.greedy_decode(graphs, mids, rows, np.zeros(4, np.int32))
     compare_greedy(gpu, ref, range(4), ATOL)
+
+
+@pytest.mark.parametrize("K,chunk", [(1, 16), (1, 320), (4, 80), (8, 80)])
+def test_suffix_chains_of_twenty_states(K, chunk):
+    """A 24-token phrase listed with every one of its suffixes: deep in the
+    phrase a state's suffix chain has up to 24 states with children, far
+    beyond the chains the fast paths walk at once (the rest go level by
+    level)."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    V = 300
+    cm = np.concatenate([np.arange(V), [-1]]).astype(np.int32)
+    ph = [10 + (7 * i) % 250 for i in range(24)]
+    lists = [[ph[i:] for i in range(24)], [ph[i:] for i in range(0, 24, 3)] + [ph[:5]],
+             [ph], [[5, 6, 7]]]
+    dec = BoostDecoder(lists, cm, token_w=1.0, end_bonus=2.0)
+    graphs = {m: oracle.build_graph(l, cm, token_w=1.0, end_bonus=2.0) for m, l in enumerate(lists)}
+    rng = np.random.default_rng(31)
+    T = 320
+    rows = rng.normal(0.0, 0.3, size=(T, 4, K, V + 1)).astype(np.float32)
+    rows[..., V] += 0.5
+    for b in range(4):
+        for t in range(T):
+            rows[t, b, :, ph[(t + 3 * b) % 24]] += 6.0
+    mids = np.arange(4, dtype=np.int32)
+    say(f"[flagged] suffix chains K={K} chunk={chunk}")
+    if K == 1:
+        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, chunk)
+        ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :], np.zeros(4, np.int32))
+        compare_greedy(gpu, ref, range(4), ATOL)
+        assert ref[1][:, 0].max() >= 20
+    else:
+        gpu = gpu_beam(dec, to_device_logits(rows), mids, chunk)
+        st0, S0 = oracle.init_carry(mids, K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(4), ATOL)
