@@ -166,3 +166,41 @@ def test_random_variative_configuration(seed):
             exp = oracle.beam_decode_stream(graphs, mids, rows[t0:t0 + cfg.chunk], want,
                                             tree_cap=64)
             compare_beam(got, exp, range(cfg.B), ATOL)
+
+
+@pytest.mark.parametrize("K,chunk", [(1, 16), (1, 40), (3, 40)])
+def test_many_streams(K, chunk):
+    """700 streams (more workgroups than CUs; one segment per stream in long
+    greedy calls), 70 models shared by the streams, against the oracle."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg = W.Config(7500 + K, "many", B=70, K=K, V=64, T=40, chunk=chunk, dtype="f32",
+                   n_phrases=30, len_lo=1, len_hi=5, token_dist="zipf", zipf_s=1.1,
+                   logit_std=1.0, blank_offset=0.5, n_case=10)
+    lists = W.phrases(cfg)
+    cm = W.class_map(cfg)
+    B = 700
+    rng = np.random.default_rng(7600 + K)
+    mids = rng.integers(-1, 70, size=B).astype(np.int32)
+    rows = rng.normal(0.0, 1.0, size=(40, B, K, 65)).astype(np.float32)
+    for b in range(B):
+        if mids[b] >= 0:
+            ph = lists[mids[b]][int(rng.integers(len(lists[mids[b]])))]
+            t0 = int(rng.integers(0, 30))
+            for i, v in enumerate(ph):
+                if t0 + i < 40:
+                    rows[t0 + i, b, :, int(v)] += 4.0
+    dec = BoostDecoder(lists, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    graphs = {int(m): oracle.build_graph(lists[m], cm, token_w=cfg.token_w,
+                                         end_bonus=cfg.end_bonus)
+              for m in set(mids.tolist()) if m >= 0}
+    say(f"[many streams] B={B} K={K} chunk={chunk}")
+    if K == 1:
+        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, chunk)
+        ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :],
+                                   np.where(mids >= 0, 0, -1).astype(np.int32))
+        compare_greedy(gpu, ref, range(B), ATOL)
+    else:
+        gpu = gpu_beam(dec, to_device_logits(rows), mids, chunk)
+        st0, S0 = oracle.init_carry(mids, K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(B), ATOL)
