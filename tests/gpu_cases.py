@@ -141,6 +141,16 @@ def gpu_beam(dec, rows_dev, model_ids, chunk: int):
     return tuple(o.cpu().numpy() for o in outs) + (states.cpu().numpy(), scores.cpu().numpy())
 
 
+def _score_error(a, b) -> float:
+    """Largest |a - b| over the entries that differ (equal entries, infinite
+    ones included, count 0; a NaN on either side counts as an error)."""
+    if a.size == 0:
+        return 0.0
+    with np.errstate(invalid="ignore"):
+        d = np.where(a == b, 0.0, np.abs(a.astype(np.float64) - b.astype(np.float64)))
+    return float(np.nanmax(d)) if not np.isnan(d).any() else float("nan")
+
+
 def compare_greedy(gpu, ref, streams, atol=1e-5, ref_streams=None):
     """gpu[i][:, streams] against ref[i][:, ref_streams] (default: the same columns)."""
     s = list(streams)
@@ -150,7 +160,7 @@ def compare_greedy(gpu, ref, streams, atol=1e-5, ref_streams=None):
     bad = np.nonzero(tok != rtok)
     assert bad[0].size == 0, f"token mismatch at (t, stream-index) {list(zip(*bad))[:5]}"
     assert np.array_equal(st, rst), "state mismatch"
-    err = float(np.max(np.abs(sc - rsc))) if sc.size else 0.0
+    err = _score_error(sc, rsc)
     assert err <= atol, f"score error {err}"
     return err
 
@@ -162,6 +172,6 @@ def compare_beam(gpu, ref, streams, atol=1e-5, ref_streams=None):
         bad = np.nonzero(gpu[i][:, s] != ref[i][:, r])
         assert bad[0].size == 0, f"{n} mismatch at {list(zip(*bad))[:5]}"
     assert np.array_equal(gpu[4][:, s], ref[4][:, r]), "accumulated score not bit-exact"
-    err = float(np.max(np.abs(gpu[3][:, s] - ref[3][:, r])))
+    err = _score_error(gpu[3][:, s], ref[3][:, r])
     assert err <= atol, f"step score error {err}"
     return err

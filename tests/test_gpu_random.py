@@ -204,3 +204,49 @@ def test_many_streams(K, chunk):
         st0, S0 = oracle.init_carry(mids, K)
         ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
         compare_beam(gpu, ref, range(B), ATOL)
+
+
+@pytest.mark.parametrize("V,K,dtype", [(300, 1, "f32"), (300, 1, "bf16"), (300, 4, "f32"),
+                                       (300, 8, "bf16"), (2600, 1, "f32"), (2600, 4, "bf16")])
+def test_masked_logits(V, K, dtype):
+    """Rows with -inf logits (masked tokens): about a third of every row, and
+    rows where only the blank and one or two tokens are finite."""
+    from paper_2608_21343_amd.decoder import BoostDecoder, to_device_logits
+    cfg = W.Config(7700 + V + K, "masked", B=5, K=K, V=V, T=48, chunk=16, dtype="f32",
+                   n_phrases=40, len_lo=1, len_hi=5, token_dist="zipf", zipf_s=1.1,
+                   logit_std=1.0, blank_offset=0.5, n_case=V // 10)
+    lists = W.phrases(cfg)
+    cm = W.class_map(cfg)
+    rng = np.random.default_rng(7800 + V + K)
+    rows = W.logits(cfg)
+    mask = rng.random(rows.shape) < 0.33
+    mask[..., V] = False
+    sparse = rng.random(rows.shape[:3]) < 0.15
+    keep = rng.integers(0, V, size=rows.shape[:3] + (2,))
+    for idx in zip(*np.nonzero(sparse)):
+        mask[idx] = True
+        mask[idx][keep[idx]] = False
+        mask[idx][V] = False
+    rows[mask] = -np.inf
+    for b in range(5):  # planted phrases stay finite
+        ph = lists[b][0]
+        for i, v in enumerate(ph):
+            rows[10 + i, b, :, int(v)] = 6.0
+    if dtype == "bf16":
+        rows = _f32_to_bf16_bits(rows)
+    rows = np.ascontiguousarray(rows)
+    mids = np.array([0, 1, 2, -1, 4], np.int32)
+    dec = BoostDecoder(lists, cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+    graphs = {m: oracle.build_graph(lists[m], cm, token_w=cfg.token_w, end_bonus=cfg.end_bonus)
+              for m in (0, 1, 2, 4)}
+    say(f"[masked] V+1={V + 1} K={K} {dtype}")
+    if K == 1:
+        gpu = gpu_greedy(dec, to_device_logits(rows[:, :, 0, :]), mids, 16)
+        ref = oracle.greedy_decode(graphs, mids, rows[:, :, 0, :],
+                                   np.where(mids >= 0, 0, -1).astype(np.int32))
+        compare_greedy(gpu, ref, range(5), ATOL)
+    else:
+        gpu = gpu_beam(dec, to_device_logits(rows), mids, 16)
+        st0, S0 = oracle.init_carry(mids, K)
+        ref = oracle.beam_decode(graphs, mids, rows, st0, S0)
+        compare_beam(gpu, ref, range(5), ATOL)
